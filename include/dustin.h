@@ -1,0 +1,203 @@
+/*
+ * dustin.h -- C ABI of libdustin, the MI355X (gfx950) hot path of Dustin's sparse
+ * verification step for long-context speculative decoding.
+ *
+ * One verification step is
+ *   1. dustin_score  (target)           S_T = init_T + sum of scoring-head attention      Eq. 5
+ *   2. dustin_score  (draft, per layer) S_D = init_D + sum over draft heads, layers, tokens Eq. 5
+ *   3. dustin_topk                      I   = sinks U window U top-m(S_D) U top-rest(S_T)   Eq. 6
+ *   4. dustin_sparse_verify_attn        attention of the gamma+1 verification queries over
+ *                                       I plus the causal verification window, run for
+ *                                       every target layer with the same I (global,
+ *                                       layer-invariant selection, method section 4.1)
+ * and dense_verify_attn is the full-cache verification attention the paper compares
+ * against (Efficiency baselines; Appendix G).
+ *
+ * Conventions shared by every entry point
+ *   - All tensor pointers are DEVICE pointers unless a name ends in _host.  The caller
+ *     owns every buffer; the library never allocates, frees or synchronises.  Work is
+ *     enqueued on `stream` (a hipStream_t; NULL = the null stream) and is asynchronous.
+ *   - Strides are in elements, int64.  The innermost axis (head_dim or position) must be
+ *     contiguous (stride 1).  bf16 means the 16-bit bfloat16 format.
+ *   - Base pointers of bf16 tensors and their strides must keep 16-byte alignment of
+ *     every row (a multiple of 8 elements); fp32/int32 tensors need 4-byte alignment.
+ *   - Arguments are validated on the host before anything is enqueued; a non-OK status
+ *     means nothing was enqueued and no output was touched.  Per-sequence values that
+ *     live in device arrays (lengths, query counts, budgets, m, selected positions, page
+ *     ids) cannot be checked on the host: kernels clamp them into the host-declared
+ *     bounds (N_b into [0, max_len], T_b into [0, nq_max], k_b into
+ *     [n_sink + n_window, k_max], m_b into [0, k_b - n_sink - n_window], positions into
+ *     the cache capacity, page ids into [0, num_pages)), so no device value can make a
+ *     kernel read or write outside the buffers the host arguments describe.
+ *   - Verification tokens: sequence b has N_b committed positions [0, N_b) and T_b
+ *     verification tokens (the last accepted token plus gamma_b drafts) whose K/V rows
+ *     are already written at positions [N_b, N_b + T_b).  Query t in [0, T_b) attends
+ *     to the selected positions plus N_b .. N_b + t (causal).  The verification tokens
+ *     are not counted in the budget k.
+ *   - GQA: query head h uses KV head h / (num_q_heads / num_kv_heads).
+ *   - Selection groups: groups == 1 gives one index set per sequence (the paper's
+ *     global set); groups == num_kv_heads gives one set per (sequence, KV head).
+ *   - No exception or C++ object crosses this boundary; every function is reentrant.
+ */
+#ifndef DUSTIN_H
+#define DUSTIN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  DUSTIN_OK = 0,
+  DUSTIN_ERR_INVALID_ARG = 1, /* null pointer, bad size, bad stride or alignment         */
+  DUSTIN_ERR_UNSUPPORTED = 2, /* valid but not implemented (head_dim, rows per group...) */
+  DUSTIN_ERR_WORKSPACE = 3,   /* workspace missing, misaligned or smaller than required   */
+  DUSTIN_ERR_LAUNCH = 4       /* the HIP runtime refused a launch                          */
+} dustin_status;
+
+/* A bf16 K or V cache of one layer.
+ *   contiguous (page_table == NULL): element (b, n, g, c) is at
+ *       data[b * stride_b + n * stride_n + g * stride_h + c],  n < capacity
+ *   paged: position n of sequence b lives in physical page p = page_table[b * max_pages +
+ *       n / page_size] at data[p * stride_page + (n % page_size) * stride_n + g * stride_h + c];
+ *       capacity = max_pages * page_size, p < num_pages. */
+typedef struct {
+  const void* data;
+  int32_t num_kv_heads;
+  int32_t head_dim;
+  int64_t stride_b;
+  int64_t stride_n;
+  int64_t stride_h;
+  int64_t capacity;            /* positions addressable per sequence (contiguous mode) */
+  const int32_t* page_table;   /* NULL = contiguous; else device int32 [B, max_pages]  */
+  int32_t page_size;           /* paged: a power of two                                */
+  int32_t max_pages;
+  int32_t num_pages;           /* paged: physical pages in the pool                    */
+  int64_t stride_page;
+} dustin_kv;
+
+/* Per-sequence sizes.  A NULL device array means "the scalar for every sequence". */
+typedef struct {
+  int32_t batch;               /* B                                                    */
+  int32_t max_len;             /* upper bound of N_b                                   */
+  int32_t nq_max;              /* upper bound of T_b (attention) or Gamma_b (score)    */
+  int32_t k_max;               /* upper bound of the budget k_b (selection, sparse)    */
+  const int32_t* seq_lens;     /* device int32 [B]: N_b (required)                     */
+  const int32_t* n_query;      /* device int32 [B] or NULL (= nq_max)                  */
+  const int32_t* budget;       /* device int32 [B] or NULL (= k_max)                   */
+  const int32_t* m;            /* device int32 [B] or NULL (= m_scalar)                */
+  int32_t m_scalar;
+} dustin_batch;
+
+/* Human-readable name of a status code (static storage). */
+const char* dustin_status_string(dustin_status status);
+
+/* Library version, (major << 16) | minor. */
+int32_t dustin_version(void);
+
+/* ---------------------------------------------------------------------------------
+ * dustin_score -- scoring-head importance, Eq. 5 (hybrid_importance) restricted to the
+ * semantic retrieval heads (online sparse estimation, method section 4.2; Appendix A).
+ *
+ *   out[b, go, n] = init[b, go, n]
+ *                 + sum_{h in heads, (groups == 1 or h's KV head == go)} sum_{j < nq_b}
+ *                   softmax_{n' < N_b}(scale * q[b, j, h] . K[b, n', g(h)])[n]
+ *
+ * for n < N_b; positions n >= N_b of out are not written.  Used once for the target's
+ * last generated token (nq_b = 1, init = the historical score or NULL) and once per draft
+ * scoring layer (nq_b = Gamma_b draft tokens; chaining init = out accumulates layers).
+ *   q        bf16 [B, nq_max, num_q_heads, head_dim], strides q_sb, q_sj, q_sh
+ *   heads_host  host int32 [n_heads], 1 <= n_heads <= 16, distinct, in [0, num_q_heads)
+ *   k        the layer's K cache; head_dim in {64, 128}
+ *   bt       seq_lens, n_query (1 <= nq_max <= 16), max_len
+ *   groups   1 or k->num_kv_heads
+ *   init     fp32 [B, groups, >= max_len] (strides init_sb, init_sg) or NULL (= 0)
+ *   out      fp32 [B, groups, >= max_len] (strides out_sb, out_sg); may alias init
+ *   workspace  device scratch of dustin_score_workspace() bytes, 256-byte aligned
+ * Rounding: fp32 dot products (bf16 products are exact), fp32 exp and sums.
+ * --------------------------------------------------------------------------------- */
+size_t dustin_score_workspace(int32_t batch, int32_t max_len, int32_t nq_max, int32_t n_heads);
+dustin_status dustin_score(const void* q, int64_t q_sb, int64_t q_sj, int64_t q_sh,
+                           int32_t num_q_heads, const int32_t* heads_host, int32_t n_heads,
+                           const dustin_kv* k, const dustin_batch* bt, float scale,
+                           int32_t groups, const float* init, int64_t init_sb, int64_t init_sg,
+                           float* out, int64_t out_sb, int64_t out_sg, void* workspace,
+                           size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------------
+ * dustin_topk -- tiered hybrid selection, Eq. 6 (hybrid_selection), with the protected
+ * set of the experimental setup (n_sink attention sinks and an n_window recent window,
+ * counted inside the budget; Appendix C).  For every (b, go):
+ *   N = N_b, k = k_b, m = m_b, P = [0, n_sink) U [N - n_window, N)
+ *   N <= k : I = [0, N)
+ *   else   : I_D = the m best of [0,N) \ P by S_D
+ *            I_T = the k - m - |P| best of [0,N) \ (P U I_D) by S_T
+ *            I   = P U I_D U I_T
+ *   "best" orders by value descending, then position ascending; values compare as
+ *   numbers with -0 == +0, and NaNs sort beyond +-inf by their sign bit.
+ *   idx[b, go, 0 .. count) = I in ascending order, count[b * groups + go] = |I| = min(k, N).
+ *   Entries idx[b, go, count ..) are not written.
+ *   s_draft / s_target  fp32 [B, G', >= max_len] (strides *_sb, *_sg; *_sg = 0
+ *       broadcasts one vector to every group); either may be NULL: no S_D requires
+ *       m = 0 (target-only, Dustin-T), no S_T requires m = k - |P| (draft-only, Dustin-D)
+ *   bt       seq_lens, budget/k_max, m/m_scalar; 1 <= max_len <= 1 << 20
+ *   groups   1 or the KV head count
+ *   idx      int32 [B, groups, >= k_max] (strides idx_sb, idx_sg), count int32 [B*groups]
+ *   workspace  dustin_topk_workspace() bytes (may be 0 bytes: pass NULL, 0)
+ * The result is a pure function of the fp32 inputs: bit-exact and deterministic.
+ * --------------------------------------------------------------------------------- */
+size_t dustin_topk_workspace(int32_t batch, int32_t groups, int32_t max_len);
+dustin_status dustin_topk(const float* s_draft, int64_t d_sb, int64_t d_sg,
+                          const float* s_target, int64_t t_sb, int64_t t_sg,
+                          const dustin_batch* bt, int32_t groups, int32_t n_sink,
+                          int32_t n_window, int32_t* idx, int64_t idx_sb, int64_t idx_sg,
+                          int32_t* count, void* workspace, size_t workspace_bytes,
+                          void* stream);
+
+/* ---------------------------------------------------------------------------------
+ * dustin_sparse_verify_attn -- verification attention over the selected tokens only
+ * (the compressed target KV cache of method section 4.1, never materialised: rows are
+ * gathered on the fly).  For b, t < T_b, h:
+ *   J = I[b, gi] (gi = g(h) if groups > 1 else 0) followed by N_b .. N_b + t
+ *   out[b, t, h] = sum_{n in J} softmax_J(scale * q[b,t,h] . K[b,n,g(h)]) V[b,n,g(h)]
+ *   q    bf16 [B, nq_max, num_q_heads, 128] (strides q_sb, q_st, q_sh); head_dim 128;
+ *        T_b * num_q_heads / num_kv_heads <= 128 rows per KV head
+ *   k, v the layer's K and V caches (same layout kind); capacity >= max_len + nq_max
+ *   idx  int32 [B, groups, >= k_max] (strides idx_sb, idx_sg) ascending positions < N_b,
+ *        count int32 [B * groups] (as written by dustin_topk)
+ *   out  bf16 [B, nq_max, num_q_heads, 128] (strides o_sb, o_st, o_sh); rows t >= T_b
+ *        are not written.  Round to nearest even.
+ *   workspace  dustin_attn_workspace(..., sparse = 1) bytes, 256-byte aligned, whose
+ *        first 4096 bytes must be zero before the first call (they are zero again
+ *        after every call)
+ * Rounding: bf16 inputs, fp32 MFMA accumulation, fp32 online softmax, probabilities
+ * rounded to bf16 before the value product, bf16 output.
+ * --------------------------------------------------------------------------------- */
+size_t dustin_attn_workspace(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
+                             int32_t nq_max, int32_t max_tokens, int32_t sparse);
+dustin_status dustin_sparse_verify_attn(const void* q, int64_t q_sb, int64_t q_st,
+                                        int64_t q_sh, int32_t num_q_heads, const dustin_kv* k,
+                                        const dustin_kv* v, const dustin_batch* bt,
+                                        const int32_t* idx, int64_t idx_sb, int64_t idx_sg,
+                                        const int32_t* count, int32_t groups, float scale,
+                                        void* out, int64_t o_sb, int64_t o_st, int64_t o_sh,
+                                        void* workspace, size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------------
+ * dense_verify_attn -- full-cache verification attention (the baseline every speedup
+ * in the paper is measured against): as above with J = [0, N_b) followed by
+ * N_b .. N_b + t.  max_tokens for the workspace is max_len.
+ * --------------------------------------------------------------------------------- */
+dustin_status dense_verify_attn(const void* q, int64_t q_sb, int64_t q_st, int64_t q_sh,
+                                int32_t num_q_heads, const dustin_kv* k, const dustin_kv* v,
+                                const dustin_batch* bt, float scale, void* out, int64_t o_sb,
+                                int64_t o_st, int64_t o_sh, void* workspace,
+                                size_t workspace_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DUSTIN_H */

@@ -1,0 +1,317 @@
+"""Python binding of libdustin, the MI355X (gfx950) hot path of Dustin's sparse verification.
+
+Every function here only marshals arguments (torch tensors -> device pointers, strides,
+the current HIP stream) and calls the C ABI declared in include/dustin.h; all arithmetic
+runs in the HIP kernels.  There is no CPU fallback: when libdustin.so is missing or the
+tensors are not on a GPU, the call raises.
+
+Step of one speculative verification (paper: method section 4, Eqs. 5 and 6):
+    s_t = score(q_last, k_layer, seq_lens, target_heads, init=history)       # S_Target
+    s_d = score(q_draft[l], k_draft[l], seq_lens, draft_heads, init=s_d)     # S_Draft, per layer
+    idx, cnt = topk(s_d, s_t, seq_lens, k_max, m_scalar=m)                   # I_verify
+    o[l] = sparse_verify_attn(q[l], k[l], v[l], idx, cnt, seq_lens)          # every layer
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from typing import Optional, Sequence
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libdustin.so")
+
+OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_LAUNCH = range(5)
+
+EXPORTED = ("dustin_status_string", "dustin_version", "dustin_score_workspace", "dustin_score",
+            "dustin_topk_workspace", "dustin_topk", "dustin_attn_workspace",
+            "dustin_sparse_verify_attn", "dense_verify_attn")
+
+
+class DustinError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        super().__init__(f"{what}: {status_string(status)} (status {status})")
+        self.status = status
+
+
+class DustinKV(ctypes.Structure):
+    _fields_ = [("data", ctypes.c_void_p), ("num_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("stride_b", ctypes.c_int64),
+                ("stride_n", ctypes.c_int64), ("stride_h", ctypes.c_int64),
+                ("capacity", ctypes.c_int64), ("page_table", ctypes.c_void_p),
+                ("page_size", ctypes.c_int32), ("max_pages", ctypes.c_int32),
+                ("num_pages", ctypes.c_int32), ("stride_page", ctypes.c_int64)]
+
+
+class DustinBatch(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("max_len", ctypes.c_int32),
+                ("nq_max", ctypes.c_int32), ("k_max", ctypes.c_int32),
+                ("seq_lens", ctypes.c_void_p), ("n_query", ctypes.c_void_p),
+                ("budget", ctypes.c_void_p), ("m", ctypes.c_void_p),
+                ("m_scalar", ctypes.c_int32)]
+
+
+_lib = None
+_i64, _i32, _vp, _sz = ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p, ctypes.c_size_t
+
+
+def lib():
+    """The loaded libdustin.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: build it with "
+                              "`python -c 'import __graft_entry__ as g; g.build()'`")
+        L = ctypes.CDLL(LIB_PATH)
+        P_KV, P_BT = ctypes.POINTER(DustinKV), ctypes.POINTER(DustinBatch)
+        L.dustin_status_string.restype = ctypes.c_char_p
+        L.dustin_status_string.argtypes = [ctypes.c_int]
+        L.dustin_version.restype = _i32
+        L.dustin_score_workspace.restype = _sz
+        L.dustin_score_workspace.argtypes = [_i32, _i32, _i32, _i32]
+        L.dustin_score.restype = ctypes.c_int
+        L.dustin_score.argtypes = [_vp, _i64, _i64, _i64, _i32, _vp, _i32, P_KV, P_BT,
+                                   ctypes.c_float, _i32, _vp, _i64, _i64, _vp, _i64, _i64,
+                                   _vp, _sz, _vp]
+        L.dustin_topk_workspace.restype = _sz
+        L.dustin_topk_workspace.argtypes = [_i32, _i32, _i32]
+        L.dustin_topk.restype = ctypes.c_int
+        L.dustin_topk.argtypes = [_vp, _i64, _i64, _vp, _i64, _i64, P_BT, _i32, _i32, _i32,
+                                  _vp, _i64, _i64, _vp, _vp, _sz, _vp]
+        L.dustin_attn_workspace.restype = _sz
+        L.dustin_attn_workspace.argtypes = [_i32, _i32, _i32, _i32, _i32, _i32]
+        L.dustin_sparse_verify_attn.restype = ctypes.c_int
+        L.dustin_sparse_verify_attn.argtypes = [_vp, _i64, _i64, _i64, _i32, P_KV, P_KV, P_BT,
+                                                _vp, _i64, _i64, _vp, _i32, ctypes.c_float,
+                                                _vp, _i64, _i64, _i64, _vp, _sz, _vp]
+        L.dense_verify_attn.restype = ctypes.c_int
+        L.dense_verify_attn.argtypes = [_vp, _i64, _i64, _i64, _i32, P_KV, P_KV, P_BT,
+                                        ctypes.c_float, _vp, _i64, _i64, _i64, _vp, _sz, _vp]
+        _lib = L
+    return _lib
+
+
+def status_string(status: int) -> str:
+    return lib().dustin_status_string(int(status)).decode()
+
+
+def _check(status: int, what: str):
+    if status != OK:
+        raise DustinError(status, what)
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _on_gpu(*ts):
+    for t in ts:
+        if t is not None and not t.is_cuda:
+            raise ValueError("libdustin runs on the GPU only: every tensor must be on a HIP device")
+
+
+def _i32_dev(x, device) -> Optional[torch.Tensor]:
+    if x is None:
+        return None
+    if isinstance(x, torch.Tensor):
+        if x.dtype != torch.int32 or not x.is_cuda:
+            raise ValueError("per-sequence arrays must be int32 device tensors")
+        return x.contiguous()
+    return torch.tensor(list(x), dtype=torch.int32, device=device)
+
+
+_WS = {}
+
+
+def workspace(nbytes: int, device, tag: str) -> Optional[torch.Tensor]:
+    """A cached, zero-initialised device scratch buffer per (device, tag) of at least
+    nbytes (the attention kernels leave their counters at zero after each call)."""
+    if nbytes == 0:
+        return None
+    key = (str(device), tag)
+    buf = _WS.get(key)
+    if buf is None or buf.numel() < nbytes:
+        buf = torch.zeros(int(nbytes) + 256, dtype=torch.uint8, device=device)
+        _WS[key] = buf
+    off = (-buf.data_ptr()) % 256
+    return buf[off:off + nbytes]
+
+
+def kv_view(cache: torch.Tensor, page_table: Optional[torch.Tensor] = None) -> DustinKV:
+    """dustin_kv of a bf16 cache: [B, N_cap, Hkv, d] (contiguous mode) or
+    [num_pages, page_size, Hkv, d] with an int32 page table [B, max_pages] (paged)."""
+    if cache.dtype != torch.bfloat16 or cache.dim() != 4 or cache.stride(3) != 1:
+        raise ValueError("cache must be bf16 [B|pages, N|page_size, Hkv, d] with contiguous d")
+    kv = DustinKV()
+    kv.data = cache.data_ptr()
+    kv.num_kv_heads = cache.shape[2]
+    kv.head_dim = cache.shape[3]
+    kv.stride_n = cache.stride(1)
+    kv.stride_h = cache.stride(2)
+    if page_table is None:
+        kv.stride_b = cache.stride(0)
+        kv.capacity = cache.shape[1]
+    else:
+        if page_table.dtype != torch.int32 or page_table.dim() != 2:
+            raise ValueError("page_table must be int32 [B, max_pages]")
+        page_table = page_table.contiguous()
+        kv.page_table = page_table.data_ptr()
+        kv.page_size = cache.shape[1]
+        kv.max_pages = page_table.shape[1]
+        kv.num_pages = cache.shape[0]
+        kv.stride_page = cache.stride(0)
+        kv._keep = page_table
+    return kv
+
+
+def _capacity(kv: DustinKV) -> int:
+    return kv.max_pages * kv.page_size if kv.page_table else kv.capacity
+
+
+def _batch(B, max_len, nq_max, k_max, seq_lens, n_query=None, budget=None, m=None, m_scalar=0):
+    bt = DustinBatch()
+    bt.batch, bt.max_len, bt.nq_max, bt.k_max = int(B), int(max_len), int(nq_max), int(k_max)
+    bt.seq_lens = seq_lens.data_ptr()
+    bt.n_query = None if n_query is None else n_query.data_ptr()
+    bt.budget = None if budget is None else budget.data_ptr()
+    bt.m = None if m is None else m.data_ptr()
+    bt.m_scalar = int(m_scalar)
+    bt._keep = (seq_lens, n_query, budget, m)
+    return bt
+
+
+# ----------------------------------------------------------------------------- score
+
+def score(q: torch.Tensor, k: torch.Tensor, seq_lens, heads: Sequence[int], *, n_query=None,
+          scale: Optional[float] = None, groups: int = 1, init: Optional[torch.Tensor] = None,
+          out: Optional[torch.Tensor] = None, max_len: Optional[int] = None, stream=None):
+    """Eq. 5 over the scoring heads.  q bf16 [B, nq_max, Hq, d]; k bf16 [B, N_cap, Hkv, d];
+    init / out fp32 [B, groups, >= max_len].  Returns out (positions >= N_b untouched)."""
+    _on_gpu(q, k, init, out)
+    B, nq_max, Hq, d = q.shape
+    dev = q.device
+    seq = _i32_dev(seq_lens, dev)
+    nqa = _i32_dev(n_query, dev)
+    max_len = k.shape[1] if max_len is None else int(max_len)
+    if out is None:
+        out = torch.empty((B, groups, max_len), dtype=torch.float32, device=dev)
+    heads_host = (ctypes.c_int32 * len(heads))(*[int(h) for h in heads])
+    kv = kv_view(k)
+    bt = _batch(B, max_len, nq_max, 0, seq, nqa)
+    nbytes = lib().dustin_score_workspace(B, max_len, nq_max, len(heads))
+    ws = workspace(nbytes, dev, "score")
+    scale = 1.0 / math.sqrt(d) if scale is None else scale
+    ins = (init.stride(0), init.stride(1)) if init is not None else (0, 0)
+    st = lib().dustin_score(_ptr(q), q.stride(0), q.stride(1), q.stride(2), Hq, heads_host,
+                            len(heads), ctypes.byref(kv), ctypes.byref(bt), float(scale),
+                            int(groups), _ptr(init), ins[0], ins[1], _ptr(out), out.stride(0),
+                            out.stride(1), _ptr(ws), nbytes, _stream(stream))
+    _check(st, "dustin_score")
+    return out
+
+
+# ----------------------------------------------------------------------------- top-k
+
+def topk(s_draft: Optional[torch.Tensor], s_target: Optional[torch.Tensor], seq_lens,
+         k_max: int, *, budget=None, m=None, m_scalar: Optional[int] = None, n_sink: int = 4,
+         n_window: int = 16, groups: int = 1, idx: Optional[torch.Tensor] = None,
+         count: Optional[torch.Tensor] = None, stream=None):
+    """Eq. 6.  s_draft / s_target fp32 [B, G' (1 = broadcast), N]; returns (idx int32
+    [B, groups, k_max] ascending, only [:count] written; count int32 [B, groups])."""
+    _on_gpu(s_draft, s_target, idx, count)
+    ref = s_target if s_target is not None else s_draft
+    B, _, max_len = ref.shape
+    dev = ref.device
+    seq = _i32_dev(seq_lens, dev)
+    bud = _i32_dev(budget, dev)
+    ma = _i32_dev(m, dev)
+    P = n_sink + n_window
+    if m_scalar is None:
+        m_scalar = 0 if s_draft is None else (k_max - P if s_target is None else (k_max - P) // 2)
+    if idx is None:
+        idx = torch.empty((B, groups, k_max), dtype=torch.int32, device=dev)
+    if count is None:
+        count = torch.empty((B, groups), dtype=torch.int32, device=dev)
+
+    def st(s):
+        if s is None:
+            return 0, 0
+        return s.stride(0), (0 if s.shape[1] == 1 else s.stride(1))
+
+    dsb, dsg = st(s_draft)
+    tsb, tsg = st(s_target)
+    bt = _batch(B, max_len, 0, k_max, seq, None, bud, ma, m_scalar)
+    rc = lib().dustin_topk(_ptr(s_draft), dsb, dsg, _ptr(s_target), tsb, tsg, ctypes.byref(bt),
+                           int(groups), int(n_sink), int(n_window), _ptr(idx), idx.stride(0),
+                           idx.stride(1), _ptr(count), None, 0, _stream(stream))
+    _check(rc, "dustin_topk")
+    return idx, count
+
+
+# ----------------------------------------------------------------------------- attention
+
+def _attn_common(q, k, v, seq_lens, n_query, page_table, max_len, out):
+    _on_gpu(q, k, v, out, page_table)
+    B, nq_max, Hq, d = q.shape
+    dev = q.device
+    kv, vv = kv_view(k, page_table), kv_view(v, page_table)
+    if max_len is None:
+        max_len = _capacity(kv) - nq_max
+    if out is None:
+        out = torch.empty_like(q)
+    return B, nq_max, Hq, d, dev, kv, vv, int(max_len), out
+
+
+def sparse_verify_attn(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, idx: torch.Tensor,
+                       count: torch.Tensor, seq_lens, *, n_query=None,
+                       page_table: Optional[torch.Tensor] = None, scale: Optional[float] = None,
+                       out: Optional[torch.Tensor] = None, max_len: Optional[int] = None,
+                       stream=None):
+    """Verification attention over idx[b, g, :count] plus the causal verification window.
+    q/out bf16 [B, T_max, Hq, 128]; idx int32 [B, G, k_max]; count int32 [B, G]."""
+    B, nq_max, Hq, d, dev, kv, vv, max_len, out = _attn_common(q, k, v, seq_lens, n_query,
+                                                                page_table, max_len, out)
+    _on_gpu(idx, count)
+    seq = _i32_dev(seq_lens, dev)
+    nqa = _i32_dev(n_query, dev)
+    G, k_max = idx.shape[1], idx.shape[2]
+    bt = _batch(B, max_len, nq_max, k_max, seq, nqa)
+    nbytes = lib().dustin_attn_workspace(B, Hq, kv.num_kv_heads, nq_max, k_max, 1)
+    ws = workspace(nbytes, dev, "attn")
+    scale = 1.0 / math.sqrt(d) if scale is None else scale
+    rc = lib().dustin_sparse_verify_attn(_ptr(q), q.stride(0), q.stride(1), q.stride(2), Hq,
+                                         ctypes.byref(kv), ctypes.byref(vv), ctypes.byref(bt),
+                                         _ptr(idx), idx.stride(0), idx.stride(1),
+                                         _ptr(count.contiguous()), G, float(scale), _ptr(out),
+                                         out.stride(0), out.stride(1), out.stride(2), _ptr(ws),
+                                         nbytes, _stream(stream))
+    _check(rc, "dustin_sparse_verify_attn")
+    return out
+
+
+def dense_verify_attn(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, seq_lens, *,
+                      n_query=None, page_table: Optional[torch.Tensor] = None,
+                      scale: Optional[float] = None, out: Optional[torch.Tensor] = None,
+                      max_len: Optional[int] = None, stream=None):
+    """Full-cache verification attention over [0, N_b) plus the causal window."""
+    B, nq_max, Hq, d, dev, kv, vv, max_len, out = _attn_common(q, k, v, seq_lens, n_query,
+                                                                page_table, max_len, out)
+    seq = _i32_dev(seq_lens, dev)
+    nqa = _i32_dev(n_query, dev)
+    bt = _batch(B, max_len, nq_max, 0, seq, nqa)
+    nbytes = lib().dustin_attn_workspace(B, Hq, kv.num_kv_heads, nq_max, max_len, 0)
+    ws = workspace(nbytes, dev, "attn")
+    scale = 1.0 / math.sqrt(d) if scale is None else scale
+    rc = lib().dense_verify_attn(_ptr(q), q.stride(0), q.stride(1), q.stride(2), Hq,
+                                 ctypes.byref(kv), ctypes.byref(vv), ctypes.byref(bt),
+                                 float(scale), _ptr(out), out.stride(0), out.stride(1),
+                                 out.stride(2), _ptr(ws), nbytes, _stream(stream))
+    _check(rc, "dense_verify_attn")
+    return out

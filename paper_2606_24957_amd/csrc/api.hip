@@ -1,0 +1,387 @@
+// api.hip -- the extern "C" boundary of libdustin: argument validation, workspace
+// layout, launch configuration.  Validation happens before any HIP call, so a rejected
+// call touches neither the device nor any output.
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include "kernels.hpp"
+
+using namespace dustin;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+constexpr size_t kCounterBytes = 4096;  // split counters at the head of the attention workspace
+constexpr int kAttnWaves = 4;
+constexpr int kMaxSplits = 128;
+constexpr int kTopkMaxLen = 1 << 20;
+
+size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+bool rows_aligned(const void* p, int64_t s0, int64_t s1, int64_t s2) {
+  // bf16 rows read or written 16 bytes at a time
+  return aligned(p, 16) && s0 % 8 == 0 && s1 % 8 == 0 && s2 % 8 == 0;
+}
+
+int env_int(const char* name, int fallback) {
+  const char* v = getenv(name);
+  if (!v || !*v) return fallback;
+  const int x = atoi(v);
+  return x > 0 ? x : fallback;
+}
+
+bool batch_ok(const dustin_batch* bt) {
+  if (!bt || bt->batch < 0 || bt->max_len < 0 || bt->nq_max < 0 || bt->k_max < 0) return false;
+  if (bt->batch > 0 && !bt->seq_lens) return false;
+  return true;
+}
+
+SeqDims dims_of(const dustin_batch* bt) {
+  SeqDims d;
+  d.seq_lens = bt->seq_lens;
+  d.n_query = bt->n_query;
+  d.budget = bt->budget;
+  d.m = bt->m;
+  d.max_len = bt->max_len;
+  d.nq_max = bt->nq_max;
+  d.k_max = bt->k_max;
+  d.m_scalar = bt->m_scalar;
+  return d;
+}
+
+// Validates a cache view for `need` addressable positions per sequence.
+dustin_status kv_of(const dustin_kv* kv, int head_dim, int64_t need, KvView* out) {
+  if (!kv || !kv->data || kv->num_kv_heads <= 0) return DUSTIN_ERR_INVALID_ARG;
+  if (kv->head_dim != head_dim) return DUSTIN_ERR_INVALID_ARG;
+  if (!aligned(kv->data, 16) || kv->stride_n % 8 || kv->stride_h % 8 || kv->stride_b % 8 ||
+      kv->stride_page % 8)
+    return DUSTIN_ERR_INVALID_ARG;
+  if (kv->stride_n <= 0 || kv->stride_h < 0 || kv->stride_b < 0) return DUSTIN_ERR_INVALID_ARG;
+  memset(out, 0, sizeof *out);
+  out->data = static_cast<const uint16_t*>(kv->data);
+  out->stride_b = kv->stride_b;
+  out->stride_n = kv->stride_n;
+  out->stride_h = kv->stride_h;
+  if (kv->page_table) {
+    const int ps = kv->page_size;
+    if (ps <= 0 || (ps & (ps - 1)) || kv->max_pages <= 0 || kv->num_pages <= 0 ||
+        kv->stride_page <= 0)
+      return DUSTIN_ERR_INVALID_ARG;
+    if (!aligned(kv->page_table, 4)) return DUSTIN_ERR_INVALID_ARG;
+    int shift = 0;
+    while ((1 << shift) < ps) ++shift;
+    out->page_table = kv->page_table;
+    out->page_shift = shift;
+    out->max_pages = kv->max_pages;
+    out->num_pages = kv->num_pages;
+    out->stride_page = kv->stride_page;
+    out->capacity = (int64_t)kv->max_pages * ps;
+  } else {
+    out->capacity = kv->capacity;
+  }
+  if (out->capacity < need || out->capacity <= 0) return DUSTIN_ERR_INVALID_ARG;
+  return DUSTIN_OK;
+}
+
+int attn_row_tiles(int nq_max, int group_size) {
+  const int rows = nq_max * group_size;
+  int rt = (rows + 15) / 16;
+  if (rt == 7) rt = 8;  // instantiated tile counts: 1..6 and 8
+  return rt < 1 ? 1 : rt;
+}
+
+int attn_splits(int batch, int num_kv_heads, int64_t tokens_per_pair) {
+  const int64_t pairs = (int64_t)batch * num_kv_heads;
+  if (pairs <= 0) return 1;
+  const int64_t steps = (tokens_per_pair + 31) / 32;
+  int s;
+  const int forced = env_int("DUSTIN_ATTN_SPLITS", 0);
+  if (forced > 0) {
+    s = forced;
+  } else {
+    const int64_t target_wgs = 512;  // two workgroups per compute unit
+    int64_t want = (target_wgs + pairs - 1) / pairs;
+    const int64_t per_wave_floor = steps / (kAttnWaves * 2);  // each wave >= 2 steps
+    if (want > per_wave_floor) want = per_wave_floor;
+    s = (int)(want < 1 ? 1 : want);
+  }
+  if (s > kMaxSplits) s = kMaxSplits;
+  if (pairs > (int64_t)(kCounterBytes / 4)) s = 1;
+  const int64_t max_useful = steps < 1 ? 1 : steps;
+  if (s > max_useful) s = (int)max_useful;
+  return s < 1 ? 1 : s;
+}
+
+size_t attn_ws_bytes(int batch, int num_q_heads, int num_kv_heads, int nq_max, int64_t tokens) {
+  if (batch <= 0 || num_kv_heads <= 0 || num_q_heads % num_kv_heads) return 0;
+  const int splits = attn_splits(batch, num_kv_heads, tokens + nq_max);
+  if (splits <= 1) return 0;
+  const int rows_pad = attn_row_tiles(nq_max, num_q_heads / num_kv_heads) * 16;
+  const size_t pairs = (size_t)batch * num_kv_heads;
+  const size_t acc = pairs * splits * rows_pad * 128 * sizeof(float);
+  const size_t ml = pairs * splits * rows_pad * 2 * sizeof(float);
+  return kCounterBytes + round_up(acc, kAlign) + round_up(ml, kAlign);
+}
+
+dustin_status run_attention(bool sparse, const void* q, int64_t q_sb, int64_t q_st, int64_t q_sh,
+                            int32_t num_q_heads, const dustin_kv* k, const dustin_kv* v,
+                            const dustin_batch* bt, const int32_t* idx, int64_t idx_sb,
+                            int64_t idx_sg, const int32_t* count, int32_t groups, float scale,
+                            void* out, int64_t o_sb, int64_t o_st, int64_t o_sh, void* ws,
+                            size_t ws_bytes, void* stream) {
+  if (!batch_ok(bt) || !q || !out || !k || !v) return DUSTIN_ERR_INVALID_ARG;
+  if (!isfinite(scale)) return DUSTIN_ERR_INVALID_ARG;
+  const int Hkv = k->num_kv_heads;
+  if (num_q_heads <= 0 || Hkv <= 0 || num_q_heads % Hkv || v->num_kv_heads != Hkv)
+    return DUSTIN_ERR_INVALID_ARG;
+  if (k->head_dim != 128 || v->head_dim != 128) return DUSTIN_ERR_UNSUPPORTED;
+  if ((k->page_table == nullptr) != (v->page_table == nullptr)) return DUSTIN_ERR_INVALID_ARG;
+  if (!rows_aligned(q, q_sb, q_st, q_sh) || !rows_aligned(out, o_sb, o_st, o_sh))
+    return DUSTIN_ERR_INVALID_ARG;
+  const int gs = num_q_heads / Hkv;
+  if ((int64_t)bt->nq_max * gs > 128) return DUSTIN_ERR_UNSUPPORTED;
+  if (sparse) {
+    if (!idx || !count || (groups != 1 && groups != Hkv)) return DUSTIN_ERR_INVALID_ARG;
+    if (!aligned(idx, 4) || !aligned(count, 4) || idx_sb < 0 || idx_sg < 0)
+      return DUSTIN_ERR_INVALID_ARG;
+  }
+  const int64_t need = (int64_t)bt->max_len + bt->nq_max;
+  KvView kv, vv;
+  dustin_status st = kv_of(k, 128, need, &kv);
+  if (st != DUSTIN_OK) return st;
+  st = kv_of(v, 128, need, &vv);
+  if (st != DUSTIN_OK) return st;
+  const int B = bt->batch;
+  if (B == 0 || bt->nq_max == 0) return DUSTIN_OK;
+  const int64_t tokens = sparse ? (int64_t)bt->k_max : (int64_t)bt->max_len;
+  const size_t need_ws = attn_ws_bytes(B, num_q_heads, Hkv, bt->nq_max, tokens);
+  if (need_ws && (!ws || ws_bytes < need_ws || !aligned(ws, kAlign))) return DUSTIN_ERR_WORKSPACE;
+
+  AttnArgs a;
+  memset(&a, 0, sizeof a);
+  a.q = static_cast<const uint16_t*>(q);
+  a.q_sb = q_sb;
+  a.q_st = q_st;
+  a.q_sh = q_sh;
+  a.out = static_cast<uint16_t*>(out);
+  a.o_sb = o_sb;
+  a.o_st = o_st;
+  a.o_sh = o_sh;
+  a.k = kv;
+  a.v = vv;
+  a.dims = dims_of(bt);
+  a.idx = idx;
+  a.idx_sb = idx_sb;
+  a.idx_sg = idx_sg;
+  a.count = count;
+  a.groups = sparse ? groups : 1;
+  a.num_kv_heads = Hkv;
+  a.group_size = gs;
+  a.scale_log2 = scale * kLog2e;
+  const int rt = attn_row_tiles(bt->nq_max, gs);
+  a.rows_pad = rt * 16;
+  a.splits = attn_splits(B, Hkv, tokens + bt->nq_max);
+  if (a.splits > 1) {
+    char* base = static_cast<char*>(ws);
+    const size_t pairs = (size_t)B * Hkv;
+    a.counters = reinterpret_cast<uint32_t*>(base);
+    a.part_acc = reinterpret_cast<float*>(base + kCounterBytes);
+    const size_t acc = pairs * a.splits * a.rows_pad * 128 * sizeof(float);
+    a.part_ml = reinterpret_cast<float*>(base + kCounterBytes + round_up(acc, kAlign));
+  }
+  const hipError_t e = launch_verify_attn(a, rt, B, sparse, kv.page_table != nullptr,
+                                          static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? DUSTIN_OK : DUSTIN_ERR_LAUNCH;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* dustin_status_string(dustin_status status) {
+  switch (status) {
+    case DUSTIN_OK: return "ok";
+    case DUSTIN_ERR_INVALID_ARG: return "invalid argument";
+    case DUSTIN_ERR_UNSUPPORTED: return "unsupported configuration";
+    case DUSTIN_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
+    case DUSTIN_ERR_LAUNCH: return "kernel launch failed";
+  }
+  return "unknown status";
+}
+
+int32_t dustin_version(void) { return (1 << 16) | 0; }
+
+// ------------------------------------------------------------------ score
+
+size_t dustin_score_workspace(int32_t batch, int32_t max_len, int32_t nq_max, int32_t n_heads) {
+  if (batch <= 0 || max_len <= 0 || nq_max <= 0 || n_heads <= 0) return 0;
+  const size_t ld = round_up((size_t)max_len, 64);
+  const size_t n_chunks = ((size_t)max_len + kScoreChunk - 1) / kScoreChunk;
+  const size_t rows = (size_t)batch * n_heads * nq_max;
+  return round_up(rows * ld * sizeof(float), kAlign) + round_up(rows * n_chunks * 2 * sizeof(float), kAlign);
+}
+
+dustin_status dustin_score(const void* q, int64_t q_sb, int64_t q_sj, int64_t q_sh,
+                           int32_t num_q_heads, const int32_t* heads_host, int32_t n_heads,
+                           const dustin_kv* k, const dustin_batch* bt, float scale,
+                           int32_t groups, const float* init, int64_t init_sb, int64_t init_sg,
+                           float* out, int64_t out_sb, int64_t out_sg, void* workspace,
+                           size_t workspace_bytes, void* stream) {
+  if (!batch_ok(bt) || !q || !k || !out || !heads_host) return DUSTIN_ERR_INVALID_ARG;
+  if (!isfinite(scale)) return DUSTIN_ERR_INVALID_ARG;
+  if (n_heads < 1 || n_heads > kScoreMaxHeads) return DUSTIN_ERR_UNSUPPORTED;
+  const int Hkv = k->num_kv_heads;
+  if (num_q_heads <= 0 || Hkv <= 0 || num_q_heads % Hkv) return DUSTIN_ERR_INVALID_ARG;
+  if (k->head_dim != 64 && k->head_dim != 128) return DUSTIN_ERR_UNSUPPORTED;
+  if (k->page_table) return DUSTIN_ERR_UNSUPPORTED;
+  if (groups != 1 && groups != Hkv) return DUSTIN_ERR_INVALID_ARG;
+  if (bt->nq_max < 1 || bt->nq_max > 16) return DUSTIN_ERR_UNSUPPORTED;
+  if (!rows_aligned(q, q_sb, q_sj, q_sh)) return DUSTIN_ERR_INVALID_ARG;
+  if (!aligned(out, 4) || out_sb < 0 || out_sg < 0) return DUSTIN_ERR_INVALID_ARG;
+  if (init && (!aligned(init, 4) || init_sb < 0 || init_sg < 0)) return DUSTIN_ERR_INVALID_ARG;
+  const int gs = num_q_heads / Hkv;
+
+  ScoreArgs a;
+  memset(&a, 0, sizeof a);
+  int n_used = 0;
+  for (int i = 0; i < n_heads; ++i) {
+    const int h = heads_host[i];
+    if (h < 0 || h >= num_q_heads) return DUSTIN_ERR_INVALID_ARG;
+    for (int j = 0; j < i; ++j)
+      if (heads_host[j] == h) return DUSTIN_ERR_INVALID_ARG;
+    a.heads[i] = h;
+    const int g = h / gs;
+    int u = 0;
+    while (u < n_used && a.used_kv[u] != g) ++u;
+    if (u == n_used) {
+      a.used_kv[n_used++] = g;
+    }
+    for (int jq = 0; jq < bt->nq_max; ++jq) {
+      if (a.pairs_per_kv[u] >= 16) return DUSTIN_ERR_UNSUPPORTED;  // one MFMA column tile
+      a.pair_head[u * 16 + a.pairs_per_kv[u]] = (uint8_t)i;
+      a.pair_query[u * 16 + a.pairs_per_kv[u]] = (uint8_t)jq;
+      a.pairs_per_kv[u]++;
+    }
+  }
+  KvView kv;
+  const dustin_status st = kv_of(k, k->head_dim, bt->max_len, &kv);
+  if (st != DUSTIN_OK) return st;
+  const int B = bt->batch;
+  if (B == 0 || bt->max_len == 0) return DUSTIN_OK;
+  const size_t need_ws = dustin_score_workspace(B, bt->max_len, bt->nq_max, n_heads);
+  if (!workspace || workspace_bytes < need_ws || !aligned(workspace, kAlign))
+    return DUSTIN_ERR_WORKSPACE;
+
+  a.q = static_cast<const uint16_t*>(q);
+  a.q_sb = q_sb;
+  a.q_sj = q_sj;
+  a.q_sh = q_sh;
+  a.k = kv;
+  a.dims = dims_of(bt);
+  a.n_heads = n_heads;
+  a.group_size = gs;
+  a.groups = groups;
+  a.scale_log2 = scale * kLog2e;
+  a.init = init;
+  a.init_sb = init_sb;
+  a.init_sg = init_sg;
+  a.out = out;
+  a.out_sb = out_sb;
+  a.out_sg = out_sg;
+  a.nq_max = bt->nq_max;
+  a.ld = (int64_t)round_up((size_t)bt->max_len, 64);
+  a.n_chunks = (bt->max_len + kScoreChunk - 1) / kScoreChunk;
+  const size_t rows = (size_t)B * n_heads * bt->nq_max;
+  a.logits = static_cast<float*>(workspace);
+  a.stats = reinterpret_cast<float*>(static_cast<char*>(workspace) +
+                                     round_up(rows * a.ld * sizeof(float), kAlign));
+  const hipError_t e = launch_score(a, B, n_used, k->head_dim, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? DUSTIN_OK : DUSTIN_ERR_LAUNCH;
+}
+
+// ------------------------------------------------------------------ top-k
+
+size_t dustin_topk_workspace(int32_t batch, int32_t groups, int32_t max_len) {
+  (void)batch;
+  (void)groups;
+  (void)max_len;
+  return 0;
+}
+
+dustin_status dustin_topk(const float* s_draft, int64_t d_sb, int64_t d_sg,
+                          const float* s_target, int64_t t_sb, int64_t t_sg,
+                          const dustin_batch* bt, int32_t groups, int32_t n_sink,
+                          int32_t n_window, int32_t* idx, int64_t idx_sb, int64_t idx_sg,
+                          int32_t* count, void* workspace, size_t workspace_bytes,
+                          void* stream) {
+  (void)workspace;
+  (void)workspace_bytes;
+  if (!batch_ok(bt) || !idx || !count) return DUSTIN_ERR_INVALID_ARG;
+  if (!s_draft && !s_target) return DUSTIN_ERR_INVALID_ARG;
+  if (groups < 1 || groups > 65535 || n_sink < 0 || n_window < 0) return DUSTIN_ERR_INVALID_ARG;
+  if (bt->max_len > kTopkMaxLen) return DUSTIN_ERR_UNSUPPORTED;
+  const int P = n_sink + n_window;
+  if (bt->k_max < P) return DUSTIN_ERR_INVALID_ARG;
+  if (!bt->m && (bt->m_scalar < 0 || bt->m_scalar > bt->k_max - P)) return DUSTIN_ERR_INVALID_ARG;
+  if (!s_draft && !bt->m && bt->m_scalar != 0) return DUSTIN_ERR_INVALID_ARG;
+  if (!s_target && !bt->m && !bt->budget && bt->m_scalar != bt->k_max - P) return DUSTIN_ERR_INVALID_ARG;
+  if (!aligned(idx, 4) || !aligned(count, 4) || idx_sb < 0 || idx_sg < 0) return DUSTIN_ERR_INVALID_ARG;
+  if ((s_draft && (!aligned(s_draft, 4) || d_sb < 0 || d_sg < 0)) ||
+      (s_target && (!aligned(s_target, 4) || t_sb < 0 || t_sg < 0)))
+    return DUSTIN_ERR_INVALID_ARG;
+  const int B = bt->batch;
+  if (B == 0) return DUSTIN_OK;
+  TopkArgs a;
+  memset(&a, 0, sizeof a);
+  a.s_draft = s_draft;
+  a.d_sb = d_sb;
+  a.d_sg = d_sg;
+  a.s_target = s_target;
+  a.t_sb = t_sb;
+  a.t_sg = t_sg;
+  a.dims = dims_of(bt);
+  a.groups = groups;
+  a.n_sink = n_sink;
+  a.n_window = n_window;
+  a.idx = idx;
+  a.idx_sb = idx_sb;
+  a.idx_sg = idx_sg;
+  a.count = count;
+  const hipError_t e = launch_topk(a, B, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? DUSTIN_OK : DUSTIN_ERR_LAUNCH;
+}
+
+// ------------------------------------------------------------------ attention
+
+size_t dustin_attn_workspace(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
+                             int32_t nq_max, int32_t max_tokens, int32_t sparse) {
+  (void)sparse;
+  if (nq_max <= 0 || max_tokens < 0) return 0;
+  return attn_ws_bytes(batch, num_q_heads, num_kv_heads, nq_max, max_tokens);
+}
+
+dustin_status dustin_sparse_verify_attn(const void* q, int64_t q_sb, int64_t q_st,
+                                        int64_t q_sh, int32_t num_q_heads, const dustin_kv* k,
+                                        const dustin_kv* v, const dustin_batch* bt,
+                                        const int32_t* idx, int64_t idx_sb, int64_t idx_sg,
+                                        const int32_t* count, int32_t groups, float scale,
+                                        void* out, int64_t o_sb, int64_t o_st, int64_t o_sh,
+                                        void* workspace, size_t workspace_bytes, void* stream) {
+  return run_attention(true, q, q_sb, q_st, q_sh, num_q_heads, k, v, bt, idx, idx_sb, idx_sg,
+                       count, groups, scale, out, o_sb, o_st, o_sh, workspace, workspace_bytes,
+                       stream);
+}
+
+dustin_status dense_verify_attn(const void* q, int64_t q_sb, int64_t q_st, int64_t q_sh,
+                                int32_t num_q_heads, const dustin_kv* k, const dustin_kv* v,
+                                const dustin_batch* bt, float scale, void* out, int64_t o_sb,
+                                int64_t o_st, int64_t o_sh, void* workspace,
+                                size_t workspace_bytes, void* stream) {
+  return run_attention(false, q, q_sb, q_st, q_sh, num_q_heads, k, v, bt, nullptr, 0, 0, nullptr,
+                       1, scale, out, o_sb, o_st, o_sh, workspace, workspace_bytes, stream);
+}
+
+}  // extern "C"

@@ -1,0 +1,78 @@
+// kernels.hpp -- argument blocks and launchers of the libdustin kernels (internal).
+#pragma once
+
+#include "common.hpp"
+
+namespace dustin {
+
+// ---- verification attention (attn.hip) ----
+struct AttnArgs {
+  const uint16_t* q;
+  int64_t q_sb, q_st, q_sh;
+  uint16_t* out;
+  int64_t o_sb, o_st, o_sh;
+  KvView k, v;
+  SeqDims dims;
+  const int32_t* idx;
+  int64_t idx_sb, idx_sg;
+  const int32_t* count;
+  int32_t groups;
+  int32_t num_kv_heads, group_size;
+  float scale_log2;
+  int32_t splits;
+  int32_t rows_pad;
+  float* part_acc;     // [B, Hkv, splits, rows_pad, 128]
+  float* part_ml;      // [B, Hkv, splits, rows_pad, 2]
+  uint32_t* counters;  // [B, Hkv]
+};
+
+hipError_t launch_verify_attn(const AttnArgs& a, int rt, int B, bool sparse, bool paged,
+                              hipStream_t stream);
+
+// ---- scoring-head importance (score.hip) ----
+constexpr int kScoreWaves = 4;
+constexpr int kScoreChunk = 1024;        // positions per pass-1 workgroup
+constexpr int kScoreFinishChunk = 2048;  // positions per pass-2 workgroup
+constexpr int kScoreMaxHeads = 16;
+
+struct ScoreArgs {
+  const uint16_t* q;
+  int64_t q_sb, q_sj, q_sh;
+  KvView k;
+  SeqDims dims;
+  int32_t heads[kScoreMaxHeads];
+  int32_t n_heads;
+  int32_t used_kv[kScoreMaxHeads];       // KV heads read by pass 1
+  int32_t pairs_per_kv[kScoreMaxHeads];  // (head, query) pairs of each used KV head
+  uint8_t pair_head[kScoreMaxHeads * 16];   // head slot of pair i of used KV head u
+  uint8_t pair_query[kScoreMaxHeads * 16];  // query of that pair
+  int32_t group_size, groups;
+  float scale_log2;
+  const float* init;
+  int64_t init_sb, init_sg;
+  float* out;
+  int64_t out_sb, out_sg;
+  float* logits;  // [B, n_heads, nq_max, ld]  scaled logits, log2 domain
+  float* stats;   // [B, n_heads, nq_max, n_chunks, 2]  (max, sum of exp2) per chunk
+  int64_t ld;
+  int32_t nq_max, n_chunks;
+};
+
+hipError_t launch_score(const ScoreArgs& a, int B, int n_used_kv, int head_dim, hipStream_t stream);
+
+// ---- tiered selection (topk.hip) ----
+struct TopkArgs {
+  const float* s_draft;
+  int64_t d_sb, d_sg;
+  const float* s_target;
+  int64_t t_sb, t_sg;
+  SeqDims dims;
+  int32_t groups, n_sink, n_window;
+  int32_t* idx;
+  int64_t idx_sb, idx_sg;
+  int32_t* count;
+};
+
+hipError_t launch_topk(const TopkArgs& a, int B, hipStream_t stream);
+
+}  // namespace dustin

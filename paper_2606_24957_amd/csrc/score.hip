@@ -1,0 +1,174 @@
+// score.hip -- scoring-head importance (Eq. 5 restricted to the semantic retrieval heads).
+//
+// Pass 1 (score_logits_kernel): one workgroup per (chunk of positions, KV head used by a
+//   scoring head, sequence).  Each K row of that KV head is read once, with the same
+//   16-byte-per-lane MFMA A-operand loads as the attention kernel, and multiplied by
+//   every (scoring head of this KV head, query) pair at once (up to 16 pairs = one MFMA
+//   column tile).  The scaled logits (log2 domain) go to the workspace together with the
+//   chunk's running (max, sum of exp2) per pair.
+// Pass 2 (score_finish_kernel): per (chunk, output group, sequence): merge the chunk
+//   statistics of every pair into its softmax normaliser, then
+//   out[n] = init[n] + sum_pairs exp2(logit - M) / Z, pairs in (head, query) order.
+#include "kernels.hpp"
+
+namespace dustin {
+
+template <int D>
+__global__ __launch_bounds__(kScoreWaves * kWave) void score_logits_kernel(ScoreArgs a) {
+  constexpr int KS = D / 32;
+  const int chunk = blockIdx.x, ug = blockIdx.y, b = blockIdx.z;
+  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+  const int lr = lane & 15, lg = lane >> 4;
+  const int g = a.used_kv[ug];
+  const int N = a.dims.len(b);
+  const int nq = a.dims.nq(b);
+  const int p_begin = chunk * kScoreChunk;
+  const int p_end = min(N, p_begin + kScoreChunk);
+
+  // pair lr of this KV head: (scoring head slot, query)
+  const int npairs = a.pairs_per_kv[ug];
+  const int pair_slot = lr < npairs ? a.pair_head[ug * 16 + lr] : 0;
+  const int pair_q = lr < npairs ? a.pair_query[ug * 16 + lr] : 0;
+  const bool pair_ok = lr < npairs && pair_q < nq;
+  bf16x8 qb[KS];
+  if (pair_ok) {
+    const uint16_t* qp = a.q + (int64_t)b * a.q_sb + (int64_t)pair_q * a.q_sj +
+                         (int64_t)a.heads[pair_slot] * a.q_sh + 8 * lg;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) qb[ks] = as_bf16x8(load16(qp + 32 * ks));
+  } else {
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) qb[ks] = as_bf16x8(u32x4{0u, 0u, 0u, 0u});
+  }
+  float* lrow = a.logits + (((int64_t)b * a.n_heads + pair_slot) * a.nq_max + pair_q) * a.ld;
+
+  float m_run = -INFINITY, s_run = 0.f;
+  constexpr int U = 4;  // 16-position tiles per iteration (loads issued together)
+  for (int p0 = p_begin + wave * 16 * U; p0 < p_end; p0 += kScoreWaves * 16 * U) {
+    u32x4 kr[U][KS];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int p = min(p0 + 16 * u + lr, max(N - 1, 0));
+      const uint16_t* kp = a.k.row<false>(b, p, g) + 8 * lg;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) kr[u][ks] = load16(kp + 32 * ks);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      f32x4 c = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) c = mfma16x16x32(as_bf16x8(kr[u][ks]), qb[ks], c);
+      const int pb = p0 + 16 * u + 4 * lg;  // this lane's 4 positions, pair lr
+      float x[4];
+      float mx = -INFINITY;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        x[e] = (pb + e < p_end) ? c[e] * a.scale_log2 : -INFINITY;
+        mx = fmaxf(mx, x[e]);
+      }
+      const float m_new = fmaxf(m_run, mx);
+      const float m_use = m_new == -INFINITY ? 0.f : m_new;
+      float add = 0.f;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) add += exp2f(x[e] - m_use);
+      s_run = s_run * exp2f(m_run - m_use) + add;
+      m_run = m_new;
+      if (pair_ok) {
+        if (pb + 3 < p_end) {
+          *reinterpret_cast<f32x4*>(lrow + pb) = f32x4{x[0], x[1], x[2], x[3]};
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (pb + e < p_end) lrow[pb + e] = x[e];
+        }
+      }
+    }
+  }
+
+  // reduce (max, sum) over lane groups, then over waves (fixed order)
+#pragma unroll
+  for (int off = 16; off <= 32; off <<= 1) {
+    const float mo = __shfl_xor(m_run, off), so = __shfl_xor(s_run, off);
+    const float mn = fmaxf(m_run, mo);
+    const float mu = mn == -INFINITY ? 0.f : mn;
+    s_run = s_run * exp2f(m_run - mu) + so * exp2f(mo - mu);
+    m_run = mn;
+  }
+  __shared__ float sm[kScoreWaves][16][2];
+  if (lg == 0) {
+    sm[wave][lr][0] = m_run;
+    sm[wave][lr][1] = s_run;
+  }
+  __syncthreads();
+  if (threadIdx.x < 16 && pair_ok) {
+    float M = -INFINITY;
+    for (int w = 0; w < kScoreWaves; ++w) M = fmaxf(M, sm[w][lr][0]);
+    const float mu = M == -INFINITY ? 0.f : M;
+    float S = 0.f;
+    for (int w = 0; w < kScoreWaves; ++w) S += sm[w][lr][1] * exp2f(sm[w][lr][0] - mu);
+    float* st = a.stats + ((((int64_t)b * a.n_heads + pair_slot) * a.nq_max + pair_q) * a.n_chunks + chunk) * 2;
+    st[0] = M;
+    st[1] = S;
+  }
+}
+
+__global__ __launch_bounds__(256) void score_finish_kernel(ScoreArgs a) {
+  const int chunk = blockIdx.x, go = blockIdx.y, b = blockIdx.z;
+  const int N = a.dims.len(b);
+  const int nq = a.dims.nq(b);
+  const int p_begin = chunk * kScoreFinishChunk;
+  if (p_begin >= N) return;
+  const int p_end = min(N, p_begin + kScoreFinishChunk);
+
+  // normalisers of the pairs that feed this output group: (slot, query, M, 1/Z)
+  __shared__ int sm_off[16 * 16];
+  __shared__ float sm_M[16 * 16], sm_iz[16 * 16];
+  __syncthreads();
+  const int total_pairs = a.n_heads * nq;
+  for (int pidx = threadIdx.x; pidx < total_pairs; pidx += blockDim.x) {
+    const int slot = pidx / nq, j = pidx - slot * nq;
+    const int kvh = a.heads[slot] / a.group_size;
+    if (a.groups != 1 && kvh != go) continue;
+    const float* st = a.stats + (((int64_t)b * a.n_heads + slot) * a.nq_max + j) * a.n_chunks * 2;
+    const int nch = (N + kScoreChunk - 1) / kScoreChunk;
+    float M = -INFINITY;
+    for (int c = 0; c < nch; ++c) M = fmaxf(M, st[2 * c]);
+    const float mu = M == -INFINITY ? 0.f : M;
+    float Z = 0.f;
+    for (int c = 0; c < nch; ++c) Z += st[2 * c + 1] * exp2f(st[2 * c] - mu);
+    // stable slot: pairs are summed in (head slot, query) order
+    sm_off[pidx] = ((int)(((int64_t)b * a.n_heads + slot) * a.nq_max + j));
+    sm_M[pidx] = mu;
+    sm_iz[pidx] = Z > 0.f ? 1.f / Z : 0.f;
+  }
+  __syncthreads();
+
+  const float* init_row = a.init ? a.init + (int64_t)b * a.init_sb + (int64_t)go * a.init_sg : nullptr;
+  float* out_row = a.out + (int64_t)b * a.out_sb + (int64_t)go * a.out_sg;
+  for (int n = p_begin + threadIdx.x; n < p_end; n += blockDim.x) {
+    float acc = 0.f;
+    for (int pidx = 0; pidx < total_pairs; ++pidx) {
+      const int slot = pidx / nq;
+      const int kvh = a.heads[slot] / a.group_size;
+      if (a.groups != 1 && kvh != go) continue;
+      const float x = a.logits[(int64_t)sm_off[pidx] * a.ld + n];
+      acc += exp2f(x - sm_M[pidx]) * sm_iz[pidx];
+    }
+    out_row[n] = (init_row ? init_row[n] : 0.f) + acc;
+  }
+}
+
+hipError_t launch_score(const ScoreArgs& a, int B, int n_used_kv, int head_dim, hipStream_t stream) {
+  dim3 grid1(a.n_chunks, n_used_kv, B);
+  if (head_dim == 128)
+    hipLaunchKernelGGL(score_logits_kernel<128>, grid1, dim3(kScoreWaves * kWave), 0, stream, a);
+  else
+    hipLaunchKernelGGL(score_logits_kernel<64>, grid1, dim3(kScoreWaves * kWave), 0, stream, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  dim3 grid2((a.dims.max_len + kScoreFinishChunk - 1) / kScoreFinishChunk, a.groups, B);
+  hipLaunchKernelGGL(score_finish_kernel, grid2, dim3(256), 0, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace dustin

@@ -73,8 +73,9 @@ class Shape:
 
     @property
     def n_cap(self) -> int:
-        """Cache rows per sequence: context plus the verification tokens."""
-        return max(n + t for n, t in zip(self.seq_lens, self.n_query))
+        """Cache rows per sequence: the longest context plus the most verification tokens
+        (the capacity every kernel call of the batch may address)."""
+        return max(self.seq_lens) + max(self.n_query)
 
     @property
     def draft_gamma(self) -> tuple:
@@ -217,7 +218,7 @@ def make_page_table(s: Shape, seed: int, device):
     per = _pages_per_seq(s)
     total = sum(per)
     perm = torch.randperm(total, generator=_gen("cpu", seed)).to(torch.int32)
-    maxp = max(per)
+    maxp = (s.n_cap + s.page_size - 1) // s.page_size
     pt = torch.zeros((s.B, maxp), dtype=torch.int32)
     off = 0
     for b, c in enumerate(per):
@@ -243,7 +244,7 @@ def make_layer(s: Shape, layer: int, device) -> Layer:
     vp = torch.zeros_like(kp)
     for b, c in enumerate(_pages_per_seq(s)):
         pages = pt[b, :c].long()
-        rows = min(c * ps, s.n_cap)
+        rows = min(c * ps, s.seq_lens[b] + s.n_query[b])
         src_k = torch.zeros((c * ps, Hkv, d), device=device, dtype=torch.bfloat16)
         src_v = torch.zeros_like(src_k)
         src_k[:rows] = kc[b, :rows]

@@ -1,0 +1,173 @@
+"""The C ABI without a GPU: libdustin.so loads, exports every function include/dustin.h
+declares, sizes its workspaces on the host, and rejects invalid arguments before any
+launch (every call here fails validation, so no kernel is ever enqueued)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2606_24957_amd as D
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "dustin.h")
+
+FAKE = 0x10000  # a non-null, 256-byte aligned address that validation never dereferences
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(dustin_\w+|dense_verify_attn)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(D.LIB_PATH):
+        pytest.skip("libdustin.so not built")
+    return D.lib()
+
+
+def test_every_declared_symbol_is_exported(L):
+    names = declared_functions()
+    assert set(names) == set(D.EXPORTED)
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_status_strings_and_version(L):
+    assert D.status_string(D.OK) == "ok"
+    for s in range(1, 5):
+        assert D.status_string(s) not in ("ok", "unknown status")
+    assert D.status_string(99) == "unknown status"
+    assert L.dustin_version() >> 16 == 1
+
+
+def test_workspace_sizes(L):
+    assert L.dustin_topk_workspace(16, 1, 32768) == 0
+    s = L.dustin_score_workspace(16, 32768, 4, 4)
+    assert s >= 16 * 4 * 4 * 32768 * 4 and s % 256 == 0
+    assert L.dustin_score_workspace(0, 10, 1, 1) == 0
+    # attention: a split-K workspace once the batch leaves compute units idle
+    w = L.dustin_attn_workspace(16, 64, 8, 5, 2048, 1)
+    assert w == 0 or w > 4096
+    assert L.dustin_attn_workspace(0, 64, 8, 5, 2048, 1) == 0
+
+
+def _batch(B=2, max_len=100, nq=4, k_max=40, m=10):
+    bt = D.DustinBatch()
+    bt.batch, bt.max_len, bt.nq_max, bt.k_max, bt.m_scalar = B, max_len, nq, k_max, m
+    bt.seq_lens = FAKE
+    return bt
+
+
+def _kv(Hkv=2, d=128, cap=200):
+    kv = D.DustinKV()
+    kv.data = FAKE
+    kv.num_kv_heads, kv.head_dim = Hkv, d
+    kv.stride_n, kv.stride_h, kv.stride_b, kv.capacity = Hkv * d, d, cap * Hkv * d, cap
+    return kv
+
+
+def _topk(L, bt, sd=FAKE, st=FAKE, groups=1, ns=4, nw=16, idx=FAKE, cnt=FAKE):
+    return L.dustin_topk(sd, 0, 0, st, 0, 0, ctypes.byref(bt), groups, ns, nw, idx, 0, 0, cnt,
+                         None, 0, None)
+
+
+def test_topk_rejects(L):
+    assert _topk(L, _batch(k_max=19)) == D.ERR_INVALID_ARG              # k < sinks + window
+    assert _topk(L, _batch(k_max=40, m=21)) == D.ERR_INVALID_ARG        # m > k - |P|
+    assert _topk(L, _batch(m=-1)) == D.ERR_INVALID_ARG
+    assert _topk(L, _batch(m=3), sd=None) == D.ERR_INVALID_ARG          # no S_D needs m = 0
+    assert _topk(L, _batch(m=3), st=None) == D.ERR_INVALID_ARG          # no S_T needs m = k-|P|
+    assert _topk(L, _batch(), sd=None, st=None) == D.ERR_INVALID_ARG
+    assert _topk(L, _batch(), idx=None) == D.ERR_INVALID_ARG
+    assert _topk(L, _batch(), groups=0) == D.ERR_INVALID_ARG
+    assert _topk(L, _batch(max_len=(1 << 20) + 1)) == D.ERR_UNSUPPORTED
+    bt = _batch()
+    bt.seq_lens = None
+    assert _topk(L, bt) == D.ERR_INVALID_ARG
+    assert L.dustin_topk(FAKE, 0, 0, FAKE, 0, 0, None, 1, 4, 16, FAKE, 0, 0, FAKE, None, 0,
+                         None) == D.ERR_INVALID_ARG
+
+
+def _attn(L, q=FAKE, kv=None, vv=None, bt=None, Hq=8, idx=FAKE, cnt=FAKE, groups=1, out=FAKE,
+          qs=(800 * 8 * 128, 8 * 128, 128), scale=0.1, ws=None, ws_bytes=0):
+    kv = kv or _kv()
+    vv = vv or _kv()
+    bt = bt or _batch()
+    return L.dustin_sparse_verify_attn(q, *qs, Hq, ctypes.byref(kv), ctypes.byref(vv),
+                                       ctypes.byref(bt), idx, 0, 0, cnt, groups, scale, out,
+                                       *qs, ws, ws_bytes, None)
+
+
+def test_attention_rejects(L):
+    assert _attn(L, q=None) == D.ERR_INVALID_ARG
+    assert _attn(L, out=None) == D.ERR_INVALID_ARG
+    assert _attn(L, idx=None) == D.ERR_INVALID_ARG
+    assert _attn(L, cnt=None) == D.ERR_INVALID_ARG
+    assert _attn(L, Hq=7) == D.ERR_INVALID_ARG                        # Hq % Hkv
+    assert _attn(L, groups=3) == D.ERR_INVALID_ARG                    # groups not in {1, Hkv}
+    assert _attn(L, q=FAKE + 2) == D.ERR_INVALID_ARG                  # 16-byte rows
+    assert _attn(L, qs=(4, 8 * 128, 128)) == D.ERR_INVALID_ARG
+    assert _attn(L, scale=float("nan")) == D.ERR_INVALID_ARG
+    assert _attn(L, kv=_kv(d=64), vv=_kv(d=64)) == D.ERR_UNSUPPORTED  # head_dim 128 only
+    assert _attn(L, kv=_kv(cap=103)) == D.ERR_INVALID_ARG             # capacity < max_len + T
+    assert _attn(L, vv=_kv(Hkv=4)) == D.ERR_INVALID_ARG
+    assert _attn(L, Hq=64, kv=_kv(Hkv=2), vv=_kv(Hkv=2), bt=_batch(nq=5)) == D.ERR_UNSUPPORTED
+    paged = _kv()
+    paged.page_table, paged.page_size, paged.max_pages, paged.num_pages = FAKE, 12, 20, 40
+    paged.stride_page = 12 * 256
+    assert _attn(L, kv=paged, vv=paged) == D.ERR_INVALID_ARG          # page size not 2^k
+    assert _attn(L, kv=paged) == D.ERR_INVALID_ARG                    # K paged, V not
+    # a batch that needs the split-K workspace refuses to run without one
+    need = L.dustin_attn_workspace(1, 8, 2, 4, 40, 1)
+    if need:
+        assert _attn(L, bt=_batch(B=1)) == D.ERR_WORKSPACE
+        assert _attn(L, bt=_batch(B=1), ws=FAKE + 8, ws_bytes=need) == D.ERR_WORKSPACE
+
+
+def test_dense_rejects(L):
+    kv, bt = _kv(), _batch()
+    qs = (800 * 8 * 128, 8 * 128, 128)
+    assert L.dense_verify_attn(None, *qs, 8, ctypes.byref(kv), ctypes.byref(kv), ctypes.byref(bt),
+                               0.1, FAKE, *qs, None, 0, None) == D.ERR_INVALID_ARG
+    assert L.dense_verify_attn(FAKE, *qs, 8, ctypes.byref(kv), ctypes.byref(kv), None, 0.1, FAKE,
+                               *qs, None, 0, None) == D.ERR_INVALID_ARG
+
+
+def _score(L, heads=(0, 3), Hq=8, kv=None, bt=None, groups=1, q=FAKE, out=FAKE, ws=FAKE,
+           ws_bytes=1 << 30):
+    kv = kv or _kv()
+    bt = bt or _batch()
+    arr = (ctypes.c_int32 * max(1, len(heads)))(*heads)
+    return L.dustin_score(q, 800 * 8 * 128, 8 * 128, 128, Hq, arr, len(heads), ctypes.byref(kv),
+                          ctypes.byref(bt), 0.1, groups, None, 0, 0, out, 0, 0, ws, ws_bytes, None)
+
+
+def test_score_rejects(L):
+    assert _score(L, heads=(0, 8)) == D.ERR_INVALID_ARG               # head out of range
+    assert _score(L, heads=(2, 2)) == D.ERR_INVALID_ARG               # duplicate head
+    assert _score(L, heads=()) == D.ERR_UNSUPPORTED
+    assert _score(L, heads=tuple(range(17)), Hq=32) == D.ERR_UNSUPPORTED
+    assert _score(L, groups=3) == D.ERR_INVALID_ARG
+    assert _score(L, q=None) == D.ERR_INVALID_ARG
+    assert _score(L, out=None) == D.ERR_INVALID_ARG
+    assert _score(L, kv=_kv(d=96)) == D.ERR_UNSUPPORTED
+    assert _score(L, bt=_batch(nq=17)) == D.ERR_UNSUPPORTED
+    # 5 queries x 4 heads of one KV head exceed one 16-column MFMA tile
+    assert _score(L, heads=(0, 1, 2, 3), bt=_batch(nq=5)) == D.ERR_UNSUPPORTED
+    assert _score(L, ws=None, ws_bytes=0) == D.ERR_WORKSPACE
+    assert _score(L, ws=FAKE + 4) == D.ERR_WORKSPACE
+    assert _score(L, ws_bytes=16) == D.ERR_WORKSPACE
+
+
+def test_product_never_touches_the_oracle():
+    """The HIP path has no CPU fallback and never imports the checker."""
+    pkg = os.path.join(ROOT, "paper_2606_24957_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".hip", ".hpp", ".cpp", ".h")):
+                text = open(os.path.join(dirpath, f)).read()
+                assert not re.search(r"^\s*(import|from)\s+oracle", text, re.M), f
+                assert "liboracle" not in text, f

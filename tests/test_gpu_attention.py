@@ -1,0 +1,206 @@
+"""GPU parity of the verification attention kernels against the oracle (through the C ABI).
+
+Small cases compare every output row; the full-size cases (Qwen2.5-72B-shaped layer, the
+ragged paged batch, the 131k stress layer) compare sampled rows, each of which the oracle
+computes exactly.  Tolerance: per row max|diff| <= 2e-2 and ||diff|| / ||ref|| <= 1e-2.
+"""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import paper_2606_24957_amd as D
+from paper_2606_24957_amd import workloads as W
+from tests.gpu_util import bits, check_attention, gpu_rows, scale_of
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+
+
+def _shape(B, n, t, Hq, Hkv, k, paged=False, seed=7, name="case"):
+    n = tuple(n) if isinstance(n, (list, tuple)) else (n,) * B
+    t = tuple(t) if isinstance(t, (list, tuple)) else (t,) * B
+    base = W.config("qwen72b")
+    return base.replace(name=name, B=B, num_q_heads=Hq, num_kv_heads=Hkv, seq_lens=n, n_query=t,
+                        budget=(k,) * B, m=((k - 20) // 2,) * B, layers=1, seed=seed,
+                        planted=tuple(max(1, x // 100) for x in n), page_size=16 if paged else 0)
+
+
+def _random_selection(s, G, seed, short=()):
+    """Sorted random positions per (b, g); sequences listed in `short` get fewer."""
+    rng = np.random.default_rng(seed)
+    k = s.k_max
+    idx = np.full((s.B, G, k), -1, dtype=np.int32)
+    cnt = np.zeros((s.B, G), dtype=np.int32)
+    for b in range(s.B):
+        for g in range(G):
+            c = min(k, s.seq_lens[b])
+            if b in short:
+                c = c // 3
+            sel = np.sort(rng.choice(s.seq_lens[b], c, replace=False)) if c else np.zeros(0)
+            idx[b, g, :c] = sel
+            cnt[b, g] = c
+    return idx, cnt
+
+
+def _run_sparse_case(s, G=1, seed=0, rows=None, short=()):
+    L = W.make_layer(s, 0, DEV)
+    seq = torch.tensor(s.seq_lens, dtype=torch.int32, device=DEV)
+    nq = torch.tensor(s.n_query, dtype=torch.int32, device=DEV)
+    idx_np, cnt_np = _random_selection(s, G, seed, short)
+    idx, cnt = torch.from_numpy(idx_np).to(DEV), torch.from_numpy(cnt_np).to(DEV)
+    out = torch.full_like(L.q, float("nan"))
+    D.sparse_verify_attn(L.q, L.k, L.v, idx, cnt, seq, n_query=nq, page_table=L.page_table, out=out)
+    torch.cuda.synchronize()
+    kk, vv = L.contiguous_kv(s)
+    if rows is None:
+        rows = O.all_rows(s.B, s.n_query, s.num_q_heads)
+    ref = O.attention(bits(L.q), bits(kk), bits(vv), s.seq_lens, scale_of(s.head_dim), rows,
+                      idx=idx_np, count=cnt_np)
+    check_attention(gpu_rows(out, rows), ref, s.name + " sparse")
+    o = out.float().cpu()
+    for b, t in enumerate(s.n_query):                  # rows t >= T_b are never written
+        assert torch.isnan(o[b, t:]).all()
+    return L, out
+
+
+def _run_dense_case(s, L=None, rows=None):
+    L = L or W.make_layer(s, 0, DEV)
+    seq = torch.tensor(s.seq_lens, dtype=torch.int32, device=DEV)
+    nq = torch.tensor(s.n_query, dtype=torch.int32, device=DEV)
+    out = D.dense_verify_attn(L.q, L.k, L.v, seq, n_query=nq, page_table=L.page_table)
+    torch.cuda.synchronize()
+    kk, vv = L.contiguous_kv(s)
+    if rows is None:
+        rows = O.all_rows(s.B, s.n_query, s.num_q_heads)
+    ref = O.attention(bits(L.q), bits(kk), bits(vv), s.seq_lens, scale_of(s.head_dim), rows)
+    check_attention(gpu_rows(out, rows), ref, s.name + " dense")
+    return out
+
+
+CASES = {
+    # name: (B, N, T, Hq, Hkv, k, paged)
+    "tiny_b1_h8_kv1": (1, 2048, 5, 8, 1, 256, False),
+    "qwen7b_like": (2, [1500, 1111], 5, 28, 4, 256, False),
+    "qwen72b_like": (2, 1300, 5, 64, 8, 300, False),
+    "single_query": (1, 777, 1, 8, 1, 100, False),
+    "gamma8_rows72": (2, 900, 9, 64, 8, 200, False),
+    "group16_rows64": (1, 1000, 4, 32, 2, 128, False),
+    "ragged_paged": (3, [700, 1234, 95], [3, 9, 6], 64, 8, 160, True),
+}
+
+
+@pytest.mark.parametrize("name", sorted(CASES))
+def test_sparse_matches_oracle(name):
+    B, n, t, Hq, Hkv, k, paged = CASES[name]
+    _run_sparse_case(_shape(B, n, t, Hq, Hkv, k, paged, name=name), G=1, seed=3, short=(0,))
+
+
+@pytest.mark.parametrize("name", ["qwen7b_like", "single_query", "ragged_paged", "gamma8_rows72"])
+def test_dense_matches_oracle(name):
+    B, n, t, Hq, Hkv, k, paged = CASES[name]
+    _run_dense_case(_shape(B, n, t, Hq, Hkv, k, paged, name=name))
+
+
+def test_sparse_per_kv_head_groups():
+    s = _shape(2, 800, 5, 64, 8, 128, name="groups_hkv")
+    _run_sparse_case(s, G=8, seed=5)
+
+
+def test_sparse_tiny_sequences_and_empty_selection():
+    """N_b smaller than a tile, N_b = 0 (window only) and an empty selection."""
+    s = _shape(3, [5, 0, 40], [5, 3, 2], 16, 2, 32, name="tiny_seqs")
+    L = W.make_layer(s, 0, DEV)
+    seq = torch.tensor(s.seq_lens, dtype=torch.int32, device=DEV)
+    nq = torch.tensor(s.n_query, dtype=torch.int32, device=DEV)
+    idx_np = np.full((3, 1, 32), -1, dtype=np.int32)
+    idx_np[0, 0, :5] = np.arange(5)
+    idx_np[2, 0, :0] = 0
+    cnt_np = np.array([[5], [0], [0]], dtype=np.int32)
+    out = D.sparse_verify_attn(L.q, L.k, L.v, torch.from_numpy(idx_np).to(DEV),
+                               torch.from_numpy(cnt_np).to(DEV), seq, n_query=nq)
+    torch.cuda.synchronize()
+    rows = O.all_rows(3, s.n_query, 16)
+    ref = O.attention(bits(L.q), bits(L.k), bits(L.v), s.seq_lens, scale_of(128), rows,
+                      idx=idx_np, count=cnt_np)
+    check_attention(gpu_rows(out, rows), ref, "tiny_seqs")
+
+
+def test_full_budget_sparse_equals_dense():
+    s = _shape(2, 600, 5, 64, 8, 600, name="full_budget")
+    L = W.make_layer(s, 0, DEV)
+    seq = torch.tensor(s.seq_lens, dtype=torch.int32, device=DEV)
+    idx = torch.arange(600, dtype=torch.int32, device=DEV).expand(2, 1, 600).contiguous()
+    cnt = torch.full((2, 1), 600, dtype=torch.int32, device=DEV)
+    sp = D.sparse_verify_attn(L.q, L.k, L.v, idx, cnt, seq).float()
+    de = D.dense_verify_attn(L.q, L.k, L.v, seq).float()
+    torch.cuda.synchronize()
+    assert (sp - de).abs().max().item() < 1e-2
+
+
+@pytest.mark.parametrize("splits", [1, 2, 5, 16])
+def test_split_counts_agree_and_are_deterministic(splits, monkeypatch):
+    monkeypatch.setenv("DUSTIN_ATTN_SPLITS", str(splits))
+    s = _shape(2, 2000, 5, 64, 8, 700, name=f"splits{splits}")
+    L, out = _run_sparse_case(s, G=1, seed=9)
+    seq = torch.tensor(s.seq_lens, dtype=torch.int32, device=DEV)
+    idx_np, cnt_np = _random_selection(s, 1, 9, ())
+    idx, cnt = torch.from_numpy(idx_np).to(DEV), torch.from_numpy(cnt_np).to(DEV)
+    a = D.sparse_verify_attn(L.q, L.k, L.v, idx, cnt, seq)
+    b = D.sparse_verify_attn(L.q, L.k, L.v, idx, cnt, seq)
+    torch.cuda.synchronize()
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+    dn = _run_dense_case(s, L)
+    dn2 = D.dense_verify_attn(L.q, L.k, L.v, seq)
+    torch.cuda.synchronize()
+    assert torch.equal(dn.view(torch.int16), dn2.view(torch.int16))
+
+
+def _sample_rows(s, n, seed):
+    rng = np.random.default_rng(seed)
+    rows = []
+    for _ in range(n):
+        b = int(rng.integers(s.B))
+        rows.append((b, int(rng.integers(s.n_query[b])), int(rng.integers(s.num_q_heads))))
+    rows.append((s.B - 1, s.n_query[s.B - 1] - 1, s.num_q_heads - 1))
+    return np.asarray(rows, dtype=np.int32)
+
+
+def _full_size_sampled(s, n_rows=48, seed=11):
+    """One full-size layer; the oracle recomputes sampled rows from host copies of the
+    sampled sequences only."""
+    L = W.make_layer(s, 0, DEV)
+    seq = torch.tensor(s.seq_lens, dtype=torch.int32, device=DEV)
+    nq = torch.tensor(s.n_query, dtype=torch.int32, device=DEV)
+    idx_np, cnt_np = _random_selection(s, 1, seed)
+    idx, cnt = torch.from_numpy(idx_np).to(DEV), torch.from_numpy(cnt_np).to(DEV)
+    sp = D.sparse_verify_attn(L.q, L.k, L.v, idx, cnt, seq, n_query=nq, page_table=L.page_table)
+    de = D.dense_verify_attn(L.q, L.k, L.v, seq, n_query=nq, page_table=L.page_table)
+    torch.cuda.synchronize()
+    rows = _sample_rows(s, n_rows, seed)
+    kk, vv = L.contiguous_kv(s)
+    for b in sorted(set(rows[:, 0].tolist())):
+        sel = rows[rows[:, 0] == b].copy()
+        sel[:, 0] = 0
+        qb, kb, vb = bits(L.q[b:b + 1]), bits(kk[b:b + 1]), bits(vv[b:b + 1])
+        ref_s = O.attention(qb, kb, vb, [s.seq_lens[b]], scale_of(128), sel,
+                            idx=idx_np[b:b + 1], count=cnt_np[b:b + 1])
+        ref_d = O.attention(qb, kb, vb, [s.seq_lens[b]], scale_of(128), sel)
+        got = rows[rows[:, 0] == b]
+        check_attention(gpu_rows(sp, got), ref_s, f"{s.name} sparse b={b}")
+        check_attention(gpu_rows(de, got), ref_d, f"{s.name} dense b={b}")
+
+
+def test_full_size_qwen72b_layer():
+    _full_size_sampled(W.config("qwen72b").replace(layers=1))
+
+
+def test_full_size_ragged_paged_layer():
+    _full_size_sampled(W.config("ragged").replace(layers=1))
+
+
+@pytest.mark.skipif(os.environ.get("DUSTIN_SKIP_131K") == "1", reason="131k layer skipped by request")
+def test_full_size_131k_layer():
+    _full_size_sampled(W.config("long131k").replace(layers=1), n_rows=24)

@@ -1,0 +1,93 @@
+"""GPU scoring-head importance (Eq. 5) against the oracle: every score within
+1e-4 * max(|S_ref|, 1/N_b), plus the row-sum invariant sum_n (S - init) = nq_b * |H|."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import paper_2606_24957_amd as D
+from paper_2606_24957_amd import workloads as W
+from tests.gpu_util import bits, check_score, host, scale_of
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+
+
+def _case(B, N, nq, Hq, Hkv, d, heads, groups=1, with_init=True, seed=0, n_list=None):
+    g = torch.Generator(device=DEV).manual_seed(seed)
+    ncap = max(n_list) if n_list else N
+    q = torch.randn((B, nq, Hq, d), generator=g, device=DEV).to(torch.bfloat16)
+    k = torch.randn((B, ncap, Hkv, d), generator=g, device=DEV).to(torch.bfloat16)
+    k[:, 7] = (3.0 * q[:, 0, 0]).to(torch.bfloat16).unsqueeze(1).expand(B, Hkv, d)  # a salient key
+    seq = n_list or [N] * B
+    init = None
+    if with_init:
+        init = torch.rand((B, groups, ncap), generator=g, device=DEV) / ncap
+    out = torch.full((B, groups, ncap), -5.0, device=DEV)
+    D.score(q, k, torch.tensor(seq, dtype=torch.int32, device=DEV), heads, groups=groups,
+            init=init, out=out, n_query=torch.tensor([nq] * B, dtype=torch.int32, device=DEV))
+    torch.cuda.synchronize()
+    ref = O.score(bits(q), bits(k), seq, [nq] * B, heads, scale_of(d), num_kv_heads=Hkv,
+                  groups=groups, init=None if init is None else host(init))
+    got = host(out)
+    for b in range(B):
+        for go in range(groups):
+            n = seq[b]
+            check_score(got[b, go, :n], ref[b, go, :n], n, f"b={b} g={go}")
+            assert np.all(got[b, go, n:] == -5.0)          # positions >= N_b untouched
+            base = 0 if init is None else host(init)[b, go, :n].astype(np.float64).sum()
+            hs = [h for h in heads if groups == 1 or h // (Hq // Hkv) == go]
+            assert abs(got[b, go, :n].astype(np.float64).sum() - base - nq * len(hs)) <= 1e-4 * nq * max(1, len(hs))
+    return got
+
+
+def test_score_target_shape():
+    """Target scoring: last token's query, 4 heads in 4 distinct KV heads, d = 128."""
+    _case(3, 5000, 1, 64, 8, 128, [0, 17, 34, 51], with_init=True)
+
+
+def test_score_draft_shape():
+    """Draft scoring: Gamma = 4 queries, heads {0, 4, 7, 11} over 2 KV heads, d = 64."""
+    _case(2, 4100, 4, 14, 2, 64, [0, 4, 7, 11], with_init=False)
+
+
+def test_score_per_group_and_ragged():
+    _case(3, 0, 2, 64, 8, 128, [0, 9, 63], groups=8, n_list=[3000, 1025, 17])
+
+
+def test_score_layer_chaining_accumulates():
+    """init aliasing out accumulates draft layers like a sum over layers in Eq. 5."""
+    B, N, nq, Hq, Hkv, d, heads = 2, 2048, 4, 14, 2, 64, [0, 4, 7, 11]
+    g = torch.Generator(device=DEV).manual_seed(3)
+    seq = torch.tensor([N, N - 100], dtype=torch.int32, device=DEV)
+    acc = torch.zeros((B, 1, N), device=DEV)
+    ref = np.zeros((B, 1, N), dtype=np.float32)
+    for _ in range(3):
+        q = torch.randn((B, nq, Hq, d), generator=g, device=DEV).to(torch.bfloat16)
+        k = torch.randn((B, N, Hkv, d), generator=g, device=DEV).to(torch.bfloat16)
+        D.score(q, k, seq, heads, init=acc, out=acc)
+        ref = O.score(bits(q), bits(k), [N, N - 100], [nq] * B, heads, scale_of(d), init=ref.copy())
+    torch.cuda.synchronize()
+    got = host(acc)
+    for b, n in enumerate([N, N - 100]):
+        check_score(got[b, 0, :n], ref[b, 0, :n], n, f"chain b={b}")
+
+
+def test_score_full_size_target_and_draft():
+    """Qwen2.5-72B-shaped target scoring layer and one Qwen2.5-0.5B-shaped draft layer at
+    B = 16, N = 32768; the oracle checks four sequences."""
+    s = W.config("qwen72b").replace(layers=1)
+    L = W.make_layer(s, 0, DEV)
+    E = W.make_estimation(s, L, DEV)
+    seq = torch.tensor(s.seq_lens, dtype=torch.int32, device=DEV)
+    st = D.score(E.q_target, L.k, seq, s.target_heads, max_len=s.n_max)
+    sd = D.score(E.draft_q[0], E.draft_k[0], seq, s.draft.heads, max_len=s.n_max,
+                 n_query=torch.tensor(s.draft_gamma, dtype=torch.int32, device=DEV))
+    torch.cuda.synchronize()
+    for b in (0, 5, 10, 15):
+        rt = O.score(bits(E.q_target[b:b + 1]), bits(L.k[b:b + 1]), [s.seq_lens[b]], [1],
+                     s.target_heads, scale_of(128), num_kv_heads=8)
+        check_score(host(st)[b, 0, :s.seq_lens[b]], rt[0, 0, :s.seq_lens[b]], s.seq_lens[b], f"target b={b}")
+        rd = O.score(bits(E.draft_q[0][b:b + 1]), bits(E.draft_k[0][b:b + 1]), [s.seq_lens[b]],
+                     [s.draft_gamma[b]], s.draft.heads, scale_of(64), num_kv_heads=2)
+        check_score(host(sd)[b, 0, :s.seq_lens[b]], rd[0, 0, :s.seq_lens[b]], s.seq_lens[b], f"draft b={b}")

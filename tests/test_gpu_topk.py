@@ -1,0 +1,113 @@
+"""GPU tiered selection (Eq. 6) against the oracle: on identical fp32 score vectors the
+index set, its ascending order and the count must match bit for bit."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import paper_2606_24957_amd as D
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+
+
+def _compare(sd, st, seq, k_max, budget=None, m=None, m_scalar=None, groups=1, ns=4, nw=16):
+    B = len(seq)
+    P = ns + nw
+    if m_scalar is None:
+        m_scalar = 0 if sd is None else (k_max - P if st is None else (k_max - P) // 2)
+    idx_ref, cnt_ref = O.select(sd, st, seq, k_max, budget=budget, m=m, m_scalar=m_scalar,
+                                n_sink=ns, n_window=nw, groups=groups)
+    tdev = lambda a: None if a is None else torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+    idx = torch.full((B, groups, k_max), -7, dtype=torch.int32, device=DEV)
+    idx_g, cnt_g = D.topk(tdev(sd), tdev(st), tdev(np.asarray(seq, np.int32)), k_max,
+                          budget=tdev(None if budget is None else np.asarray(budget, np.int32)),
+                          m=tdev(None if m is None else np.asarray(m, np.int32)),
+                          m_scalar=m_scalar, n_sink=ns, n_window=nw, groups=groups, idx=idx)
+    torch.cuda.synchronize()
+    cnt_g = cnt_g.cpu().numpy()
+    idx_g = idx_g.cpu().numpy()
+    np.testing.assert_array_equal(cnt_g, cnt_ref)
+    for b in range(B):
+        for g in range(groups):
+            c = cnt_ref[b, g]
+            np.testing.assert_array_equal(idx_g[b, g, :c], idx_ref[b, g, :c], err_msg=f"b={b} g={g}")
+            assert np.all(idx_g[b, g, c:] == -7)          # entries past count untouched
+    return idx_g, cnt_g
+
+
+def _scores(kind, B, N, seed):
+    rng = np.random.default_rng(seed)
+    if kind == "uniform":
+        x = rng.random((B, 1, N))
+    elif kind == "dirichlet":
+        x = rng.gamma(0.1, size=(B, 1, N))
+        x /= x.sum(-1, keepdims=True)
+    elif kind == "quantized":
+        x = rng.integers(0, 7, (B, 1, N)) / 7.0
+    elif kind == "equal":
+        x = np.full((B, 1, N), 0.25)
+    elif kind == "zeros":
+        x = np.where(rng.random((B, 1, N)) < 0.97, 0.0, rng.random((B, 1, N)))
+        x = np.where(rng.random((B, 1, N)) < 0.5, -0.0, x)
+    elif kind == "signed":
+        x = rng.standard_normal((B, 1, N)) * 1e3
+    elif kind == "special":
+        x = rng.standard_normal((B, 1, N))
+        for v in (np.inf, -np.inf, np.nan, -np.nan, 1e-45, -1e-45, 3.4e38):
+            x[:, :, rng.integers(0, N, 20)] = v
+    else:
+        raise KeyError(kind)
+    return x.astype(np.float32)
+
+
+@pytest.mark.parametrize("kind", ["uniform", "dirichlet", "quantized", "equal", "zeros", "signed", "special"])
+def test_topk_bit_exact(kind):
+    B, N, k = 4, 5000, 512
+    _compare(_scores(kind, B, N, 1), _scores(kind, B, N, 2), [N] * B, k)
+
+
+@pytest.mark.parametrize("N", [21, 33, 1000, 4097, 32768, 131072])
+def test_topk_lengths(N):
+    k = min(2048, max(20, N // 8))
+    _compare(_scores("uniform", 2, N, N), _scores("dirichlet", 2, N, N + 1), [N, N - 1], k)
+
+
+def test_topk_short_sequences_take_all():
+    N = 600
+    _compare(_scores("uniform", 3, N, 3), _scores("uniform", 3, N, 4), [600, 100, 0], 256)
+
+
+def test_topk_variants_target_only_and_draft_only():
+    B, N, k = 2, 3000, 300
+    sd, st = _scores("uniform", B, N, 5), _scores("uniform", B, N, 6)
+    _compare(None, st, [N] * B, k, m_scalar=0)
+    _compare(sd, None, [N] * B, k, m_scalar=k - 20)
+    _compare(sd, st, [N] * B, k, m_scalar=0)
+    _compare(sd, st, [N] * B, k, m_scalar=k - 20)
+
+
+def test_topk_per_sequence_budget_m_and_groups():
+    B, G, N = 3, 8, 4096
+    rng = np.random.default_rng(9)
+    sd = _scores("uniform", B, N, 7)                           # broadcast over groups
+    st = rng.random((B, G, N)).astype(np.float32)
+    seq = [4096, 3000, 50]
+    budget = [256, 300, 64]
+    m = [100, 0, 22]
+    _compare(sd, st, seq, 320, budget=budget, m=m, groups=G)
+
+
+def test_topk_streaming_llm_closed_form():
+    """n_window = k - 4 with m = 0 gives sinks + the most recent k - 4 positions."""
+    N, k = 10000, 256
+    idx, cnt = _compare(None, _scores("uniform", 1, N, 8), [N], k, m_scalar=0, nw=k - 4)
+    assert idx[0, 0, :k].tolist() == list(range(4)) + list(range(N - k + 4, N))
+
+
+def test_topk_deterministic_repeat():
+    B, N, k = 16, 32768, 2048
+    sd, st = _scores("quantized", B, N, 10), _scores("zeros", B, N, 11)
+    a, _ = _compare(sd, st, [N] * B, k)
+    b, _ = _compare(sd, st, [N] * B, k)
+    assert np.array_equal(a, b)
