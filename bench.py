@@ -1,0 +1,377 @@
+#!/usr/bin/env python3
+"""Benchmark of the Dustin sparse verification step on one MI355X.
+
+One step is every stage of the hot path on one batch of synthetic input, with the inputs
+resident in HBM:
+    target scoring-head importance        (Eq. 5, target half)
+    draft scoring-head importance x 3     (Eq. 5, draft half, one call per draft layer)
+    tiered hybrid selection               (Eq. 6)
+    sparse verification attention x L     (one global index set reused by all L layers)
+    dense full-cache verification x L     (the comparison the paper normalises against)
+HIP events on the launch stream separate the stages.  Prints ONE JSON line; every other
+message goes to stderr.
+
+    python bench.py [--gpus 1] [--steps 30] [--warmup 5] [--workload qwen72b] [--k 2048]
+"""
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBPS = 8000.0           # MI355X HBM3E, vendor figure
+SPARSE_KERNEL = "verify_attn_kernel"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    p = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=30)
+    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--workload", default="qwen72b",
+                   choices=["tiny", "qwen7b", "qwen72b", "ragged", "long131k"])
+    p.add_argument("--k", type=int, default=None, help="override the budget k (e.g. 512)")
+    p.add_argument("--layers", type=int, default=None, help="override the stacked layer count")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-sample-seqs", type=int, default=16)
+    p.add_argument("--copy-probe", action="store_true",
+                   help="also run one plain 1 GiB device copy (counter calibration)")
+    p.add_argument("--only", choices=["all", "sparse", "dense", "estimate"], default="all",
+                   help="restrict the timed step (profiling runs)")
+    return p.parse_args()
+
+
+# ----------------------------------------------------------------------------- bytes
+
+def sparse_bytes(s):
+    """Algorithmic HBM bytes of one sparse layer: gathered K and V rows of every KV head
+    (selected + verification window), Q read, O written, the index list read (+ one page
+    table entry per gathered token when paged)."""
+    tot = 0
+    for n, t, k in zip(s.seq_lens, s.n_query, s.budget):
+        kk = min(k, n)
+        tot += s.num_kv_heads * (kk + t) * s.head_dim * 2 * 2
+        tot += 2 * t * s.num_q_heads * s.head_dim * 2
+        tot += s.groups * kk * 4
+        if s.page_size:
+            tot += s.num_kv_heads * (kk + t) * 4
+    return tot
+
+
+def dense_bytes(s):
+    tot = 0
+    for n, t in zip(s.seq_lens, s.n_query):
+        tot += s.num_kv_heads * (n + t) * s.head_dim * 2 * 2
+        tot += 2 * t * s.num_q_heads * s.head_dim * 2
+        if s.page_size:
+            tot += s.num_kv_heads * (n + t) * 4
+    return tot
+
+
+def score_bytes(s, target=True):
+    """Distinct KV heads touched by the scoring heads, read once, plus S written (and the
+    historical init read)."""
+    if target:
+        gs = s.num_q_heads // s.num_kv_heads
+        kvh = len({h // gs for h in s.target_heads})
+        return sum(kvh * n * s.head_dim * 2 + 4 * n * (1 + (s.init_kind is not None))
+                   for n in s.seq_lens)
+    d = s.draft
+    gs = d.num_q_heads // d.num_kv_heads
+    kvh = len({h // gs for h in d.heads})
+    per_layer = sum(kvh * n * d.head_dim * 2 for n in s.seq_lens)
+    return d.layers * per_layer + sum(4 * n for n in s.seq_lens) * (2 * d.layers - 1)
+
+
+def topk_bytes(s):
+    return sum(2 * 4 * n + 4 * min(k, n) for n, k in zip(s.seq_lens, s.budget))
+
+
+# ----------------------------------------------------------------------------- traffic
+
+def kernel_sources_sha():
+    h = hashlib.sha256()
+    for f in ("attn.hip", "common.hpp", "kernels.hpp"):
+        with open(os.path.join(ROOT, "paper_2606_24957_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload, k):
+    """HBM bytes per sparse launch from the committed rocprofv3 counter summary, or None
+    when it is missing or was taken on different kernel sources."""
+    path = os.path.join(ROOT, "profiles", f"hbm_traffic_sparse_verify_attn_{workload}_k{k}.md")
+    if not os.path.exists(path):
+        return None
+    m = re.search(r"<!--\s*traffic:\s*(\{.*?\})\s*-->", open(path).read(), re.S)
+    if not m:
+        return None
+    rec = json.loads(m.group(1))
+    if rec.get("source_sha256") != kernel_sources_sha():
+        return None
+    return rec.get("bytes_per_launch")
+
+
+# ----------------------------------------------------------------------------- CPU baseline
+
+def cpu_baseline(s, layer0, est, n_seq):
+    """The oracle as it stands, on the host cores, for the first n_seq sequences of the same
+    synthetic batch: target + draft scoring, selection, one sparse layer, one dense layer;
+    times scaled to the whole batch."""
+    import numpy as np
+    import oracle as O
+    from paper_2606_24957_amd.workloads import bf16_bits
+
+    nb = min(n_seq, s.B)
+    sl = slice(0, nb)
+    seq = list(s.seq_lens[:nb])
+    nq = list(s.n_query[:nb])
+    scale = 1.0 / (s.head_dim ** 0.5)
+    kk, vv = layer0.contiguous_kv(s)
+    q = bf16_bits(layer0.q[sl])
+    k = bf16_bits(kk[sl])
+    v = bf16_bits(vv[sl])
+    times = {}
+    t0 = time.perf_counter()
+    init = None if est.init_target is None else est.init_target[sl].cpu().numpy()
+    st = O.score(bf16_bits(est.q_target[sl]), k, seq, [1] * nb, s.target_heads, scale, init=init)
+    times["score_target"] = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    if est.s_draft_given is not None:
+        sd = est.s_draft_given[sl].cpu().numpy()
+    else:
+        sd = None
+        dscale = 1.0 / (s.draft.head_dim ** 0.5)
+        for l in range(s.draft.layers):
+            sd = O.score(bf16_bits(est.draft_q[l][sl]), bf16_bits(est.draft_k[l][sl]), seq,
+                         [t - 1 for t in nq], s.draft.heads, dscale, init=sd)
+    times["score_draft"] = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    idx, cnt = O.select(sd, st, seq, s.k_max, budget=s.budget[:nb], m=s.m[:nb])
+    times["select"] = time.perf_counter() - t0
+    rows = O.all_rows(nb, nq, s.num_q_heads)
+    t0 = time.perf_counter()
+    O.attention(q, k, v, seq, scale, rows, idx=idx, count=cnt)
+    times["sparse_layer"] = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    O.attention(q, k, v, seq, scale, rows)
+    times["dense_layer"] = time.perf_counter() - t0
+    f = s.B / nb
+    us = {key: val * f * 1e6 for key, val in times.items()}
+    return {
+        "value": round(us["sparse_layer"], 1),
+        "unit": "us/layer",
+        "cores": O.max_threads(),
+        "kind": "oracle",
+        "sample": (f"sequences 0..{nb - 1} of {s.B} of layer 0 (same synthetic bytes), full "
+                   f"oracle step: target+draft scoring, selection, one sparse and one dense "
+                   f"layer; times scaled x{f:g} to the batch"),
+        "dense_us_per_layer": round(us["dense_layer"], 1),
+        "estimation_us_per_step": round(us["score_target"] + us["score_draft"] + us["select"], 1),
+        "wall_s": round(sum(times.values()), 2),
+    }
+
+
+# ----------------------------------------------------------------------------- main
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        log(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the data-parallel "
+            "path shards by sequence or KV head with no exchange inside a layer, see DESIGN.md")
+        sys.exit(2)
+    import torch
+    import paper_2606_24957_amd as D
+    from paper_2606_24957_amd import workloads as W
+
+    if not torch.cuda.is_available():
+        log("no GPU visible: bench.py needs an MI355X")
+        sys.exit(3)
+    D.lib()  # fails loudly when libdustin.so is missing
+    dev = "cuda"
+    s = W.config(args.workload)
+    if args.k is not None:
+        s = s.replace(budget=(args.k,) * s.B, m=((args.k - s.n_sink - s.n_window) // 2,) * s.B)
+    if args.layers is not None:
+        s = s.replace(layers=args.layers)
+    L = s.layers
+    log(f"[bench] workload {s.name}: B={s.B} N={s.n_max} Hq={s.num_q_heads} Hkv={s.num_kv_heads} "
+        f"T={s.t_max} k={s.k_max} layers={L} paged={bool(s.page_size)}")
+    t0 = time.perf_counter()
+    layers = [W.make_layer(s, l, dev) for l in range(L)]
+    est = W.make_estimation(s, layers[0], dev)
+    torch.cuda.synchronize()
+    log(f"[bench] inputs generated in {time.perf_counter() - t0:.1f}s")
+
+    B, N = s.B, s.n_max
+    seq = torch.tensor(s.seq_lens, dtype=torch.int32, device=dev)
+    nq = torch.tensor(s.n_query, dtype=torch.int32, device=dev)
+    gam = torch.tensor(s.draft_gamma, dtype=torch.int32, device=dev)
+    bud = torch.tensor(s.budget, dtype=torch.int32, device=dev)
+    mm = torch.tensor(s.m, dtype=torch.int32, device=dev)
+    s_t = torch.zeros((B, 1, N), dtype=torch.float32, device=dev)
+    s_d = torch.zeros((B, 1, N), dtype=torch.float32, device=dev)
+    idx = torch.zeros((B, s.groups, s.k_max), dtype=torch.int32, device=dev)
+    cnt = torch.zeros((B, s.groups), dtype=torch.int32, device=dev)
+    outs = [torch.empty_like(l.q) for l in layers]
+    outs_d = [torch.empty_like(l.q) for l in layers]
+
+    # prepared launches (arguments marshalled once)
+    score_t = D.plan_score(est.q_target, layers[0].k, seq, s.target_heads, init=est.init_target,
+                           out=s_t, max_len=N, page_table=layers[0].page_table)
+    score_d = []
+    if est.s_draft_given is not None:
+        s_d.copy_(est.s_draft_given)
+    else:
+        for l in range(s.draft.layers):
+            score_d.append(D.plan_score(est.draft_q[l], est.draft_k[l], seq, s.draft.heads,
+                                        n_query=gam, init=None if l == 0 else s_d, out=s_d,
+                                        max_len=N))
+    sel = D.plan_topk(s_d, s_t, seq, s.k_max, budget=bud, m=mm, n_sink=s.n_sink,
+                      n_window=s.n_window, groups=s.groups, idx=idx, count=cnt)
+    sparse = [D.plan_sparse_verify_attn(l.q, l.k, l.v, idx, cnt, seq, n_query=nq,
+                                        page_table=l.page_table, out=o)
+              for l, o in zip(layers, outs)]
+    dense = [D.plan_dense_verify_attn(l.q, l.k, l.v, seq, n_query=nq, page_table=l.page_table,
+                                      out=o) for l, o in zip(layers, outs_d)]
+
+    def ev():
+        e = torch.cuda.Event(enable_timing=True)
+        e.record()
+        return e
+
+    def step(rec):
+        marks = [ev()] if rec else None
+        if args.only in ("all", "estimate", "sparse"):
+            score_t()
+            if rec: marks.append(ev())
+            for c in score_d:
+                c()
+            if rec: marks.append(ev())
+            sel()
+            if rec: marks.append(ev())
+        if args.only in ("all", "sparse"):
+            for c in sparse:
+                c()
+                if rec: marks.append(ev())
+        if args.only in ("all", "dense"):
+            for c in dense:
+                c()
+                if rec: marks.append(ev())
+        return marks
+
+    for _ in range(args.warmup):
+        step(False)
+    torch.cuda.synchronize()
+    if args.copy_probe:
+        a = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        b_ = torch.empty_like(a)
+        b_.copy_(a)
+        torch.cuda.synchronize()
+        del a, b_
+    all_marks = []
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for _ in range(args.steps):
+        all_marks.append(step(True))
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
+    ms_per_step = wall * 1e3 / args.steps
+
+    # per-stage durations from the events (ms)
+    est_t, est_d, est_k, sp, dn = [], [], [], [], []
+    for m in all_marks:
+        i = 0
+        if args.only in ("all", "estimate", "sparse"):
+            est_t.append(m[0].elapsed_time(m[1]))
+            est_d.append(m[1].elapsed_time(m[2]))
+            est_k.append(m[2].elapsed_time(m[3]))
+            i = 3
+        if args.only in ("all", "sparse"):
+            sp += [m[i + j].elapsed_time(m[i + j + 1]) for j in range(L)]
+            i += L
+        if args.only in ("all", "dense"):
+            dn += [m[i + j].elapsed_time(m[i + j + 1]) for j in range(L)]
+
+    def med(x):
+        x = sorted(x)
+        return x[len(x) // 2] if x else float("nan")
+
+    def mean(x):
+        return sum(x) / len(x) if x else float("nan")
+
+    sp_us, dn_us = mean(sp) * 1e3, mean(dn) * 1e3
+    est_us = (mean(est_t) + mean(est_d) + mean(est_k)) * 1e3
+    sb, db = sparse_bytes(s), dense_bytes(s)
+    eb = score_bytes(s, True) + (0 if est.s_draft_given is not None else score_bytes(s, False)) + topk_bytes(s)
+    achieved = sb / (sp_us * 1e-6) / 1e9 if sp else float("nan")
+    dense_gbps = db / (dn_us * 1e-6) / 1e9 if dn else float("nan")
+    log(f"[bench] sparse {sp_us:.2f} us/layer (median {med(sp) * 1e3:.2f}) = {achieved:.0f} GB/s on "
+        f"{sb / 1e6:.1f} MB; dense {dn_us:.1f} us/layer = {dense_gbps:.0f} GB/s; estimation "
+        f"{est_us:.1f} us/step (target {mean(est_t) * 1e3:.1f}, draft {mean(est_d) * 1e3:.1f}, "
+        f"topk {mean(est_k) * 1e3:.1f}); {ms_per_step:.3f} ms/step wall")
+
+    cpu = None
+    if not args.no_cpu_baseline and args.only == "all":
+        log("[bench] timing the oracle on the host cores ...")
+        cpu = cpu_baseline(s, layers[0], est, args.cpu_sample_seqs)
+        log(f"[bench] oracle: {cpu}")
+
+    traffic = measured_traffic(s.name, s.k_max)
+    rec = {
+        "metric": "sparse verify-attention us/layer + achieved HBM GB/s, B=16 ctx=32k 72B-shape",
+        "value": round(sp_us, 3),
+        "unit": "us/layer",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded; Qwen2.5-72B/0.5B-shaped attention, planted salient keys)",
+        "config": {
+            "workload": s.name, "batch": B, "context": N, "num_q_heads": s.num_q_heads,
+            "num_kv_heads": s.num_kv_heads, "head_dim": s.head_dim, "verify_queries": s.t_max,
+            "budget_k": s.k_max, "draft_share_m": s.m[0], "sinks": s.n_sink, "window": s.n_window,
+            "scoring_heads": list(s.target_heads),
+            "draft_scoring": None if s.draft is None else
+            {"layers": s.draft.layers, "heads": list(s.draft.heads), "kv_heads": s.draft.num_kv_heads,
+             "head_dim": s.draft.head_dim},
+            "stacked_layers": L, "paged": bool(s.page_size), "selection_groups": s.groups,
+        },
+        "achieved_GBps": round(achieved, 1),
+        "roofline": {
+            "bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+            "frac": round(achieved / PEAK_HBM_GBPS, 4), "traffic": traffic,
+            "kernel": SPARSE_KERNEL + " (sparse)", "bytes_per_launch": sb,
+            "avg_launch_us": round(sp_us, 3),
+        },
+        "dense": {"us_per_layer": round(dn_us, 3), "GBps": round(dense_gbps, 1), "bytes_per_launch": db,
+                  "frac": round(dense_gbps / PEAK_HBM_GBPS, 4)},
+        "estimation": {"us_per_step": round(est_us, 3), "target_score_us": round(mean(est_t) * 1e3, 3),
+                       "draft_score_us": round(mean(est_d) * 1e3, 3), "topk_us": round(mean(est_k) * 1e3, 3),
+                       "bytes": eb, "GBps": round(eb / (est_us * 1e-6) / 1e9, 1) if est_us == est_us else None},
+        "speedup": {
+            "per_layer": round(dn_us / sp_us, 3) if sp else None,
+            f"per_step_L{L}": round(L * dn_us / (est_us + L * sp_us), 3) if sp else None,
+            "per_step_L80": round(80 * dn_us / (est_us + 80 * sp_us), 3) if sp else None,
+        },
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

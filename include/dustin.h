@@ -62,7 +62,8 @@ typedef enum {
  *       data[b * stride_b + n * stride_n + g * stride_h + c],  n < capacity
  *   paged: position n of sequence b lives in physical page p = page_table[b * max_pages +
  *       n / page_size] at data[p * stride_page + (n % page_size) * stride_n + g * stride_h + c];
- *       capacity = max_pages * page_size, p < num_pages. */
+ *       capacity = max_pages * page_size, p < num_pages, num_pages * page_size < 2^31.
+ *       K and V of one attention call must share the same page table and page size. */
 typedef struct {
   const void* data;
   int32_t num_kv_heads;
@@ -169,9 +170,9 @@ dustin_status dustin_topk(const float* s_draft, int64_t d_sb, int64_t d_sg,
  *        count int32 [B * groups] (as written by dustin_topk)
  *   out  bf16 [B, nq_max, num_q_heads, 128] (strides o_sb, o_st, o_sh); rows t >= T_b
  *        are not written.  Round to nearest even.
- *   workspace  dustin_attn_workspace(..., sparse = 1) bytes, 256-byte aligned, whose
- *        first 4096 bytes must be zero before the first call (they are zero again
- *        after every call)
+ *   workspace  dustin_attn_workspace(..., sparse = 1) bytes, 256-byte aligned (0 bytes,
+ *        i.e. NULL, when the batch has enough (b, KV head) pairs to fill the GPU without
+ *        splitting the token list); calls sharing a workspace must not overlap
  * Rounding: bf16 inputs, fp32 MFMA accumulation, fp32 online softmax, probabilities
  * rounded to bf16 before the value product, bf16 output.
  * --------------------------------------------------------------------------------- */

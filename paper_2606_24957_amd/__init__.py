@@ -127,6 +127,19 @@ def _i32_dev(x, device) -> Optional[torch.Tensor]:
     return torch.tensor(list(x), dtype=torch.int32, device=device)
 
 
+class Call:
+    """One prepared libdustin call: every argument marshalled once, replayed by calling
+    the object (one C call per launch, on the stream captured when it was planned)."""
+
+    def __init__(self, fn, args, what, keep, result):
+        self._fn, self._args, self._what, self._keep = fn, args, what, keep
+        self.result = result
+
+    def __call__(self):
+        _check(self._fn(*self._args), self._what)
+        return self.result
+
+
 _WS = {}
 
 
@@ -189,41 +202,47 @@ def _batch(B, max_len, nq_max, k_max, seq_lens, n_query=None, budget=None, m=Non
 
 # ----------------------------------------------------------------------------- score
 
-def score(q: torch.Tensor, k: torch.Tensor, seq_lens, heads: Sequence[int], *, n_query=None,
-          scale: Optional[float] = None, groups: int = 1, init: Optional[torch.Tensor] = None,
-          out: Optional[torch.Tensor] = None, max_len: Optional[int] = None, stream=None):
-    """Eq. 5 over the scoring heads.  q bf16 [B, nq_max, Hq, d]; k bf16 [B, N_cap, Hkv, d];
-    init / out fp32 [B, groups, >= max_len].  Returns out (positions >= N_b untouched)."""
-    _on_gpu(q, k, init, out)
+def plan_score(q: torch.Tensor, k: torch.Tensor, seq_lens, heads: Sequence[int], *,
+               n_query=None, scale: Optional[float] = None, groups: int = 1,
+               init: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None,
+               max_len: Optional[int] = None, page_table: Optional[torch.Tensor] = None,
+               stream=None) -> Call:
+    """Prepared dustin_score (Eq. 5 over the scoring heads).  q bf16 [B, nq_max, Hq, d];
+    k bf16 [B, N_cap, Hkv, d] (or paged with page_table); init / out fp32
+    [B, groups, >= max_len]."""
+    _on_gpu(q, k, init, out, page_table)
     B, nq_max, Hq, d = q.shape
     dev = q.device
     seq = _i32_dev(seq_lens, dev)
     nqa = _i32_dev(n_query, dev)
-    max_len = k.shape[1] if max_len is None else int(max_len)
+    kv = kv_view(k, page_table)
+    max_len = _capacity(kv) if max_len is None else int(max_len)
     if out is None:
         out = torch.empty((B, groups, max_len), dtype=torch.float32, device=dev)
     heads_host = (ctypes.c_int32 * len(heads))(*[int(h) for h in heads])
-    kv = kv_view(k)
     bt = _batch(B, max_len, nq_max, 0, seq, nqa)
     nbytes = lib().dustin_score_workspace(B, max_len, nq_max, len(heads))
     ws = workspace(nbytes, dev, "score")
     scale = 1.0 / math.sqrt(d) if scale is None else scale
     ins = (init.stride(0), init.stride(1)) if init is not None else (0, 0)
-    st = lib().dustin_score(_ptr(q), q.stride(0), q.stride(1), q.stride(2), Hq, heads_host,
-                            len(heads), ctypes.byref(kv), ctypes.byref(bt), float(scale),
-                            int(groups), _ptr(init), ins[0], ins[1], _ptr(out), out.stride(0),
-                            out.stride(1), _ptr(ws), nbytes, _stream(stream))
-    _check(st, "dustin_score")
-    return out
+    args = (_ptr(q), q.stride(0), q.stride(1), q.stride(2), Hq, heads_host, len(heads),
+            ctypes.byref(kv), ctypes.byref(bt), float(scale), int(groups), _ptr(init), ins[0],
+            ins[1], _ptr(out), out.stride(0), out.stride(1), _ptr(ws), nbytes, _stream(stream))
+    return Call(lib().dustin_score, args, "dustin_score", (q, k, init, kv, bt, ws, heads_host), out)
+
+
+def score(q, k, seq_lens, heads, **kw):
+    """Eq. 5 over the scoring heads; returns out (positions >= N_b untouched)."""
+    return plan_score(q, k, seq_lens, heads, **kw)()
 
 
 # ----------------------------------------------------------------------------- top-k
 
-def topk(s_draft: Optional[torch.Tensor], s_target: Optional[torch.Tensor], seq_lens,
+def plan_topk(s_draft: Optional[torch.Tensor], s_target: Optional[torch.Tensor], seq_lens,
          k_max: int, *, budget=None, m=None, m_scalar: Optional[int] = None, n_sink: int = 4,
          n_window: int = 16, groups: int = 1, idx: Optional[torch.Tensor] = None,
-         count: Optional[torch.Tensor] = None, stream=None):
-    """Eq. 6.  s_draft / s_target fp32 [B, G' (1 = broadcast), N]; returns (idx int32
+         count: Optional[torch.Tensor] = None, stream=None) -> Call:
+    """Prepared dustin_topk, Eq. 6.  s_draft / s_target fp32 [B, G' (1 = broadcast), N]; returns (idx int32
     [B, groups, k_max] ascending, only [:count] written; count int32 [B, groups])."""
     _on_gpu(s_draft, s_target, idx, count)
     ref = s_target if s_target is not None else s_draft
@@ -248,11 +267,17 @@ def topk(s_draft: Optional[torch.Tensor], s_target: Optional[torch.Tensor], seq_
     dsb, dsg = st(s_draft)
     tsb, tsg = st(s_target)
     bt = _batch(B, max_len, 0, k_max, seq, None, bud, ma, m_scalar)
-    rc = lib().dustin_topk(_ptr(s_draft), dsb, dsg, _ptr(s_target), tsb, tsg, ctypes.byref(bt),
-                           int(groups), int(n_sink), int(n_window), _ptr(idx), idx.stride(0),
-                           idx.stride(1), _ptr(count), None, 0, _stream(stream))
-    _check(rc, "dustin_topk")
-    return idx, count
+    args = (_ptr(s_draft), dsb, dsg, _ptr(s_target), tsb, tsg, ctypes.byref(bt), int(groups),
+            int(n_sink), int(n_window), _ptr(idx), idx.stride(0), idx.stride(1), _ptr(count),
+            None, 0, _stream(stream))
+    return Call(lib().dustin_topk, args, "dustin_topk", (s_draft, s_target, bt), (idx, count))
+
+
+def topk(s_draft, s_target, seq_lens, k_max, **kw):
+    """Eq. 6; returns (idx int32 [B, groups, k_max], count int32 [B, groups])."""
+    return plan_topk(s_draft, s_target, seq_lens, k_max, **kw)()
+
+
 
 
 # ----------------------------------------------------------------------------- attention
@@ -269,12 +294,12 @@ def _attn_common(q, k, v, seq_lens, n_query, page_table, max_len, out):
     return B, nq_max, Hq, d, dev, kv, vv, int(max_len), out
 
 
-def sparse_verify_attn(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, idx: torch.Tensor,
-                       count: torch.Tensor, seq_lens, *, n_query=None,
-                       page_table: Optional[torch.Tensor] = None, scale: Optional[float] = None,
-                       out: Optional[torch.Tensor] = None, max_len: Optional[int] = None,
-                       stream=None):
-    """Verification attention over idx[b, g, :count] plus the causal verification window.
+def plan_sparse_verify_attn(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor,
+                            idx: torch.Tensor, count: torch.Tensor, seq_lens, *, n_query=None,
+                            page_table: Optional[torch.Tensor] = None,
+                            scale: Optional[float] = None, out: Optional[torch.Tensor] = None,
+                            max_len: Optional[int] = None, stream=None) -> Call:
+    """Prepared verification attention over idx[b, g, :count] plus the causal verification window.
     q/out bf16 [B, T_max, Hq, 128]; idx int32 [B, G, k_max]; count int32 [B, G]."""
     B, nq_max, Hq, d, dev, kv, vv, max_len, out = _attn_common(q, k, v, seq_lens, n_query,
                                                                 page_table, max_len, out)
@@ -286,21 +311,26 @@ def sparse_verify_attn(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, idx: t
     nbytes = lib().dustin_attn_workspace(B, Hq, kv.num_kv_heads, nq_max, k_max, 1)
     ws = workspace(nbytes, dev, "attn")
     scale = 1.0 / math.sqrt(d) if scale is None else scale
-    rc = lib().dustin_sparse_verify_attn(_ptr(q), q.stride(0), q.stride(1), q.stride(2), Hq,
-                                         ctypes.byref(kv), ctypes.byref(vv), ctypes.byref(bt),
-                                         _ptr(idx), idx.stride(0), idx.stride(1),
-                                         _ptr(count.contiguous()), G, float(scale), _ptr(out),
-                                         out.stride(0), out.stride(1), out.stride(2), _ptr(ws),
-                                         nbytes, _stream(stream))
-    _check(rc, "dustin_sparse_verify_attn")
-    return out
+    count = count.contiguous()
+    args = (_ptr(q), q.stride(0), q.stride(1), q.stride(2), Hq, ctypes.byref(kv),
+            ctypes.byref(vv), ctypes.byref(bt), _ptr(idx), idx.stride(0), idx.stride(1),
+            _ptr(count), G, float(scale), _ptr(out), out.stride(0), out.stride(1), out.stride(2),
+            _ptr(ws), nbytes, _stream(stream))
+    return Call(lib().dustin_sparse_verify_attn, args, "dustin_sparse_verify_attn",
+                (q, k, v, idx, count, kv, vv, bt, ws), out)
 
 
-def dense_verify_attn(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, seq_lens, *,
-                      n_query=None, page_table: Optional[torch.Tensor] = None,
-                      scale: Optional[float] = None, out: Optional[torch.Tensor] = None,
-                      max_len: Optional[int] = None, stream=None):
-    """Full-cache verification attention over [0, N_b) plus the causal window."""
+def sparse_verify_attn(q, k, v, idx, count, seq_lens, **kw):
+    """Verification attention over idx[b, g, :count] plus the causal verification window;
+    returns out bf16 [B, T_max, Hq, 128] (rows t >= T_b untouched)."""
+    return plan_sparse_verify_attn(q, k, v, idx, count, seq_lens, **kw)()
+
+
+def plan_dense_verify_attn(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, seq_lens, *,
+                           n_query=None, page_table: Optional[torch.Tensor] = None,
+                           scale: Optional[float] = None, out: Optional[torch.Tensor] = None,
+                           max_len: Optional[int] = None, stream=None) -> Call:
+    """Prepared full-cache verification attention over [0, N_b) plus the causal window."""
     B, nq_max, Hq, d, dev, kv, vv, max_len, out = _attn_common(q, k, v, seq_lens, n_query,
                                                                 page_table, max_len, out)
     seq = _i32_dev(seq_lens, dev)
@@ -309,9 +339,12 @@ def dense_verify_attn(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, seq_len
     nbytes = lib().dustin_attn_workspace(B, Hq, kv.num_kv_heads, nq_max, max_len, 0)
     ws = workspace(nbytes, dev, "attn")
     scale = 1.0 / math.sqrt(d) if scale is None else scale
-    rc = lib().dense_verify_attn(_ptr(q), q.stride(0), q.stride(1), q.stride(2), Hq,
-                                 ctypes.byref(kv), ctypes.byref(vv), ctypes.byref(bt),
-                                 float(scale), _ptr(out), out.stride(0), out.stride(1),
-                                 out.stride(2), _ptr(ws), nbytes, _stream(stream))
-    _check(rc, "dense_verify_attn")
-    return out
+    args = (_ptr(q), q.stride(0), q.stride(1), q.stride(2), Hq, ctypes.byref(kv),
+            ctypes.byref(vv), ctypes.byref(bt), float(scale), _ptr(out), out.stride(0),
+            out.stride(1), out.stride(2), _ptr(ws), nbytes, _stream(stream))
+    return Call(lib().dense_verify_attn, args, "dense_verify_attn", (q, k, v, kv, vv, bt, ws), out)
+
+
+def dense_verify_attn(q, k, v, seq_lens, **kw):
+    """Full-cache verification attention over [0, N_b) plus the causal window."""
+    return plan_dense_verify_attn(q, k, v, seq_lens, **kw)()

@@ -2,6 +2,7 @@
 // layout, launch configuration.  Validation happens before any HIP call, so a rejected
 // call touches neither the device nor any output.
 #include <math.h>
+#include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
 
@@ -12,9 +13,8 @@ using namespace dustin;
 namespace {
 
 constexpr size_t kAlign = 256;
-constexpr size_t kCounterBytes = 4096;  // split counters at the head of the attention workspace
 constexpr int kAttnWaves = 4;
-constexpr int kMaxSplits = 128;
+constexpr int kMaxSplits = 64;
 constexpr int kTopkMaxLen = 1 << 20;
 
 size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
@@ -31,6 +31,16 @@ int env_int(const char* name, int fallback) {
   if (!v || !*v) return fallback;
   const int x = atoi(v);
   return x > 0 ? x : fallback;
+}
+
+// Workgroups per (split, b, g): 1 (all 128 output columns, scores computed once) or 2 (64
+// columns each, scores computed by both).  Two slices fill the GPU without splitting the
+// token list (no partials, no second kernel), which wins for the short gathered lists of
+// the sparse path and for large row tiles; long dense lists use one slice and token splits.
+int attn_slices(int64_t tokens_per_pair, int row_tiles) {
+  const int forced = env_int("DUSTIN_ATTN_SLICES", 0);
+  if (forced == 1 || forced == 2) return forced;
+  return (tokens_per_pair < 8192 || row_tiles >= 4) ? 2 : 1;
 }
 
 bool batch_ok(const dustin_batch* bt) {
@@ -79,10 +89,12 @@ dustin_status kv_of(const dustin_kv* kv, int head_dim, int64_t need, KvView* out
     out->num_pages = kv->num_pages;
     out->stride_page = kv->stride_page;
     out->capacity = (int64_t)kv->max_pages * ps;
+    if (((int64_t)kv->num_pages << shift) > INT32_MAX) return DUSTIN_ERR_UNSUPPORTED;
   } else {
     out->capacity = kv->capacity;
   }
   if (out->capacity < need || out->capacity <= 0) return DUSTIN_ERR_INVALID_ARG;
+  if (!kv->page_table && out->capacity > INT32_MAX) return DUSTIN_ERR_UNSUPPORTED;
   return DUSTIN_OK;
 }
 
@@ -93,7 +105,7 @@ int attn_row_tiles(int nq_max, int group_size) {
   return rt < 1 ? 1 : rt;
 }
 
-int attn_splits(int batch, int num_kv_heads, int64_t tokens_per_pair) {
+int attn_splits(int batch, int num_kv_heads, int64_t tokens_per_pair, int slices) {
   const int64_t pairs = (int64_t)batch * num_kv_heads;
   if (pairs <= 0) return 1;
   const int64_t steps = (tokens_per_pair + 31) / 32;
@@ -102,14 +114,14 @@ int attn_splits(int batch, int num_kv_heads, int64_t tokens_per_pair) {
   if (forced > 0) {
     s = forced;
   } else {
-    const int64_t target_wgs = 512;  // two workgroups per compute unit
-    int64_t want = (target_wgs + pairs - 1) / pairs;
-    const int64_t per_wave_floor = steps / (kAttnWaves * 2);  // each wave >= 2 steps
+    // enough workgroups for every compute unit (256 CUs)
+    const int64_t target_units = 256 / slices;
+    int64_t want = (target_units + pairs - 1) / pairs;
+    const int64_t per_wave_floor = steps / (kAttnWaves * 4);  // each wave >= 4 steps
     if (want > per_wave_floor) want = per_wave_floor;
     s = (int)(want < 1 ? 1 : want);
   }
   if (s > kMaxSplits) s = kMaxSplits;
-  if (pairs > (int64_t)(kCounterBytes / 4)) s = 1;
   const int64_t max_useful = steps < 1 ? 1 : steps;
   if (s > max_useful) s = (int)max_useful;
   return s < 1 ? 1 : s;
@@ -117,13 +129,14 @@ int attn_splits(int batch, int num_kv_heads, int64_t tokens_per_pair) {
 
 size_t attn_ws_bytes(int batch, int num_q_heads, int num_kv_heads, int nq_max, int64_t tokens) {
   if (batch <= 0 || num_kv_heads <= 0 || num_q_heads % num_kv_heads) return 0;
-  const int splits = attn_splits(batch, num_kv_heads, tokens + nq_max);
+  const int rt = attn_row_tiles(nq_max, num_q_heads / num_kv_heads);
+  const int splits = attn_splits(batch, num_kv_heads, tokens + nq_max, attn_slices(tokens + nq_max, rt));
   if (splits <= 1) return 0;
-  const int rows_pad = attn_row_tiles(nq_max, num_q_heads / num_kv_heads) * 16;
+  const int rows_pad = rt * 16;
   const size_t pairs = (size_t)batch * num_kv_heads;
   const size_t acc = pairs * splits * rows_pad * 128 * sizeof(float);
   const size_t ml = pairs * splits * rows_pad * 2 * sizeof(float);
-  return kCounterBytes + round_up(acc, kAlign) + round_up(ml, kAlign);
+  return round_up(acc, kAlign) + round_up(ml, kAlign);
 }
 
 dustin_status run_attention(bool sparse, const void* q, int64_t q_sb, int64_t q_st, int64_t q_sh,
@@ -133,12 +146,15 @@ dustin_status run_attention(bool sparse, const void* q, int64_t q_sb, int64_t q_
                             void* out, int64_t o_sb, int64_t o_st, int64_t o_sh, void* ws,
                             size_t ws_bytes, void* stream) {
   if (!batch_ok(bt) || !q || !out || !k || !v) return DUSTIN_ERR_INVALID_ARG;
-  if (!isfinite(scale)) return DUSTIN_ERR_INVALID_ARG;
+  if (!isfinite(scale) || !(scale > 0.f)) return DUSTIN_ERR_INVALID_ARG;
   const int Hkv = k->num_kv_heads;
   if (num_q_heads <= 0 || Hkv <= 0 || num_q_heads % Hkv || v->num_kv_heads != Hkv)
     return DUSTIN_ERR_INVALID_ARG;
   if (k->head_dim != 128 || v->head_dim != 128) return DUSTIN_ERR_UNSUPPORTED;
-  if ((k->page_table == nullptr) != (v->page_table == nullptr)) return DUSTIN_ERR_INVALID_ARG;
+  if (k->page_table != v->page_table) return DUSTIN_ERR_INVALID_ARG;  // one table for K and V
+  if (k->page_table && (k->page_size != v->page_size || k->max_pages != v->max_pages ||
+                        k->num_pages != v->num_pages))
+    return DUSTIN_ERR_INVALID_ARG;
   if (!rows_aligned(q, q_sb, q_st, q_sh) || !rows_aligned(out, o_sb, o_st, o_sh))
     return DUSTIN_ERR_INVALID_ARG;
   const int gs = num_q_heads / Hkv;
@@ -180,19 +196,20 @@ dustin_status run_attention(bool sparse, const void* q, int64_t q_sb, int64_t q_
   a.groups = sparse ? groups : 1;
   a.num_kv_heads = Hkv;
   a.group_size = gs;
+  a.pairs = B * Hkv;
   a.scale_log2 = scale * kLog2e;
   const int rt = attn_row_tiles(bt->nq_max, gs);
+  const int slices = attn_slices(tokens + bt->nq_max, rt);
   a.rows_pad = rt * 16;
-  a.splits = attn_splits(B, Hkv, tokens + bt->nq_max);
+  a.splits = attn_splits(B, Hkv, tokens + bt->nq_max, slices);
   if (a.splits > 1) {
     char* base = static_cast<char*>(ws);
     const size_t pairs = (size_t)B * Hkv;
-    a.counters = reinterpret_cast<uint32_t*>(base);
-    a.part_acc = reinterpret_cast<float*>(base + kCounterBytes);
+    a.part_acc = reinterpret_cast<float*>(base);
     const size_t acc = pairs * a.splits * a.rows_pad * 128 * sizeof(float);
-    a.part_ml = reinterpret_cast<float*>(base + kCounterBytes + round_up(acc, kAlign));
+    a.part_ml = reinterpret_cast<float*>(base + round_up(acc, kAlign));
   }
-  const hipError_t e = launch_verify_attn(a, rt, B, sparse, kv.page_table != nullptr,
+  const hipError_t e = launch_verify_attn(a, rt, slices, sparse, kv.page_table != nullptr,
                                           static_cast<hipStream_t>(stream));
   return e == hipSuccess ? DUSTIN_OK : DUSTIN_ERR_LAUNCH;
 }
@@ -236,7 +253,6 @@ dustin_status dustin_score(const void* q, int64_t q_sb, int64_t q_sj, int64_t q_
   const int Hkv = k->num_kv_heads;
   if (num_q_heads <= 0 || Hkv <= 0 || num_q_heads % Hkv) return DUSTIN_ERR_INVALID_ARG;
   if (k->head_dim != 64 && k->head_dim != 128) return DUSTIN_ERR_UNSUPPORTED;
-  if (k->page_table) return DUSTIN_ERR_UNSUPPORTED;
   if (groups != 1 && groups != Hkv) return DUSTIN_ERR_INVALID_ARG;
   if (bt->nq_max < 1 || bt->nq_max > 16) return DUSTIN_ERR_UNSUPPORTED;
   if (!rows_aligned(q, q_sb, q_sj, q_sh)) return DUSTIN_ERR_INVALID_ARG;

@@ -40,17 +40,37 @@ __device__ __forceinline__ uint32_t bf16_rne_bits(float x) {
 
 __device__ __forceinline__ float bf16_bits_to_float(uint32_t h) { return __uint_as_float(h << 16); }
 
+// Pairwise reductions across 16-lane rows using the gfx950 permlane swaps (VALU, no LDS
+// traffic).  For every lane the two results of a swap of x with itself hold {x of this
+// lane, x of lane ^ 16} (permlane16) or {x of this lane, x of lane ^ 32} (permlane32), so
+// a symmetric operation over both is the butterfly step.
+__device__ __forceinline__ float max_xor16(float x) {
+  const uint32_t u = __float_as_uint(x);
+  const auto r = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float max_xor32(float x) {
+  const uint32_t u = __float_as_uint(x);
+  const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float sum_xor16(float x) {
+  const uint32_t u = __float_as_uint(x);
+  const auto r = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float sum_xor32(float x) {
+  const uint32_t u = __float_as_uint(x);
+  const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 // Butterfly over lanes l ^ 16 and l ^ 32: combines the four 16-lane groups of a wave.
-__device__ __forceinline__ float max_over_lane_groups(float x) {
-  x = fmaxf(x, __shfl_xor(x, 16));
-  x = fmaxf(x, __shfl_xor(x, 32));
-  return x;
-}
-__device__ __forceinline__ float sum_over_lane_groups(float x) {
-  x += __shfl_xor(x, 16);
-  x += __shfl_xor(x, 32);
-  return x;
-}
+__device__ __forceinline__ float max_over_lane_groups(float x) { return max_xor32(max_xor16(x)); }
+__device__ __forceinline__ float sum_over_lane_groups(float x) { return sum_xor32(sum_xor16(x)); }
+
+// 2^x on the hardware exp unit (results below 2^-126 flush to zero).
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 __device__ __forceinline__ int clampi(int x, int lo, int hi) { return x < lo ? lo : (x > hi ? hi : x); }
 

@@ -11,22 +11,23 @@ struct AttnArgs {
   int64_t q_sb, q_st, q_sh;
   uint16_t* out;
   int64_t o_sb, o_st, o_sh;
-  KvView k, v;
+  KvView k, v;          // paged K and V share one page table and page size
   SeqDims dims;
-  const int32_t* idx;
+  const int32_t* idx;   // NULL: dense (every committed position)
   int64_t idx_sb, idx_sg;
   const int32_t* count;
   int32_t groups;
   int32_t num_kv_heads, group_size;
+  int32_t pairs;        // B * num_kv_heads
   float scale_log2;
-  int32_t splits;
+  int32_t splits;       // token splits per (b, g)
   int32_t rows_pad;
-  float* part_acc;     // [B, Hkv, splits, rows_pad, 128]
-  float* part_ml;      // [B, Hkv, splits, rows_pad, 2]
-  uint32_t* counters;  // [B, Hkv]
+  float* part_acc;      // [pairs, splits, rows_pad, 128]  (splits > 1 only)
+  float* part_ml;       // [pairs, splits, rows_pad, 2]
 };
 
-hipError_t launch_verify_attn(const AttnArgs& a, int rt, int B, bool sparse, bool paged,
+// slices: workgroups per (split, b, g), each producing 128 / slices output columns
+hipError_t launch_verify_attn(const AttnArgs& a, int rt, int slices, bool sparse, bool paged,
                               hipStream_t stream);
 
 // ---- scoring-head importance (score.hip) ----

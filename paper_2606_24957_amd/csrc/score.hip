@@ -13,7 +13,7 @@
 
 namespace dustin {
 
-template <int D>
+template <int D, bool kPaged>
 __global__ __launch_bounds__(kScoreWaves * kWave) void score_logits_kernel(ScoreArgs a) {
   constexpr int KS = D / 32;
   const int chunk = blockIdx.x, ug = blockIdx.y, b = blockIdx.z;
@@ -49,7 +49,7 @@ __global__ __launch_bounds__(kScoreWaves * kWave) void score_logits_kernel(Score
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int p = min(p0 + 16 * u + lr, max(N - 1, 0));
-      const uint16_t* kp = a.k.row<false>(b, p, g) + 8 * lg;
+      const uint16_t* kp = a.k.row<kPaged>(b, p, g) + 8 * lg;
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) kr[u][ks] = load16(kp + 32 * ks);
     }
@@ -160,10 +160,15 @@ __global__ __launch_bounds__(256) void score_finish_kernel(ScoreArgs a) {
 
 hipError_t launch_score(const ScoreArgs& a, int B, int n_used_kv, int head_dim, hipStream_t stream) {
   dim3 grid1(a.n_chunks, n_used_kv, B);
-  if (head_dim == 128)
-    hipLaunchKernelGGL(score_logits_kernel<128>, grid1, dim3(kScoreWaves * kWave), 0, stream, a);
-  else
-    hipLaunchKernelGGL(score_logits_kernel<64>, grid1, dim3(kScoreWaves * kWave), 0, stream, a);
+  const dim3 block(kScoreWaves * kWave);
+  const bool paged = a.k.page_table != nullptr;
+  if (head_dim == 128) {
+    if (paged) hipLaunchKernelGGL((score_logits_kernel<128, true>), grid1, block, 0, stream, a);
+    else hipLaunchKernelGGL((score_logits_kernel<128, false>), grid1, block, 0, stream, a);
+  } else {
+    if (paged) hipLaunchKernelGGL((score_logits_kernel<64, true>), grid1, block, 0, stream, a);
+    else hipLaunchKernelGGL((score_logits_kernel<64, false>), grid1, block, 0, stream, a);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   dim3 grid2((a.dims.max_len + kScoreFinishChunk - 1) / kScoreFinishChunk, a.groups, B);
