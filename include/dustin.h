@@ -143,7 +143,7 @@ dustin_status dustin_score(const void* q, int64_t q_sb, int64_t q_sj, int64_t q_
  *   s_draft / s_target  fp32 [B, G', >= max_len] (strides *_sb, *_sg; *_sg = 0
  *       broadcasts one vector to every group); either may be NULL: no S_D requires
  *       m = 0 (target-only, Dustin-T), no S_T requires m = k - |P| (draft-only, Dustin-D)
- *   bt       seq_lens, budget/k_max, m/m_scalar; 1 <= max_len <= 1 << 20
+ *   bt       seq_lens, budget/k_max, m/m_scalar; 1 <= max_len <= 1 << 19
  *   groups   1 or the KV head count
  *   idx      int32 [B, groups, >= k_max] (strides idx_sb, idx_sg), count int32 [B*groups]
  *   workspace  dustin_topk_workspace() bytes (may be 0 bytes: pass NULL, 0)

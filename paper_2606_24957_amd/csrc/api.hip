@@ -15,7 +15,7 @@ namespace {
 constexpr size_t kAlign = 256;
 constexpr int kAttnWaves = 4;
 constexpr int kMaxSplits = 64;
-constexpr int kTopkMaxLen = 1 << 20;
+constexpr int kTopkMaxLen = 1 << 19;
 
 size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 

@@ -1,19 +1,33 @@
 // topk.hip -- tiered hybrid selection (Eq. 6), bit-exact and deterministic.
 //
-// One workgroup of 1024 threads per (sequence, selection group).  The chosen set lives
-// in an LDS bitmap of the row (thread t owns whole 32-position words, so no atomics are
-// needed to mark).  Each tier is a radix select on the order key of the fp32 scores
-// (digits of 11, 11 and 10 bits, MSB first, histograms in LDS) over the positions whose
-// bit is still clear; it yields the threshold key tau and how many positions equal to
-// tau still fit.  Marking takes every candidate above tau and the first of those equal
-// to tau in position order (a block-wide scan over the words).  A final scan of the word
-// popcounts writes the set in ascending order.
+// One workgroup of 1024 threads (16 waves) per (sequence, selection group).  The row's
+// order-preserving keys are staged in LDS, a segment at a time (one segment holds a whole
+// row of up to ~32K positions, so such a row is read from HBM once per tier); the chosen
+// set is an LDS bitmap.  Inside a segment wave w owns a contiguous run of positions and
+// walks it 64 at a time, so a ballot covers two whole bitmap words that only this wave
+// writes.
+//
+// Each tier selects `need` more positions among the clear bits by (key desc, position
+// asc), key = the order-preserving uint32 of the fp32 score:
+//   1. 12-bit histogram of the key's top digit over the free positions, then the digit
+//      whose cumulative count from the top reaches `need`;
+//   2. the same for bits 19..10 and then 9..0 among the free keys matching the prefix so
+//      far, which yields the threshold key tau and how many keys equal to tau still fit;
+//   3. in position order, every free key above tau and the first `remaining` equal to it
+//      are marked.
+// A final ordered pass over the bitmap writes the set in ascending position order.
 #include "kernels.hpp"
 
 namespace dustin {
 
 constexpr int kTopkThreads = 1024;
 constexpr int kTopkWaves = kTopkThreads / kWave;
+constexpr int kBins1 = 4096;                            // first digit: key bits 31..20
+constexpr int kBins = 1024;                             // later digits: 19..10, 9..0
+constexpr int kTopkLds = 160 * 1024;                    // LDS of one gfx950 workgroup
+constexpr int kLoadBatch = 16;                          // global loads in flight per thread
+constexpr int kScanBatch = 8;                           // LDS key reads in flight per lane
+constexpr int kSegQuantum = kTopkThreads * kLoadBatch;  // segments are multiples of this
 
 __device__ __forceinline__ uint32_t order_key(float x) {
   uint32_t u = __float_as_uint(x);
@@ -21,131 +35,231 @@ __device__ __forceinline__ uint32_t order_key(float x) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-// Exclusive scan of one value per thread over the block; returns the block total too.
-__device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t x, uint32_t* sm_wave, uint32_t& total) {
+__device__ __forceinline__ uint64_t lanemask_lt(int lane) { return (1ull << lane) - 1ull; }
+
+// hist[bin] += 1 for every active lane.  (Aggregating lanes of one bin with ballots
+// first measured slower on score rows than the LDS atomics it saves.)
+__device__ __forceinline__ void hist_add(uint32_t* hist, uint32_t bin, bool active) {
+  if (active) atomicAdd(&hist[bin], 1u);
+}
+
+struct TopkSmem {
+  uint32_t hist[kBins1];
+  uint32_t wave_cnt[kTopkWaves];
+  uint32_t misc[4];
+};
+
+// Exclusive prefix over the 16 per-wave counts (after a barrier) and their total.
+__device__ __forceinline__ uint32_t wave_offset(const TopkSmem& s, int wave, uint32_t* total) {
+  uint32_t off = 0, tot = 0;
+#pragma unroll
+  for (int w = 0; w < kTopkWaves; ++w) {
+    const uint32_t c = s.wave_cnt[w];
+    off += w < wave ? c : 0u;
+    tot += c;
+  }
+  *total = tot;
+  return off;
+}
+
+// Per-wave counts -> (this wave's exclusive offset, block total); two barriers.
+__device__ __forceinline__ uint32_t block_offsets(TopkSmem& s, uint32_t wave_count, uint32_t* total) {
   const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
-  uint32_t inc = x;
+  if (lane == 0) s.wave_cnt[wave] = wave_count;
+  __syncthreads();
+  const uint32_t off = wave_offset(s, wave, total);
+  __syncthreads();
+  return off;
+}
+
+// The digit where the count of keys from the top of hist[0..nbins) reaches `remaining`;
+// writes (digit, remaining within that digit) to s.misc[0..1].
+__device__ void find_digit(TopkSmem& s, int nbins, uint32_t remaining) {
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+  const int per = nbins / kTopkThreads;
+  const int lo = (kTopkThreads - 1 - tid) * per;  // thread 0 owns the highest bins
+  uint32_t mine = 0;
+  for (int i = 0; i < per; ++i) mine += s.hist[lo + i];
+  uint32_t inc = mine;  // inclusive scan in tid order = from the top bin down
 #pragma unroll
   for (int off = 1; off < kWave; off <<= 1) {
     const uint32_t y = __shfl_up(inc, off);
     if (lane >= off) inc += y;
   }
-  if (lane == kWave - 1) sm_wave[wave] = inc;
+  if (lane == kWave - 1) s.wave_cnt[wave] = inc;
   __syncthreads();
-  if (wave == 0) {
-    uint32_t w = lane < kTopkWaves ? sm_wave[lane] : 0u;
-#pragma unroll
-    for (int off = 1; off < kTopkWaves; off <<= 1) {
-      const uint32_t y = __shfl_up(w, off);
-      if (lane >= off) w += y;
+  uint32_t tot;
+  const uint32_t above = wave_offset(s, wave, &tot) + inc - mine;  // keys in higher bins
+  if (above < remaining && above + mine >= remaining) {
+    uint32_t run = above;
+    for (int i = per - 1; i >= 0; --i) {
+      const uint32_t c = s.hist[lo + i];
+      if (run + c >= remaining) {
+        s.misc[0] = (uint32_t)(lo + i);
+        s.misc[1] = remaining - run;
+        break;
+      }
+      run += c;
     }
-    if (lane < kTopkWaves) sm_wave[lane] = w;  // inclusive wave totals
   }
   __syncthreads();
-  const uint32_t before = wave ? sm_wave[wave - 1] : 0u;
-  total = sm_wave[kTopkWaves - 1];
-  __syncthreads();
-  return before + inc - x;
 }
 
-// Select `need` more positions among the clear bits of `bm` (words [0, nwords)) by
-// (key(s) descending, position ascending) and set their bits.
-__device__ void select_tier(const float* __restrict__ s, int N, uint32_t need, uint32_t* bm,
-                            int nwords, uint32_t* hist, uint32_t* sm_wave, uint32_t* sm_misc) {
+// One row's keys staged in LDS, `seg` positions at a time.
+struct KeyStage {
+  const float* row;
+  uint32_t* keys;      // [seg] in LDS
+  const uint32_t* bm;  // chosen bitmap, [ceil(N / 32)] words in LDS
+  int N, seg, nseg, loaded;
+
+  // positions [s seg, s seg + seg) -> keys: thread t takes j = t + 1024 r, sixteen loads
+  // in flight at a time (seg is a multiple of kSegQuantum; positions past the row read
+  // its last element and store 0)
+  __device__ void load(int s) {
+    if (loaded == s) return;
+    __syncthreads();  // the previous segment's readers are done
+    const int base = s * seg, R = seg / kTopkThreads;
+    for (int r0 = 0; r0 < R; r0 += kLoadBatch) {
+      float v[kLoadBatch];
+#pragma unroll
+      for (int u = 0; u < kLoadBatch; ++u) {
+        const int n = base + (int)threadIdx.x + (r0 + u) * kTopkThreads;
+        v[u] = row[n < N ? n : N - 1];
+      }
+#pragma unroll
+      for (int u = 0; u < kLoadBatch; ++u) {
+        const int j = (int)threadIdx.x + (r0 + u) * kTopkThreads;
+        keys[j] = base + j < N ? order_key(v[u]) : 0u;
+      }
+    }
+    __syncthreads();
+    loaded = s;
+  }
+
+  // Wave w's run inside the segment is [w per, (w + 1) per), per a multiple of 64.
+  __device__ int per_wave() const { return seg / kTopkWaves; }
+
+  // Is the segment-relative position j free (inside the row and not yet chosen)?
+  __device__ bool free_at(int s, int j) const {
+    const int n = s * seg + j;
+    return n < N && !((bm[n >> 5] >> (n & 31)) & 1u);
+  }
+
+  // Keys and free flags of kScanBatch consecutive 64-position steps of this wave's run,
+  // steps i0 .. i0 + kScanBatch - 1 (steps past the run read step 0 and come out taken).
+  __device__ __forceinline__ void fetch(int s, int w0, int i0, int steps, uint32_t* key,
+                                        bool* fr) const {
+    const int lane = threadIdx.x & (kWave - 1);
+    uint32_t word[kScanBatch];
+#pragma unroll
+    for (int u = 0; u < kScanBatch; ++u) {
+      const int i = i0 + u < steps ? i0 + u : 0;
+      const int j = w0 + i * kWave + lane;
+      const int n = min(s * seg + j, N - 1);
+      key[u] = keys[j];
+      word[u] = bm[n >> 5];
+    }
+#pragma unroll
+    for (int u = 0; u < kScanBatch; ++u) {
+      const int n = s * seg + w0 + (i0 + u) * kWave + lane;
+      fr[u] = i0 + u < steps && n < N && !((word[u] >> (n & 31)) & 1u);
+    }
+  }
+};
+
+// ORs the ballot of the 64 positions starting at n (a multiple of 64) into the bitmap.
+__device__ __forceinline__ void mark64(uint32_t* bm, int n, int N, uint64_t m) {
+  const int lane = threadIdx.x & (kWave - 1);
+  if (lane == 0 && n < N && (uint32_t)m) bm[n >> 5] |= (uint32_t)m;
+  if (lane == 32 && n + 32 < N && (uint32_t)(m >> 32)) bm[(n >> 5) + 1] |= (uint32_t)(m >> 32);
+}
+
+__device__ void select_tier(TopkSmem& s, KeyStage& ks, uint32_t need, uint32_t* bm) {
   if (need == 0) return;
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+  const int per = ks.per_wave(), w0 = wave * per, steps = per / kWave;
+
+  // ---- 1. the three digits: 31..20 over every free key, then 19..10 and 9..0 among
+  // the free keys that match the digits found so far
   uint32_t prefix = 0, pmask = 0, remaining = need;
-  const int shifts[3] = {21, 10, 0};
-  const int widths[3] = {11, 11, 10};
   for (int pass = 0; pass < 3; ++pass) {
-    const int sh = shifts[pass];
-    const uint32_t dmask = (1u << widths[pass]) - 1u;
-    const int nbins = 1 << widths[pass];
-    for (int i = tid; i < nbins; i += kTopkThreads) hist[i] = 0u;
+    const int sh = pass == 0 ? 20 : (pass == 1 ? 10 : 0);
+    const uint32_t dmask = pass == 0 ? 4095u : 1023u;
+    const int nbins = pass == 0 ? kBins1 : kBins;
+    for (int i = tid; i < nbins; i += kTopkThreads) s.hist[i] = 0u;
     __syncthreads();
-    for (int w = tid; w < nwords; w += kTopkThreads) {
-      const uint32_t free_bits = ~bm[w];
-      if (!free_bits) continue;
-      const int n0 = w * 32;
-      for (int i = 0; i < 32; ++i) {
-        const int n = n0 + i;
-        if (n >= N) break;
-        if (!((free_bits >> i) & 1u)) continue;
-        const uint32_t key = order_key(s[n]);
-        if ((key & pmask) == prefix) atomicAdd(&hist[(key >> sh) & dmask], 1u);
+    for (int sg = 0; sg < ks.nseg; ++sg) {
+      ks.load(sg);
+      for (int i0 = 0; i0 < steps; i0 += kScanBatch) {
+        uint32_t key[kScanBatch];
+        bool fr[kScanBatch];
+        ks.fetch(sg, w0, i0, steps, key, fr);
+#pragma unroll
+        for (int u = 0; u < kScanBatch; ++u)
+          hist_add(s.hist, (key[u] >> sh) & dmask, fr[u] && (key[u] & pmask) == prefix);
       }
     }
     __syncthreads();
-    // suffix sums over bins: thread t scans its bins from the top (bins per thread = nbins/1024)
-    const int per = nbins / kTopkThreads;  // 2 or 1
-    const int lo = (kTopkThreads - 1 - tid) * per;  // thread 0 takes the highest bins
-    uint32_t mine = 0;
-    for (int i = 0; i < per; ++i) mine += hist[lo + i];
-    uint32_t tot;
-    const uint32_t above = block_exclusive_scan(mine, sm_wave, tot);  // count in higher bins
-    // the digit where the cumulative count from the top reaches `remaining`
-    if (above < remaining && above + mine >= remaining) {
-      uint32_t run = above;
-      for (int i = per - 1; i >= 0; --i) {
-        const uint32_t c = hist[lo + i];
-        if (run + c >= remaining) {
-          sm_misc[0] = (uint32_t)(lo + i);
-          sm_misc[1] = remaining - run;
-          break;
-        }
-        run += c;
-      }
-    }
-    __syncthreads();
-    prefix |= sm_misc[0] << sh;
+    find_digit(s, nbins, remaining);
+    prefix |= s.misc[0] << sh;
     pmask |= dmask << sh;
-    remaining = sm_misc[1];
-    __syncthreads();
+    remaining = s.misc[1];
   }
   const uint32_t tau = prefix;
-  // mark: keys above tau, and the first `remaining` keys equal to tau in position order
-  uint32_t carry = 0;
-  for (int base = 0; base < nwords; base += kTopkThreads) {
-    const int w = base + tid;
-    uint32_t eq_bits = 0, gt_bits = 0;
-    if (w < nwords) {
-      const uint32_t free_bits = ~bm[w];
-      const int n0 = w * 32;
-      for (int i = 0; i < 32; ++i) {
-        const int n = n0 + i;
-        if (n >= N) break;
-        if (!((free_bits >> i) & 1u)) continue;
-        const uint32_t key = order_key(s[n]);
-        if (key > tau) gt_bits |= 1u << i;
-        else if (key == tau) eq_bits |= 1u << i;
-      }
+
+  // ---- 2. ordered marking: every free key above tau, then the first `remaining` free
+  // keys equal to tau in position order
+  uint32_t rank_base = 0;
+  for (int sg = 0; sg < ks.nseg; ++sg) {
+    ks.load(sg);
+    uint32_t c = 0;
+    for (int i0 = 0; i0 < steps; i0 += kScanBatch) {
+      uint32_t key[kScanBatch];
+      bool fr[kScanBatch];
+      ks.fetch(sg, w0, i0, steps, key, fr);
+#pragma unroll
+      for (int u = 0; u < kScanBatch; ++u) c += __popcll(__ballot(fr[u] && key[u] == tau));
     }
-    uint32_t tot;
-    const uint32_t rank0 = carry + block_exclusive_scan(__popc(eq_bits), sm_wave, tot);
-    if (w < nwords) {
-      uint32_t take = gt_bits;
-      uint32_t r = rank0;
-      uint32_t eb = eq_bits;
-      while (eb && r < remaining) {
-        const uint32_t bit = eb & (~eb + 1u);
-        take |= bit;
-        eb ^= bit;
-        ++r;
+    uint32_t seg_total;
+    uint32_t rank = rank_base + block_offsets(s, c, &seg_total);
+    for (int i0 = 0; i0 < steps; i0 += kScanBatch) {
+      uint32_t key[kScanBatch];
+      bool fr[kScanBatch];
+      ks.fetch(sg, w0, i0, steps, key, fr);
+      uint64_t take[kScanBatch];
+#pragma unroll
+      for (int u = 0; u < kScanBatch; ++u) {
+        const bool eq = fr[u] && key[u] == tau;
+        const uint64_t eqm = __ballot(eq);
+        const uint32_t r = rank + __popcll(eqm & lanemask_lt(lane));
+        rank += __popcll(eqm);
+        take[u] = __ballot((fr[u] && key[u] > tau) || (eq && r < remaining));
       }
-      bm[w] |= take;
+      // bitmap words change only after every read of this batch
+#pragma unroll
+      for (int u = 0; u < kScanBatch; ++u)
+        if (i0 + u < steps) mark64(bm, sg * ks.seg + w0 + (i0 + u) * kWave, ks.N, take[u]);
     }
-    carry += tot;
+    rank_base += seg_total;
   }
   __syncthreads();
 }
 
-__global__ __launch_bounds__(kTopkThreads) void topk_kernel(TopkArgs a) {
-  extern __shared__ uint32_t bm[];  // [nwords]
-  __shared__ uint32_t hist[2048];
-  __shared__ uint32_t sm_wave[kTopkWaves];
-  __shared__ uint32_t sm_misc[2];
+// Key-segment length for rows of up to max_len positions: the LDS left beside the
+// static state and the bitmap, a multiple of kSegQuantum, at most the row rounded up.
+static int topk_segment(int max_len) {
+  const int nwords = (max_len + 31) / 32;
+  const int avail = (kTopkLds - (int)sizeof(TopkSmem)) / 4 - nwords;
+  const int cap = avail / kSegQuantum * kSegQuantum;
+  const int row = (max_len + kSegQuantum - 1) / kSegQuantum * kSegQuantum;
+  return row < cap ? row : cap;
+}
+
+__global__ __launch_bounds__(kTopkThreads) void topk_kernel(TopkArgs a, int seg) {
+  extern __shared__ __align__(16) uint32_t dyn[];  // [seg] staged keys | [nwords] chosen bitmap
+  __shared__ TopkSmem s;
   const int go = blockIdx.x, b = blockIdx.y;
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
   const int N = a.dims.len(b);
   const int P = a.n_sink + a.n_window;
   const int k = clampi(a.dims.budget ? a.dims.budget[b] : a.dims.k_max, P, a.dims.k_max);
@@ -158,53 +272,83 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(TopkArgs a) {
     if (tid == 0) a.count[b * a.groups + go] = N;
     return;
   }
+  uint32_t* bm = dyn + seg;
+  // protected positions (and the padding past N) start out taken
   const int nwords = (N + 31) / 32;
   for (int w = tid; w < nwords; w += kTopkThreads) {
     uint32_t bits = 0;
     const int n0 = w * 32;
     for (int i = 0; i < 32; ++i) {
       const int n = n0 + i;
-      if (n < N && (n < a.n_sink || n >= N - a.n_window)) bits |= 1u << i;
+      if (n >= N || n < a.n_sink || n >= N - a.n_window) bits |= 1u << i;
     }
-    // positions >= N are marked taken so they are never candidates
-    if (n0 + 32 > N) bits |= ~0u << (N - n0);
     bm[w] = bits;
   }
+  // a row shorter than the segment uses a shorter one (still a multiple of kSegQuantum)
+  const int rseg = min(seg, (N + kSegQuantum - 1) / kSegQuantum * kSegQuantum);
+  KeyStage ks{nullptr, dyn, bm, N, rseg, (N + rseg - 1) / rseg, -1};
   __syncthreads();
-  if (a.s_draft)
-    select_tier(a.s_draft + (int64_t)b * a.d_sb + (int64_t)go * a.d_sg, N, (uint32_t)m, bm, nwords,
-                hist, sm_wave, sm_misc);
-  if (a.s_target)
-    select_tier(a.s_target + (int64_t)b * a.t_sb + (int64_t)go * a.t_sg, N, (uint32_t)(k - m - P), bm,
-                nwords, hist, sm_wave, sm_misc);
-  // ascending write-out of the set bits (positions >= N were set only as padding)
-  uint32_t carry = 0;
-  for (int base = 0; base < nwords; base += kTopkThreads) {
-    const int w = base + tid;
-    uint32_t bits = 0;
-    if (w < nwords) {
-      bits = bm[w];
-      const int n0 = w * 32;
-      if (n0 + 32 > N) bits &= (N - n0 >= 32) ? ~0u : ((1u << (N - n0)) - 1u);
+  if (a.s_draft) {
+    ks.row = a.s_draft + (int64_t)b * a.d_sb + (int64_t)go * a.d_sg;
+    ks.loaded = -1;
+    select_tier(s, ks, (uint32_t)m, bm);
+  }
+  if (a.s_target) {
+    ks.row = a.s_target + (int64_t)b * a.t_sb + (int64_t)go * a.t_sg;
+    ks.loaded = -1;
+    select_tier(s, ks, (uint32_t)(k - m - P), bm);
+  }
+
+  // ascending write-out: wave w owns bitmap words [w W, (w + 1) W), one word per lane
+  const int wper = (nwords + kTopkWaves - 1) / kTopkWaves;
+  const int w0 = min(nwords, wave * wper), w1 = min(nwords, w0 + wper);
+  auto word_bits = [&](int w) -> uint32_t {
+    uint32_t bits = w < w1 ? bm[w] : 0u;
+    if (w == nwords - 1 && (N & 31)) bits &= (1u << (N & 31)) - 1u;
+    return bits;
+  };
+  uint32_t c = 0;
+  for (int base = w0; base < w1; base += kWave) {
+    uint32_t pc = __popc(word_bits(base + lane));
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) pc += __shfl_xor(pc, off);
+    c += pc;  // every lane holds this iteration's wave total
+  }
+  uint32_t total;
+  uint32_t o = block_offsets(s, c, &total);
+  for (int base = w0; base < w1; base += kWave) {
+    const int w = base + lane;
+    uint32_t bits = word_bits(w);
+    const uint32_t pc = __popc(bits);
+    uint32_t inc = pc;
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+      const uint32_t y = __shfl_up(inc, off);
+      if (lane >= off) inc += y;
     }
-    uint32_t tot;
-    uint32_t o = carry + block_exclusive_scan(__popc(bits), sm_wave, tot);
+    uint32_t pos = o + inc - pc;
+    o += __shfl(inc, kWave - 1);
     while (bits) {
       const int i = __ffs(bits) - 1;
       bits &= bits - 1u;
-      if (o < (uint32_t)k) out[o] = w * 32 + i;  // never past the budget
-      ++o;
+      if (pos < (uint32_t)k) out[pos] = w * 32 + i;  // never past the budget
+      ++pos;
     }
-    carry += tot;
   }
-  if (tid == 0) a.count[b * a.groups + go] = (int32_t)min(carry, (uint32_t)k);
+  if (tid == 0) a.count[b * a.groups + go] = (int32_t)min(total, (uint32_t)k);
 }
 
 hipError_t launch_topk(const TopkArgs& a, int B, hipStream_t stream) {
+  const int seg = topk_segment(a.dims.max_len);
+  if (seg < kSegQuantum) return hipErrorInvalidValue;
   const int nwords = (a.dims.max_len + 31) / 32;
+  const size_t dyn = (size_t)(seg + nwords) * sizeof(uint32_t);
+  const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(topk_kernel),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize,
+                                           kTopkLds - (int)sizeof(TopkSmem));
+  if (e != hipSuccess) return e;
   dim3 grid(a.groups, B);
-  hipLaunchKernelGGL(topk_kernel, grid, dim3(kTopkThreads), (size_t)nwords * sizeof(uint32_t),
-                     stream, a);
+  hipLaunchKernelGGL(topk_kernel, grid, dim3(kTopkThreads), dyn, stream, a, seg);
   return hipGetLastError();
 }
 

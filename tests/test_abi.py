@@ -83,7 +83,7 @@ def test_topk_rejects(L):
     assert _topk(L, _batch(), sd=None, st=None) == D.ERR_INVALID_ARG
     assert _topk(L, _batch(), idx=None) == D.ERR_INVALID_ARG
     assert _topk(L, _batch(), groups=0) == D.ERR_INVALID_ARG
-    assert _topk(L, _batch(max_len=(1 << 20) + 1)) == D.ERR_UNSUPPORTED
+    assert _topk(L, _batch(max_len=(1 << 19) + 1)) == D.ERR_UNSUPPORTED
     bt = _batch()
     bt.seq_lens = None
     assert _topk(L, bt) == D.ERR_INVALID_ARG
