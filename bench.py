@@ -14,7 +14,6 @@ message goes to stderr.
     python bench.py [--gpus 1] [--steps 30] [--warmup 5] [--workload qwen72b] [--k 2048]
 """
 import argparse
-import hashlib
 import json
 import os
 import re
@@ -99,14 +98,6 @@ def topk_bytes(s):
 
 # ----------------------------------------------------------------------------- traffic
 
-def kernel_sources_sha():
-    h = hashlib.sha256()
-    for f in ("attn.hip", "common.hpp", "kernels.hpp"):
-        with open(os.path.join(ROOT, "paper_2606_24957_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
-    return h.hexdigest()[:16]
-
-
 def measured_traffic(workload, k):
     """HBM bytes per sparse launch from the committed rocprofv3 counter summary, or None
     when it is missing or was taken on different kernel sources."""
@@ -116,6 +107,7 @@ def measured_traffic(workload, k):
     m = re.search(r"<!--\s*traffic:\s*(\{.*?\})\s*-->", open(path).read(), re.S)
     if not m:
         return None
+    from paper_2606_24957_amd.rocprof_summary import kernel_sources_sha
     rec = json.loads(m.group(1))
     if rec.get("source_sha256") != kernel_sources_sha():
         return None
