@@ -33,7 +33,7 @@ hipError_t launch_verify_attn(const AttnArgs& a, int rt, int slices, bool sparse
 // ---- scoring-head importance (score.hip) ----
 constexpr int kScoreWaves = 4;
 constexpr int kScoreChunk = 1024;        // positions per pass-1 workgroup
-constexpr int kScoreFinishChunk = 2048;  // positions per pass-2 workgroup
+constexpr int kScoreFinishChunk = 1024;  // positions per pass-2 workgroup (4 per thread)
 constexpr int kScoreMaxHeads = 16;
 
 struct ScoreArgs {

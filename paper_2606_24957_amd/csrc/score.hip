@@ -16,7 +16,9 @@ namespace dustin {
 template <int D, bool kPaged>
 __global__ __launch_bounds__(kScoreWaves * kWave) void score_logits_kernel(ScoreArgs a) {
   constexpr int KS = D / 32;
-  const int chunk = blockIdx.x, ug = blockIdx.y, b = blockIdx.z;
+  // KV heads vary fastest: workgroups that run together read the same positions of every
+  // used KV head (neighbouring 256-byte pieces of the same cache rows)
+  const int ug = blockIdx.x, chunk = blockIdx.y, b = blockIdx.z;
   const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
   const int lr = lane & 15, lg = lane >> 4;
   const int g = a.used_kv[ug];
@@ -70,8 +72,8 @@ __global__ __launch_bounds__(kScoreWaves * kWave) void score_logits_kernel(Score
       const float m_use = m_new == -INFINITY ? 0.f : m_new;
       float add = 0.f;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) add += exp2f(x[e] - m_use);
-      s_run = s_run * exp2f(m_run - m_use) + add;
+      for (int e = 0; e < 4; ++e) add += fast_exp2(x[e] - m_use);
+      s_run = s_run * fast_exp2(m_run - m_use) + add;
       m_run = m_new;
       if (pair_ok) {
         if (pb + 3 < p_end) {
@@ -91,7 +93,7 @@ __global__ __launch_bounds__(kScoreWaves * kWave) void score_logits_kernel(Score
     const float mo = __shfl_xor(m_run, off), so = __shfl_xor(s_run, off);
     const float mn = fmaxf(m_run, mo);
     const float mu = mn == -INFINITY ? 0.f : mn;
-    s_run = s_run * exp2f(m_run - mu) + so * exp2f(mo - mu);
+    s_run = s_run * fast_exp2(m_run - mu) + so * fast_exp2(mo - mu);
     m_run = mn;
   }
   __shared__ float sm[kScoreWaves][16][2];
@@ -105,61 +107,106 @@ __global__ __launch_bounds__(kScoreWaves * kWave) void score_logits_kernel(Score
     for (int w = 0; w < kScoreWaves; ++w) M = fmaxf(M, sm[w][lr][0]);
     const float mu = M == -INFINITY ? 0.f : M;
     float S = 0.f;
-    for (int w = 0; w < kScoreWaves; ++w) S += sm[w][lr][1] * exp2f(sm[w][lr][0] - mu);
+    for (int w = 0; w < kScoreWaves; ++w) S += sm[w][lr][1] * fast_exp2(sm[w][lr][0] - mu);
     float* st = a.stats + ((((int64_t)b * a.n_heads + pair_slot) * a.nq_max + pair_q) * a.n_chunks + chunk) * 2;
     st[0] = M;
     st[1] = S;
   }
 }
 
-__global__ __launch_bounds__(256) void score_finish_kernel(ScoreArgs a) {
+__device__ __forceinline__ float wave_max(float x) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) x = fmaxf(x, __shfl_xor(x, off));
+  return x;
+}
+
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) x += __shfl_xor(x, off);
+  return x;
+}
+
+__device__ __forceinline__ bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+constexpr int kFinishThreads = 256;
+constexpr int kFinishBatch = 8;  // logits rows loaded together per thread
+
+__global__ __launch_bounds__(kFinishThreads) void score_finish_kernel(ScoreArgs a) {
   const int chunk = blockIdx.x, go = blockIdx.y, b = blockIdx.z;
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
   const int N = a.dims.len(b);
   const int nq = a.dims.nq(b);
   const int p_begin = chunk * kScoreFinishChunk;
   if (p_begin >= N) return;
-  const int p_end = min(N, p_begin + kScoreFinishChunk);
 
-  // normalisers of the pairs that feed this output group: (slot, query, M, 1/Z)
-  __shared__ int sm_off[16 * 16];
-  __shared__ float sm_M[16 * 16], sm_iz[16 * 16];
+  // the (head slot, query) pairs feeding output group go, in that order, with their
+  // logits row, softmax max M (log2 domain) and 1 / Z
+  __shared__ int sm_row[kScoreMaxHeads * 16];
+  __shared__ float sm_M[kScoreMaxHeads * 16], sm_iz[kScoreMaxHeads * 16];
+  __shared__ int sm_np;
+  if (tid == 0) {
+    int np = 0;
+    for (int slot = 0; slot < a.n_heads; ++slot) {
+      if (a.groups != 1 && a.heads[slot] / a.group_size != go) continue;
+      for (int j = 0; j < nq; ++j) sm_row[np++] = (b * a.n_heads + slot) * a.nq_max + j;
+    }
+    sm_np = np;
+  }
   __syncthreads();
-  const int total_pairs = a.n_heads * nq;
-  for (int pidx = threadIdx.x; pidx < total_pairs; pidx += blockDim.x) {
-    const int slot = pidx / nq, j = pidx - slot * nq;
-    const int kvh = a.heads[slot] / a.group_size;
-    if (a.groups != 1 && kvh != go) continue;
-    const float* st = a.stats + (((int64_t)b * a.n_heads + slot) * a.nq_max + j) * a.n_chunks * 2;
-    const int nch = (N + kScoreChunk - 1) / kScoreChunk;
+  const int np = sm_np;
+  // each wave merges the per-chunk statistics of every fourth pair, one chunk per lane
+  const int nch = (N + kScoreChunk - 1) / kScoreChunk;
+  for (int i = wave; i < np; i += kFinishThreads / kWave) {
+    const float* st = a.stats + (int64_t)sm_row[i] * a.n_chunks * 2;
     float M = -INFINITY;
-    for (int c = 0; c < nch; ++c) M = fmaxf(M, st[2 * c]);
+    for (int c = lane; c < nch; c += kWave) M = fmaxf(M, st[2 * c]);
+    M = wave_max(M);
     const float mu = M == -INFINITY ? 0.f : M;
     float Z = 0.f;
-    for (int c = 0; c < nch; ++c) Z += st[2 * c + 1] * exp2f(st[2 * c] - mu);
-    // stable slot: pairs are summed in (head slot, query) order
-    sm_off[pidx] = ((int)(((int64_t)b * a.n_heads + slot) * a.nq_max + j));
-    sm_M[pidx] = mu;
-    sm_iz[pidx] = Z > 0.f ? 1.f / Z : 0.f;
+    for (int c = lane; c < nch; c += kWave) Z += st[2 * c + 1] * fast_exp2(st[2 * c] - mu);
+    Z = wave_sum(Z);
+    if (lane == 0) {
+      sm_M[i] = mu;
+      sm_iz[i] = Z > 0.f ? 1.f / Z : 0.f;
+    }
   }
   __syncthreads();
 
+  // four consecutive positions per thread (the logits rows are 64-element aligned, so
+  // the vector load stays inside a row even past N)
+  const int n0 = p_begin + 4 * tid;
+  if (n0 >= N) return;
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  for (int i0 = 0; i0 < np; i0 += kFinishBatch) {
+    f32x4 x[kFinishBatch];
+#pragma unroll
+    for (int u = 0; u < kFinishBatch; ++u) {
+      const int i = i0 + u < np ? i0 + u : i0;
+      x[u] = *reinterpret_cast<const f32x4*>(a.logits + (int64_t)sm_row[i] * a.ld + n0);
+    }
+#pragma unroll
+    for (int u = 0; u < kFinishBatch; ++u) {
+      if (i0 + u < np) {
+        const float M = sm_M[i0 + u], iz = sm_iz[i0 + u];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc[e] += fast_exp2(x[u][e] - M) * iz;
+      }
+    }
+  }
   const float* init_row = a.init ? a.init + (int64_t)b * a.init_sb + (int64_t)go * a.init_sg : nullptr;
   float* out_row = a.out + (int64_t)b * a.out_sb + (int64_t)go * a.out_sg;
-  for (int n = p_begin + threadIdx.x; n < p_end; n += blockDim.x) {
-    float acc = 0.f;
-    for (int pidx = 0; pidx < total_pairs; ++pidx) {
-      const int slot = pidx / nq;
-      const int kvh = a.heads[slot] / a.group_size;
-      if (a.groups != 1 && kvh != go) continue;
-      const float x = a.logits[(int64_t)sm_off[pidx] * a.ld + n];
-      acc += exp2f(x - sm_M[pidx]) * sm_iz[pidx];
-    }
-    out_row[n] = (init_row ? init_row[n] : 0.f) + acc;
+  if (n0 + 3 < N && aligned16(out_row + n0) && (!init_row || aligned16(init_row + n0))) {
+    const f32x4 in = init_row ? *reinterpret_cast<const f32x4*>(init_row + n0) : f32x4{0.f, 0.f, 0.f, 0.f};
+    *reinterpret_cast<f32x4*>(out_row + n0) = in + acc;
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if (n0 + e < N) out_row[n0 + e] = (init_row ? init_row[n0 + e] : 0.f) + acc[e];
   }
 }
 
 hipError_t launch_score(const ScoreArgs& a, int B, int n_used_kv, int head_dim, hipStream_t stream) {
-  dim3 grid1(a.n_chunks, n_used_kv, B);
+  dim3 grid1(n_used_kv, a.n_chunks, B);
   const dim3 block(kScoreWaves * kWave);
   const bool paged = a.k.page_table != nullptr;
   if (head_dim == 128) {
@@ -172,7 +219,7 @@ hipError_t launch_score(const ScoreArgs& a, int B, int n_used_kv, int head_dim, 
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   dim3 grid2((a.dims.max_len + kScoreFinishChunk - 1) / kScoreFinishChunk, a.groups, B);
-  hipLaunchKernelGGL(score_finish_kernel, grid2, dim3(256), 0, stream, a);
+  hipLaunchKernelGGL(score_finish_kernel, grid2, dim3(kFinishThreads), 0, stream, a);
   return hipGetLastError();
 }
 
