@@ -63,7 +63,11 @@ typedef enum {
  *   paged: position n of sequence b lives in physical page p = page_table[b * max_pages +
  *       n / page_size] at data[p * stride_page + (n % page_size) * stride_n + g * stride_h + c];
  *       capacity = max_pages * page_size, p < num_pages, num_pages * page_size < 2^31.
- *       K and V of one attention call must share the same page table and page size. */
+ *       K and V of one attention call must share the same page table and page size.
+ *   The attention entry points also need the rows of a cache to be reachable with a
+ *   32-bit byte offset (rows * stride_n * 2 < 2^32, rows = capacity or num_pages *
+ *   page_size) and, when paged, pages packed back to back (stride_page == page_size *
+ *   stride_n); otherwise they return DUSTIN_ERR_UNSUPPORTED. */
 typedef struct {
   const void* data;
   int32_t num_kv_heads;
@@ -172,7 +176,11 @@ dustin_status dustin_topk(const float* s_draft, int64_t d_sb, int64_t d_sg,
  *        are not written.  Round to nearest even.
  *   workspace  dustin_attn_workspace(..., sparse = 1) bytes, 256-byte aligned (0 bytes,
  *        i.e. NULL, when the batch has enough (b, KV head) pairs to fill the GPU without
- *        splitting the token list); calls sharing a workspace must not overlap
+ *        splitting the token list).  Its first 256 KB are a counter region (one int32 per
+ *        (b, KV head); B * num_kv_heads <= 65536), the partial results of token splits
+ *        follow.  Zero-fill the workspace once before its first use: every call leaves the
+ *        counter region at zero again, so one buffer can then serve calls of any shape.
+ *        Calls sharing a workspace must not overlap.
  * Rounding: bf16 inputs, fp32 MFMA accumulation, fp32 online softmax, probabilities
  * rounded to bf16 before the value product, bf16 output.
  * --------------------------------------------------------------------------------- */

@@ -13,8 +13,6 @@ using namespace dustin;
 namespace {
 
 constexpr size_t kAlign = 256;
-constexpr int kAttnWaves = 4;
-constexpr int kMaxSplits = 64;
 constexpr int kTopkMaxLen = 1 << 19;
 
 size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
@@ -31,16 +29,6 @@ int env_int(const char* name, int fallback) {
   if (!v || !*v) return fallback;
   const int x = atoi(v);
   return x > 0 ? x : fallback;
-}
-
-// Workgroups per (split, b, g): 1 (all 128 output columns, scores computed once) or 2 (64
-// columns each, scores computed by both).  Two slices fill the GPU without splitting the
-// token list (no partials, no second kernel), which wins for the short gathered lists of
-// the sparse path and for large row tiles; long dense lists use one slice and token splits.
-int attn_slices(int64_t tokens_per_pair, int row_tiles) {
-  const int forced = env_int("DUSTIN_ATTN_SLICES", 0);
-  if (forced == 1 || forced == 2) return forced;
-  return (tokens_per_pair < 8192 || row_tiles >= 4) ? 2 : 1;
 }
 
 bool batch_ok(const dustin_batch* bt) {
@@ -105,38 +93,49 @@ int attn_row_tiles(int nq_max, int group_size) {
   return rt < 1 ? 1 : rt;
 }
 
-int attn_splits(int batch, int num_kv_heads, int64_t tokens_per_pair, int slices) {
+// Token splits per (b, g): enough workgroups for one per CU (256 CUs, one workgroup of
+// four waves each), each split at least 8 steps of 32 tokens (two per wave).
+int attn_splits(int batch, int num_kv_heads, int64_t tokens_per_pair) {
   const int64_t pairs = (int64_t)batch * num_kv_heads;
   if (pairs <= 0) return 1;
   const int64_t steps = (tokens_per_pair + 31) / 32;
-  int s;
+  int64_t s;
   const int forced = env_int("DUSTIN_ATTN_SPLITS", 0);
   if (forced > 0) {
     s = forced;
   } else {
-    // enough workgroups for every compute unit (256 CUs)
-    const int64_t target_units = 256 / slices;
-    int64_t want = (target_units + pairs - 1) / pairs;
-    const int64_t per_wave_floor = steps / (kAttnWaves * 4);  // each wave >= 4 steps
-    if (want > per_wave_floor) want = per_wave_floor;
-    s = (int)(want < 1 ? 1 : want);
+    s = (256 + pairs - 1) / pairs;
+    if (s > steps / 8) s = steps / 8;
   }
-  if (s > kMaxSplits) s = kMaxSplits;
-  const int64_t max_useful = steps < 1 ? 1 : steps;
-  if (s > max_useful) s = (int)max_useful;
-  return s < 1 ? 1 : s;
+  if (s > kAttnMaxSplits) s = kAttnMaxSplits;
+  if (s > steps) s = steps;
+  return s < 1 ? 1 : (int)s;
+}
+
+// Split workspace: a fixed counter region first (one int32 per (b, g) for up to
+// kAttnMaxPairs pairs, zero between calls whatever shape used it last), then the partials.
+constexpr int64_t kAttnMaxPairs = 65536;
+
+struct AttnWs {
+  size_t counters, acc, ml, total;
+};
+
+AttnWs attn_ws_layout(int batch, int num_kv_heads, int rows_pad, int splits) {
+  AttnWs w{0, 0, 0, 0};
+  if (splits <= 1) return w;
+  const size_t pairs = (size_t)batch * num_kv_heads;
+  w.counters = kAttnMaxPairs * sizeof(int32_t);
+  w.acc = round_up(pairs * splits * rows_pad * 128 * sizeof(float), kAlign);
+  w.ml = round_up(pairs * splits * rows_pad * 2 * sizeof(float), kAlign);
+  w.total = w.counters + w.acc + w.ml;
+  return w;
 }
 
 size_t attn_ws_bytes(int batch, int num_q_heads, int num_kv_heads, int nq_max, int64_t tokens) {
   if (batch <= 0 || num_kv_heads <= 0 || num_q_heads % num_kv_heads) return 0;
   const int rt = attn_row_tiles(nq_max, num_q_heads / num_kv_heads);
-  const int splits = attn_splits(batch, num_kv_heads, tokens + nq_max, attn_slices(tokens + nq_max, rt));
-  if (splits <= 1) return 0;
-  const int rows_pad = rt * 16;
-  const size_t pairs = (size_t)batch * num_kv_heads;
-  const size_t acc = pairs * splits * rows_pad * 128 * sizeof(float);
-  const size_t ml = pairs * splits * rows_pad * 2 * sizeof(float);
-  return round_up(acc, kAlign) + round_up(ml, kAlign);
+  const int splits = attn_splits(batch, num_kv_heads, tokens + nq_max);
+  return attn_ws_layout(batch, num_kv_heads, rt * 16, splits).total;
 }
 
 dustin_status run_attention(bool sparse, const void* q, int64_t q_sb, int64_t q_st, int64_t q_sh,
@@ -159,6 +158,7 @@ dustin_status run_attention(bool sparse, const void* q, int64_t q_sb, int64_t q_
     return DUSTIN_ERR_INVALID_ARG;
   const int gs = num_q_heads / Hkv;
   if ((int64_t)bt->nq_max * gs > 128) return DUSTIN_ERR_UNSUPPORTED;
+  if ((int64_t)bt->batch * Hkv > kAttnMaxPairs) return DUSTIN_ERR_UNSUPPORTED;
   if (sparse) {
     if (!idx || !count || (groups != 1 && groups != Hkv)) return DUSTIN_ERR_INVALID_ARG;
     if (!aligned(idx, 4) || !aligned(count, 4) || idx_sb < 0 || idx_sg < 0)
@@ -170,6 +170,14 @@ dustin_status run_attention(bool sparse, const void* q, int64_t q_sb, int64_t q_
   if (st != DUSTIN_OK) return st;
   st = kv_of(v, 128, need, &vv);
   if (st != DUSTIN_OK) return st;
+  // the attention kernels address a row as base + 32-bit byte offset (row * stride_n * 2),
+  // with row = page * page_size + slot for a paged cache: pages must be packed back to back
+  for (const KvView* c : {&kv, &vv}) {
+    if (c->page_table && c->stride_page != ((int64_t)1 << c->page_shift) * c->stride_n)
+      return DUSTIN_ERR_UNSUPPORTED;
+    const int64_t rows = c->page_table ? ((int64_t)c->num_pages << c->page_shift) : c->capacity;
+    if ((rows - 1) * c->stride_n * 2 + 256 > (int64_t)UINT32_MAX) return DUSTIN_ERR_UNSUPPORTED;
+  }
   const int B = bt->batch;
   if (B == 0 || bt->nq_max == 0) return DUSTIN_OK;
   const int64_t tokens = sparse ? (int64_t)bt->k_max : (int64_t)bt->max_len;
@@ -199,17 +207,19 @@ dustin_status run_attention(bool sparse, const void* q, int64_t q_sb, int64_t q_
   a.pairs = B * Hkv;
   a.scale_log2 = scale * kLog2e;
   const int rt = attn_row_tiles(bt->nq_max, gs);
-  const int slices = attn_slices(tokens + bt->nq_max, rt);
   a.rows_pad = rt * 16;
-  a.splits = attn_splits(B, Hkv, tokens + bt->nq_max, slices);
+  const int64_t tokens_max = tokens + bt->nq_max;
+  a.splits = attn_splits(B, Hkv, tokens_max);
+  const int64_t steps_max = (tokens_max + 31) / 32;
+  a.split_steps = (int)((steps_max + a.splits - 1) / a.splits);
   if (a.splits > 1) {
+    const AttnWs w = attn_ws_layout(B, Hkv, a.rows_pad, a.splits);
     char* base = static_cast<char*>(ws);
-    const size_t pairs = (size_t)B * Hkv;
-    a.part_acc = reinterpret_cast<float*>(base);
-    const size_t acc = pairs * a.splits * a.rows_pad * 128 * sizeof(float);
-    a.part_ml = reinterpret_cast<float*>(base + round_up(acc, kAlign));
+    a.counters = reinterpret_cast<int32_t*>(base);
+    a.part_acc = reinterpret_cast<float*>(base + w.counters);
+    a.part_ml = reinterpret_cast<float*>(base + w.counters + w.acc);
   }
-  const hipError_t e = launch_verify_attn(a, rt, slices, sparse, kv.page_table != nullptr,
+  const hipError_t e = launch_verify_attn(a, rt, sparse, kv.page_table != nullptr,
                                           static_cast<hipStream_t>(stream));
   return e == hipSuccess ? DUSTIN_OK : DUSTIN_ERR_LAUNCH;
 }

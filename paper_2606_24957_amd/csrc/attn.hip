@@ -2,120 +2,198 @@
 // and dense (every committed position), both followed by the causal verification window.
 //
 // Work decomposition
-//   unit  (split, sequence b, KV head g).  All T_b * (Hq / Hkv) query rows of the KV head
-//         (its GQA group for every verification token) share each K/V row, so a selected
-//         row is fetched from HBM once per layer.
-//   slice the NH = 128 / DH workgroups of a unit each produce DH of the 128 output columns.
-//         They all need the full K row (for the scores) but only their V columns.  Their
-//         block ids are congruent mod 8, so the dispatcher puts them on the same XCD and
-//         the K rows the first one fetches are served to the others from that XCD's L2.
-//         This fills the chip without splitting the token list, so no partial results
-//         travel through memory; token splits are only used when units are scarce, and
-//         their partials are merged by a second, tiny kernel.
-//   wave  walks 32-token steps of the unit (waves interleave steps), with the next step's
-//         K/V loads in flight while the current one is computed:
-//           S^T[32 tok x rows] = K[32 x 128] Q^T    MFMA 16x16x32, K rows loaded straight
-//                                                   into A-operand registers (16 B/lane)
-//           online softmax over tokens (fp32, exp2 domain); the running max is only moved
-//           when a row's max grows by more than 2^8, a wave-uniform event, so the
-//           accumulator is rarely rescaled
-//           V^T via the LDS transpose load          V rows go to a wave-private LDS tile
-//                                                   and come back with 4 tokens of one
-//                                                   d column per lane, the PV layout
-//           O^T[DH x rows] += V^T P^T               MFMA 16x16x32; a ones tile gives the
-//                                                   row sums of the same bf16 weights
-//   merge the W waves' (max, sum, acc) through LDS in a fixed order (deterministic).
+//   unit   (sequence b, KV head g, token split).  All T_b * (Hq / Hkv) query rows of the
+//          KV head (its GQA group for every verification token) share each K/V row, so a
+//          row is fetched from HBM exactly once per layer, and a workgroup produces all
+//          128 output columns of its rows.  The token list is cut into as many splits as
+//          it takes to put one workgroup on every CU; the splits of a unit get block ids
+//          congruent mod 8 (one XCD) and the last one to finish merges them (below).
+//   wave   walks 32-token steps of its workgroup's range (the four waves interleave
+//          steps).  A step's K and V rows go straight from HBM into a wave-private LDS
+//          tile with the gfx950 direct-to-LDS load (global_load_lds_dwordx4): every load
+//          instruction moves four whole 256-byte rows, and no VGPR holds data in flight.
+//          The chunks of a row are XOR-swizzled so that the MFMA operand reads below are
+//          free of bank conflicts.  Per step:
+//            wait for the step's rows, read K (MFMA A layout) and V^T (LDS transpose
+//            load) into registers, start the next step's loads, then
+//            S^T[32 tok x rows] = K[32 x 128] Q^T     MFMA 16x16x32 bf16
+//            online softmax over tokens (fp32, exp2 domain); the running max only moves
+//            when a row's max grows by more than 2^8, a wave-uniform event, so the
+//            accumulator is rarely rescaled
+//            O^T[128 x rows] += V^T P^T               MFMA 16x16x32; a ones tile gives
+//                                                     the row sums of the same bf16 P
+//          so each wave keeps exactly one step (16 KB) in flight while it computes.
+//   merge  the waves' (max, sum, acc) combine through LDS in a fixed order.  With one
+//          split the workgroup writes the normalised output.  Otherwise it publishes its
+//          partial with write-through (agent-scope) stores, waits for them to complete,
+//          and counts itself in with an atomic add on the unit's counter; the workgroup
+//          that arrives last reads the other partials back with agent-scope loads,
+//          merges all of them in split order (deterministic whichever arrives last),
+//          writes the output and returns the counter to zero.  No workgroup waits for
+//          another and no cache is flushed.
 //
-// Gathered positions (sparse) and page translations (paged) are resolved once per unit
-// into an LDS table of physical rows, so the inner loop does no dependent global loads.
+// Gathered positions (sparse) and page translations (paged) are resolved into an LDS table
+// of physical rows before the token loop, so the loop does no dependent global loads.
 #include "kernels.hpp"
 
 namespace dustin {
 
 constexpr int kD = 128;
-#ifndef DUSTIN_ATTN_WAVES
-#define DUSTIN_ATTN_WAVES 4
-#endif
-#ifndef DUSTIN_ATTN_DEPTH
-#define DUSTIN_ATTN_DEPTH 1
-#endif
-constexpr int kAttnWavesPerGroup = DUSTIN_ATTN_WAVES;  // one wave per SIMD
-constexpr int kDepth = DUSTIN_ATTN_DEPTH;              // steps in flight ahead of the compute
-constexpr int kStageSteps = 192;         // 32-token steps whose rows are staged per chunk
-constexpr float kRescaleLog2 = 8.f;      // lazy rescale threshold (factor 256)
+constexpr int kW = 4;                  // waves per workgroup: one per SIMD
+constexpr int kStep = 32;              // tokens per wave step
+constexpr int kTile = kStep * kD * 2;  // bytes of one step's K (or V) rows: 8 KB
+constexpr int kStageBatch = 8;         // staged positions per thread per chunk
+constexpr int kStageSteps = kW * kWave * kStageBatch / 32;  // steps staged per chunk (64)
+constexpr float kRescaleLog2 = 8.f;    // lazy rescale threshold (factor 256)
+
 
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
-
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) void lds_void;
 
 // gfx950 LDS transpose load: within each 16-lane group, lane i receives element i % 4 of
 // the 8 bytes addressed by group lane 4 e + i / 4, for e = 0..3.
-__device__ __forceinline__ v4i16 lds_read_tr16(const uint16_t* p) {
+__device__ __forceinline__ v4i16 lds_read_tr16(const char* p) {
   return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
       (__attribute__((address_space(3))) v4i16*)(reinterpret_cast<uintptr_t>(p)));
+}
+
+// gfx950 direct-to-LDS load: lane l's 16 bytes at src land at lds + 16 l.
+__device__ __forceinline__ void load_lds16(const void* src, char* lds) {
+  __builtin_amdgcn_global_load_lds(src, (lds_void*)(reinterpret_cast<uintptr_t>(lds)), 16, 0, 0);
 }
 
 __device__ __forceinline__ uint32_t cvt_pk_bf16(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{lo, hi}, bf16x2));
 }
 
-template <int NKS>
-struct StepRegs {
-  u32x4 k[2][4];    // K rows of the step's two 16-token tiles (all 128 columns)
-  u32x4 v[2][NKS];  // V rows, this slice's columns only
-};
+// Workgroup barrier for hand-offs of ds_write data only.  It waits for the wave's LDS
+// instructions but, unlike __syncthreads (whose fence also covers direct-to-LDS loads),
+// not for its outstanding global loads: the wave's own loads of its next step keep flowing
+// across it.  The empty asm statements keep the compiler from moving memory accesses
+// across the barrier.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
 
-template <int RT, int W, int DH, bool kStage, bool kPaged>
-__global__ __launch_bounds__(W * kWave) void verify_attn_kernel(AttnArgs a) {
-  constexpr int NH = kD / DH;      // d slices per unit
-  constexpr int NDT = DH / 16;     // output 16-column tiles per wave
-  constexpr int NVK = DH / 32;     // 32-column V chunks per row
-  constexpr int kVPitch = DH + 8;  // LDS row pitch (bf16) of a wave's V tile
-  constexpr int kQPitch = kD + 8;  // LDS row pitch (bf16) of the staged queries
-  constexpr int kPitch = DH + 4;   // LDS row pitch (fp32) of the merged accumulator
-  // One LDS arena: staged rows | V tiles | queries during the token loop, the merged
-  // accumulator afterwards.
-  constexpr int kStageBytes = kStage ? kStageSteps * 32 * 4 : 0;
-  constexpr int kVBytes = W * 32 * kVPitch * 2;
-  constexpr int kQBytes = RT * 16 * kQPitch * 2;
-  constexpr int kLoopBytes = kStageBytes + kVBytes + kQBytes;
-  constexpr int kMergeBytes = RT * 16 * kPitch * 4;
-  __shared__ __attribute__((aligned(16))) char smem[kLoopBytes > kMergeBytes ? kLoopBytes : kMergeBytes];
-  uint32_t* const sm_phys = reinterpret_cast<uint32_t*>(smem);
-  uint16_t* const sm_q = reinterpret_cast<uint16_t*>(smem + kStageBytes + kVBytes);
-  float* const sm_acc = reinterpret_cast<float*>(smem);
+// s_waitcnt with only one counter constrained (gfx9 encoding; the others at their maxima)
+__device__ __forceinline__ void wait_vmem_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }  // vmcnt(0)
+__device__ __forceinline__ void wait_lds_all() { __builtin_amdgcn_s_waitcnt(0xC07F); }   // lgkmcnt(0)
+
+// Placement of a step's rows in a wave's 8 KB tile.  Load instruction i (0..7) fills LDS
+// rows 4 i .. 4 i + 3 with tokens i, 8 + i, 16 + i, 24 + i (lanes 16 q .. 16 q + 15 move
+// token 8 q + i), so token j of the step sits in LDS row 4 (j & 7) + (j >> 3).  Within a
+// row, the 16-byte chunk c of K is stored at chunk c ^ (j & 15) and chunk c of V at
+// c ^ 2 (j & 7): the 16 rows read by one MFMA operand load (K) and the four rows x eight
+// half-chunks of one transpose load (V) then fall into distinct LDS banks.
+__device__ __forceinline__ int tile_row(int j) { return 4 * (j & 7) + (j >> 3); }
+__device__ __forceinline__ int k_chunk(int j, int c) { return c ^ (j & 15); }
+__device__ __forceinline__ int v_chunk(int j, int c) { return c ^ ((j & 7) << 1); }
+
+template <int RT, bool kSparse, bool kPaged, bool kQReg>
+__global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
+  constexpr bool kStage = kSparse || kPaged;  // rows resolved through an LDS table
+  constexpr int NDT = kD / 16;     // output 16-column tiles
+  constexpr int kQPitch = kD + 8;  // LDS row pitch (bf16) of staged queries (kQReg false)
+  constexpr int kPitch = kD + 4;   // LDS row pitch (fp32) of the merged accumulator
+  constexpr int kTilesBytes = kW * 2 * kTile;                    // K and V tiles of every wave
+  constexpr int kStageBytes = kStage ? kStageSteps * kStep * 4 : 0;
+  constexpr int kQBytes = kQReg ? 0 : RT * 16 * kQPitch * 2;
+  constexpr int kLoopBytes = kTilesBytes + kStageBytes + kQBytes;
+  constexpr int kBufFloats = RT * 16 * kPitch;                  // one wave's accumulator
+  constexpr int kNB = RT <= 4 ? kW : 2;                          // wave accumulators LDS holds
+  constexpr int kFinalBytes = kNB * kBufFloats * 4;
+  __shared__ __attribute__((aligned(1024))) char smem[kLoopBytes > kFinalBytes ? kLoopBytes : kFinalBytes];
+  uint32_t* const sm_phys = reinterpret_cast<uint32_t*>(smem + kTilesBytes);
+  uint16_t* const sm_q = reinterpret_cast<uint16_t*>(smem + kTilesBytes + kStageBytes);
 
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);  // wave-uniform
   const int lr = lane & 15, lg = lane >> 4;
-  uint16_t* const vtile = reinterpret_cast<uint16_t*>(smem + kStageBytes) + wave * 32 * kVPitch;
+  char* const ktile = smem + wave * 2 * kTile;
+  char* const vtile = ktile + kTile;
 
-  const int id = blockIdx.x, xcd = id & 7, slot = id >> 3;
-  const int half = slot % NH;
-  const int unit = (slot / NH) * 8 + xcd;
-  if (unit >= a.splits * a.pairs) return;
-  const int pair = unit % a.pairs, split = unit / a.pairs;
+  // every XCD owns a contiguous run of (pair, split) units: the splits of a pair, and the
+  // KV heads of a sequence, share an XCD (its L2 and its address translations)
+  const int units = a.pairs * a.splits;
+  const int per_xcd = (units + 7) >> 3;
+  const int u = blockIdx.x >> 3, lin = (blockIdx.x & 7) * per_xcd + u;
+  if (u >= per_xcd || lin >= units) return;
+  const int pair = lin / a.splits, split = lin - pair * a.splits;
   const int b = pair / a.num_kv_heads, g = pair - b * a.num_kv_heads;
-  const int dbase = half * DH;
 
-  const int N = a.dims.len(b);
-  const int T = a.dims.nq(b);
-  if (T == 0) return;
+  // ---- prologue: one round trip.  The per-sequence sizes, the queries and the selected
+  // positions of the first chunk are loaded together; the latter two speculatively (every
+  // query slot, positions below k_max), which stays in bounds whatever the sizes are.
   const int gi = a.groups == 1 ? 0 : g;
-  int wstart = N;
-  const int32_t* idx_row = nullptr;
-  if (a.idx) {
-    wstart = clampi(a.count[b * a.groups + gi], 0, a.dims.k_max);
-    idx_row = a.idx + (int64_t)b * a.idx_sb + (int64_t)gi * a.idx_sg;
+  const int32_t* idx_row = kSparse ? a.idx + (int64_t)b * a.idx_sb + (int64_t)gi * a.idx_sg : nullptr;
+  const int n_raw = a.dims.seq_lens[b];
+  const int t_raw = a.dims.n_query ? a.dims.n_query[b] : a.dims.nq_max;
+  const int c_raw = kSparse ? a.count[b * a.groups + gi] : 0;
+  const int s_begin = split * a.split_steps;
+  const int rows_mem = a.dims.nq_max * a.group_size;  // query rows present in memory
+  auto q_row_ptr = [&](int r) {
+    const int t = r / a.group_size, hh = r - t * a.group_size;
+    return a.q + (int64_t)b * a.q_sb + (int64_t)t * a.q_st + (int64_t)(g * a.group_size + hh) * a.q_sh;
+  };
+  // Q^T as B operands: lane holds Q[row rt*16+lr][32 ks + 8 lg + e] (row r = t G + hh),
+  // in registers for up to 5 row tiles, else staged in LDS and read per step.
+  bf16x8 qreg[kQReg ? RT : 1][4];
+  constexpr int kQChunks = RT * 16 * (kD / 8), kQPer = (kQChunks + kW * kWave - 1) / (kW * kWave);
+  u32x4 qx[kQReg ? 1 : kQPer];
+  if constexpr (kQReg) {
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) {
+      const int r = rt * 16 + lr;
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks)
+        qreg[rt][ks] = r < rows_mem ? as_bf16x8(load16(q_row_ptr(r) + 8 * lg + 32 * ks))
+                                    : as_bf16x8(u32x4{0u, 0u, 0u, 0u});
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < kQPer; ++j) {
+      const int e = threadIdx.x + j * kW * kWave;
+      const int r = e / (kD / 8), c0 = (e % (kD / 8)) * 8;
+      qx[j] = (e < kQChunks && r < rows_mem) ? load16(q_row_ptr(r) + c0) : u32x4{0u, 0u, 0u, 0u};
+    }
   }
+  int32_t sel[kStageBatch];  // selected positions of this thread's tokens in a chunk
+  auto load_selection = [&](int cs) {
+#pragma unroll
+    for (int j = 0; j < kStageBatch; ++j) {
+      const int v = cs * kStep + (int)threadIdx.x + j * kW * kWave;
+      sel[j] = kSparse ? idx_row[min(v, a.dims.k_max - 1)] : 0;
+    }
+  };
+  if constexpr (kStage) load_selection(s_begin);
+  // the positions of this lane's tokens in the wave's first step, so that its loads can
+  // start before the block-wide staging pass (contiguous caches; a paged one needs the
+  // staged translation)
+  const int first_v0 = (s_begin + wave) * kStep + 8 * lg;
+  int32_t first_sel[8];
+  if constexpr (kStage && !kPaged) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) first_sel[i] = idx_row[min(first_v0 + i, a.dims.k_max - 1)];
+  }
+
+  const int N = clampi(n_raw, 0, a.dims.max_len);
+  const int T = clampi(t_raw, 0, a.dims.nq_max);
+  if (T == 0) return;
+  const int wstart = kSparse ? clampi(c_raw, 0, a.dims.k_max) : N;
   const int total = wstart + T;        // virtual tokens: selected (or all) then window
   const int rows = T * a.group_size;   // <= RT * 16 (checked on the host via nq_max)
-  const int nsteps = (total + 31) >> 5;
-  const int per_split = (nsteps + a.splits - 1) / a.splits;
-  const int s_begin = split * per_split;
-  const int s_end = min(nsteps, s_begin + per_split);
+  const int nsteps = (total + kStep - 1) / kStep;
+  // this sequence's split count: ranges of split_steps steps (the host sizes them for the
+  // longest sequence); splits past the end have nothing to do
+  const int nsplit = (nsteps + a.split_steps - 1) / a.split_steps;
+  if (split >= nsplit) return;
+  const int s_end = min(nsteps, s_begin + a.split_steps);
 
   // Rows are addressed as uniform base + 32-bit byte offset phys * stride_n (the host
   // checks that every offset fits): phys is the position (contiguous) or
@@ -123,61 +201,54 @@ __global__ __launch_bounds__(W * kWave) void verify_attn_kernel(AttnArgs a) {
   const char* kbase = reinterpret_cast<const char*>(
       a.k.data + (kPaged ? 0 : (int64_t)b * a.k.stride_b) + (int64_t)g * a.k.stride_h);
   const char* vbase = reinterpret_cast<const char*>(
-      a.v.data + (kPaged ? 0 : (int64_t)b * a.v.stride_b) + (int64_t)g * a.v.stride_h + dbase);
+      a.v.data + (kPaged ? 0 : (int64_t)b * a.v.stride_b) + (int64_t)g * a.v.stride_h);
   const uint32_t kstride = (uint32_t)a.k.stride_n * 2u, vstride = (uint32_t)a.v.stride_n * 2u;
 
-  // physical row of virtual token v (clamped into the cache; past-the-end -> row 0)
-  auto phys_of = [&](int v) -> uint32_t {
+  // Position of virtual token v (clamped into the cache; past-the-end -> 0) and its
+  // physical row.
+  auto pos_of = [&](int v, int32_t selected) -> int64_t {
     int64_t pos;
-    if (v < wstart) pos = idx_row ? (int64_t)idx_row[v] : (int64_t)v;
+    if (v < wstart) pos = kSparse ? (int64_t)selected : (int64_t)v;
     else if (v < total) pos = (int64_t)N + (v - wstart);
     else pos = 0;
-    pos = pos < 0 ? 0 : (pos >= a.k.capacity ? a.k.capacity - 1 : pos);
-    if constexpr (kPaged) {
-      const int page = clampi(a.k.page_table[(int64_t)b * a.k.max_pages + (pos >> a.k.page_shift)], 0,
-                              a.k.num_pages - 1);
+    return pos < 0 ? 0 : (pos >= a.k.capacity ? a.k.capacity - 1 : pos);
+  };
+  auto page_of = [&](int64_t pos) -> int {
+    return clampi(a.k.page_table[(int64_t)b * a.k.max_pages + (pos >> a.k.page_shift)], 0,
+                  a.k.num_pages - 1);
+  };
+  auto phys_at = [&](int64_t pos, int page) -> uint32_t {
+    if constexpr (kPaged)
       return ((uint32_t)page << a.k.page_shift) | (uint32_t)(pos & ((1 << a.k.page_shift) - 1));
-    } else {
+    else
       return (uint32_t)pos;
-    }
   };
 
-  // Q^T as B operands: lane holds Q[row rt*16+lr][32 ks + 8 lg + e] (row r = t G + hh).
-  // They are staged in LDS and read per step (16-byte reads), which keeps the VGPRs for
-  // the in-flight K/V rows.
-  constexpr bool kQLds = true;
-  bf16x8 qreg[kQLds ? 1 : RT][4];
   int limit[RT];  // token v is visible to this lane's row iff v <= limit
 #pragma unroll
   for (int rt = 0; rt < RT; ++rt) {
     const int r = rt * 16 + lr;
     limit[rt] = wstart + (r < rows ? r / a.group_size : T - 1);
   }
-  auto q_row_ptr = [&](int r) {
-    const int t = r / a.group_size, hh = r - t * a.group_size;
-    return a.q + (int64_t)b * a.q_sb + (int64_t)t * a.q_st + (int64_t)(g * a.group_size + hh) * a.q_sh;
-  };
-  if constexpr (kQLds) {
-    for (int u = threadIdx.x; u < RT * 16 * (kD / 8); u += W * kWave) {
-      const int r = u / (kD / 8), c0 = (u % (kD / 8)) * 8;
-      const u32x4 x = r < rows ? load16(q_row_ptr(r) + c0) : u32x4{0u, 0u, 0u, 0u};
-      *reinterpret_cast<u32x4*>(sm_q + r * kQPitch + c0) = x;
-    }
+  if constexpr (kQReg) {
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt)
+      if (rt * 16 + lr >= rows)  // rows of absent verification tokens act as zero queries
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) qreg[rt][ks] = as_bf16x8(u32x4{0u, 0u, 0u, 0u});
   } else {
 #pragma unroll
-    for (int rt = 0; rt < RT; ++rt) {
-      const int r = rt * 16 + lr;
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks)
-        qreg[rt][ks] = r < rows ? as_bf16x8(load16(q_row_ptr(r) + 8 * lg + 32 * ks))
-                                : as_bf16x8(u32x4{0u, 0u, 0u, 0u});
+    for (int j = 0; j < kQPer; ++j) {
+      const int e = threadIdx.x + j * kW * kWave;
+      const int r = e / (kD / 8), c0 = (e % (kD / 8)) * 8;
+      if (e < kQChunks) *reinterpret_cast<u32x4*>(sm_q + r * kQPitch + c0) = r < rows ? qx[j] : u32x4{0u, 0u, 0u, 0u};
     }
   }
   auto q_operand = [&](int rt, int ks) -> bf16x8 {
-    if constexpr (kQLds)
-      return as_bf16x8(*reinterpret_cast<const u32x4*>(sm_q + (rt * 16 + lr) * kQPitch + 8 * lg + 32 * ks));
-    else
+    if constexpr (kQReg)
       return qreg[rt][ks];
+    else
+      return as_bf16x8(*reinterpret_cast<const u32x4*>(sm_q + (rt * 16 + lr) * kQPitch + 8 * lg + 32 * ks));
   };
 
   // A operand of ones: one MFMA per row tile sums the bf16 probabilities of a step, so the
@@ -196,37 +267,72 @@ __global__ __launch_bounds__(W * kWave) void verify_attn_kernel(AttnArgs a) {
 
   int chunk_v0 = 0;  // first virtual token staged in sm_phys
 
-  // K rows of both tiles first, then V rows: the score MFMAs wait for K only.
-  auto issue = [&](int st, StepRegs<NVK>& R) {
-    uint32_t phys[2];
+  // Loads of one step into this wave's tiles: this lane moves chunk lr of tokens 8 lg + i
+  // (i = 0..7) of the step, whose physical rows are ph[i]; one instruction per i for K and
+  // one for V.
+  auto issue_rows = [&](const uint32_t (&ph)[8]) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int v = (st << 5) + 16 * i + lr;
-      if constexpr (kStage) phys[i] = sm_phys[v - chunk_v0];
-      else phys[i] = v < total ? (uint32_t)v : 0u;
+    for (int i = 0; i < 8; ++i) {
+      const int j = 8 * lg + i;
+      load_lds16(kbase + ph[i] * kstride + 16 * k_chunk(j, lr), ktile + i * 1024);
+      load_lds16(vbase + ph[i] * vstride + 16 * v_chunk(j, lr), vtile + i * 1024);
     }
+  };
+  auto issue = [&](int st) {
+    const int v0 = st * kStep + 8 * lg;
+    uint32_t ph[8];
+    if constexpr (kStage) {
+      const u32x4* src = reinterpret_cast<const u32x4*>(sm_phys + (v0 - chunk_v0));
+      const u32x4 p0 = src[0], p1 = src[1];
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const uint16_t* kp = reinterpret_cast<const uint16_t*>(kbase + phys[i] * kstride) + 8 * lg;
+      for (int i = 0; i < 4; ++i) {
+        ph[i] = p0[i];
+        ph[4 + i] = p1[i];
+      }
+    } else {
 #pragma unroll
-      for (int ks = 0; ks < 4; ++ks) R.k[i][ks] = load16(kp + 32 * ks);
+      for (int i = 0; i < 8; ++i) ph[i] = v0 + i < total ? (uint32_t)(v0 + i) : 0u;
     }
+    issue_rows(ph);
+  };
+
+  struct Operands {
+    bf16x8 k[2][4];    // K rows of the step's two 16-token tiles (MFMA A layout)
+    bf16x8 vt[NDT];    // V^T of each 16-column tile over the 32 tokens (MFMA A layout)
+  };
+
+  // Reads the step's operands out of this wave's tiles (after its loads completed).
+  auto read_tiles = [&](Operands& op) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const uint16_t* vp = reinterpret_cast<const uint16_t*>(vbase + phys[i] * vstride) + 8 * lg;
+    for (int t2 = 0; t2 < 2; ++t2) {
+      const int j = 16 * t2 + lr;
+      const char* row = ktile + tile_row(j) * 256;
 #pragma unroll
-      for (int kv = 0; kv < NVK; ++kv) R.v[i][kv] = load16(vp + 32 * kv);
+      for (int ks = 0; ks < 4; ++ks)
+        op.k[t2][ks] = as_bf16x8(*reinterpret_cast<const u32x4*>(row + 16 * k_chunk(j, 4 * ks + lg)));
+    }
+    // lane lr of a 16-lane group addresses token 4 lg + lr / 4 (+16 for the second half of
+    // k), columns 16 dt + 4 (lr % 4) .. + 3; it receives V[token 4 lg + e (+16)][16 dt + lr]
+    const int j0 = 4 * lg + (lr >> 2), j1 = j0 + 16;
+    const char* r0 = vtile + tile_row(j0) * 256 + 8 * (lr & 1);
+    const char* r1 = vtile + tile_row(j1) * 256 + 8 * (lr & 1);
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt) {
+      const int c = 2 * dt + ((lr >> 1) & 1);
+      const v4i16 lo = lds_read_tr16(r0 + 16 * v_chunk(j0, c));
+      const v4i16 hi = lds_read_tr16(r1 + 16 * v_chunk(j1, c));
+      op.vt[dt] = as_bf16x8(u32x4{__builtin_bit_cast(u32x2, lo)[0], __builtin_bit_cast(u32x2, lo)[1],
+                                  __builtin_bit_cast(u32x2, hi)[0], __builtin_bit_cast(u32x2, hi)[1]});
     }
   };
 
-  // One 32-token step: V rows to this wave's LDS tile; (1) the score tiles of every 16-row
-  // tile; (2) the softmax of each (one wave-uniform decision to move the reference maxima);
-  // (3) per 16-column tile of V, its transposed operand read back with the LDS transpose
-  // load and applied to every row tile.  Scores stay in raw units until one FMA forms
+  // One 32-token step on register operands: (1) the score tiles of every 16-row tile;
+  // (2) the softmax of each (one wave-uniform decision to move the reference maxima);
+  // (3) the value product.  Scores stay in raw units until one FMA forms
   // (s * scale * log2 e - m) inside exp2; the reference max m is in scaled units.
-  auto compute = [&](int st, const StepRegs<NVK>& R) {
-    const int v0 = st << 5;
-    const bool edge = v0 + 31 >= wstart;  // wave-uniform: masking only near the window
+  auto compute = [&](int st, const Operands& op) {
+    const int v0 = st * kStep;
+    const bool edge = v0 + kStep - 1 >= wstart;  // wave-uniform: masking only near the window
     // (1) S^T tiles: lane holds tokens v0 + 16 i + 4 lg + e for query row rt*16 + lr
     f32x4 sc[RT][2];
 #pragma unroll
@@ -235,15 +341,9 @@ __global__ __launch_bounds__(W * kWave) void verify_attn_kernel(AttnArgs a) {
       for (int i = 0; i < 2; ++i) {
         f32x4 c = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int ks = 0; ks < 4; ++ks) c = mfma16x16x32(as_bf16x8(R.k[i][ks]), q_operand(rt, ks), c);
+        for (int ks = 0; ks < 4; ++ks) c = mfma16x16x32(op.k[i][ks], q_operand(rt, ks), c);
         sc[rt][i] = c;
       }
-    // V rows of the step into this wave's LDS tile (read back transposed in (3))
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int kv = 0; kv < NVK; ++kv)
-        *reinterpret_cast<u32x4*>(vtile + (16 * i + lr) * kVPitch + 32 * kv + 8 * lg) = R.v[i][kv];
     // (2) masked row maxima, lazy rescale, probabilities
     float mx[RT];
     bool grow = false;
@@ -287,225 +387,294 @@ __global__ __launch_bounds__(W * kWave) void verify_attn_kernel(AttnArgs a) {
                                cvt_pk_bf16(p[1][0], p[1][1]), cvt_pk_bf16(p[1][2], p[1][3])});
       accl[rt] = mfma16x16x32(ones, pT[rt], accl[rt]);
     }
-    // (3) V^T A operand of column tile dt via the LDS transpose load: in each 16-lane
-    // group, lane j points at row 4 lg + j / 4 (+16 for tile 1), columns 16 dt + 4 (j % 4);
-    // lane lr then receives V[token 4 lg + e (+16)][16 dt + lr], e = 0..3.
-    const uint16_t* trow = vtile + (4 * lg + (lr >> 2)) * kVPitch + 4 * (lr & 3);
+    // (3) O^T tiles
 #pragma unroll
-    for (int dt = 0; dt < NDT; ++dt) {
-      const v4i16 lo = lds_read_tr16(trow + 16 * dt);
-      const v4i16 hi = lds_read_tr16(trow + 16 * kVPitch + 16 * dt);
-      const bf16x8 vt = as_bf16x8(u32x4{__builtin_bit_cast(u32x2, lo)[0], __builtin_bit_cast(u32x2, lo)[1],
-                                        __builtin_bit_cast(u32x2, hi)[0], __builtin_bit_cast(u32x2, hi)[1]});
+    for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
-      for (int rt = 0; rt < RT; ++rt) acc[rt][dt] = mfma16x16x32(vt, pT[rt], acc[rt][dt]);
-    }
+      for (int rt = 0; rt < RT; ++rt) acc[rt][dt] = mfma16x16x32(op.vt[dt], pT[rt], acc[rt][dt]);
   };
 
-  // Ring of kDepth + 1 register buffers: step i + kDepth is issued before step i is
-  // computed.  Issues past this wave's last step repeat that step (an L2 hit), so every
-  // compute is preceded by exactly kDepth younger steps and waits for its own loads only.
-  StepRegs<NVK> R[kDepth + 1];
+  // Physical rows of this thread's tokens in chunk cs (reads sel, and the page table).
+  uint32_t staged[kStageBatch];
+  auto stage_rows = [&](int cs) {
+    int64_t pos[kStageBatch];
+    int page[kStageBatch];
+#pragma unroll
+    for (int j = 0; j < kStageBatch; ++j) pos[j] = pos_of(cs * kStep + (int)threadIdx.x + j * kW * kWave, sel[j]);
+#pragma unroll
+    for (int j = 0; j < kStageBatch; ++j) page[j] = kPaged ? page_of(pos[j]) : 0;
+#pragma unroll
+    for (int j = 0; j < kStageBatch; ++j) staged[j] = phys_at(pos[j], page[j]);
+  };
+  auto store_staged = [&](int cs, int ce) {
+    chunk_v0 = cs * kStep;
+    const int nv = ce * kStep - chunk_v0;
+#pragma unroll
+    for (int j = 0; j < kStageBatch; ++j) {
+      const int e = (int)threadIdx.x + j * kW * kWave;
+      if (e < nv) sm_phys[e] = staged[j];
+    }
+  };
+  // the first chunk's table is written before anything else is issued
+  if constexpr (kStage) {
+    stage_rows(s_begin);
+    store_staged(s_begin, min(s_end, s_begin + kStageSteps));
+  }
+
+  // This wave's first step, if it lies in the first chunk, is issued right away: after
+  // every prologue load has been consumed, so that no later wait waits for its rows.
+  wait_vmem_all();
+  __builtin_amdgcn_sched_barrier(0);
+  bool first_issued = false;
+  if constexpr (!kPaged) {
+    if (s_begin + wave < min(s_end, s_begin + kStageSteps)) {
+      uint32_t ph[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        if constexpr (kStage) ph[i] = phys_at(pos_of(first_v0 + i, first_sel[i]), 0);
+        else ph[i] = first_v0 + i < total ? (uint32_t)(first_v0 + i) : 0u;
+      }
+      issue_rows(ph);
+      first_issued = true;
+    }
+  }
   for (int cs = s_begin; cs < s_end; cs += kStageSteps) {
     const int ce = min(s_end, cs + kStageSteps);
     if constexpr (kStage) {
-      __syncthreads();  // the previous chunk's rows are no longer read
-      chunk_v0 = cs << 5;
-      for (int v = chunk_v0 + threadIdx.x; v < (ce << 5); v += W * kWave) sm_phys[v - chunk_v0] = phys_of(v);
-    }
-    __syncthreads();  // staged rows (and staged queries) are visible
-    const int first = cs + wave;
-    const int nw = first < ce ? (ce - first + W - 1) / W : 0;  // this wave's steps: first + i W
-    if (nw == 0) continue;
-    auto step = [&](int i) { return first + min(i, nw - 1) * W; };
-#pragma unroll
-    for (int j = 0; j < kDepth; ++j) issue(step(j), R[j]);
-    int i = 0;
-    bool more = true;
-    while (more) {
-#pragma unroll
-      for (int j = 0; j <= kDepth; ++j) {
-        issue(step(i + kDepth), R[(j + kDepth) % (kDepth + 1)]);
-        // keep the prefetch ahead of every wait of this step's compute
-        __builtin_amdgcn_sched_barrier(0);
-        compute(step(i), R[j]);
-        if (++i == nw) {
-          more = false;
-          break;
-        }
+      if (cs != s_begin) {
+        __syncthreads();  // the previous chunk's rows are no longer read
+        load_selection(cs);
+        stage_rows(cs);
+        store_staged(cs, ce);
       }
     }
+    lds_barrier();  // staged rows (and staged queries) are visible
+    // this wave's steps: cs + wave + i kW
+    int st = cs + wave;
+    if (st >= ce) continue;
+    if (!(first_issued && cs == s_begin)) issue(st);
+    while (true) {
+      wait_vmem_all();  // this step's rows are in the tiles
+      Operands op;
+      read_tiles(op);
+      const int next = st + kW;
+      if (next < ce) {
+        wait_lds_all();  // the tiles have been read out before the next loads overwrite them
+        issue(next);
+      }
+      compute(st, op);
+      if (next >= ce) break;
+      st = next;
+    }
   }
 
-  // ---- merge the W waves (fixed order: deterministic) ----
-  __shared__ float sm_m[W][RT * 16];
-  __shared__ float sm_l[W][RT * 16];
-  __shared__ float sm_ML[2][RT * 16];
+  // ---- combine the waves: each leaves its raw (max, sum, acc) in LDS; then every thread
+  // merges four columns of its rows over the waves, in wave order (deterministic) ----
+  __shared__ float sm_m[kW][RT * 16];
+  __shared__ float sm_l[kW][RT * 16];
+  __shared__ int sm_last;
+  float* const bufs = reinterpret_cast<float*>(smem);  // [kNB][RT * 16][kPitch]
+  auto put_acc = [&](float* buf) {
 #pragma unroll
-  for (int rt = 0; rt < RT; ++rt) {
-    if (lg == 0) {
-      sm_m[wave][rt * 16 + lr] = m_ref[rt];
-      sm_l[wave][rt * 16 + lr] = accl[rt][0];
-    }
-  }
-  __syncthreads();
-  float fac[RT];
+    for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-  for (int rt = 0; rt < RT; ++rt) {
-    const int r = rt * 16 + lr;
-    float M = -INFINITY;
+      for (int dt = 0; dt < NDT; ++dt)
+        *reinterpret_cast<f32x4*>(buf + (rt * 16 + lr) * kPitch + 16 * dt + 4 * lg) = acc[rt][dt];
+  };
+  auto put_stats = [&]() {
+    if (lg == 0)
 #pragma unroll
-    for (int w = 0; w < W; ++w) M = fmaxf(M, sm_m[w][r]);
-    const float Mu = M == -INFINITY ? 0.f : M;
-    fac[rt] = m_ref[rt] == -INFINITY ? 0.f : fast_exp2(m_ref[rt] - Mu);
-    if (wave == 0 && lg == 0) {
-      float L = 0.f;
-#pragma unroll
-      for (int w = 0; w < W; ++w)
-        L += sm_m[w][r] == -INFINITY ? 0.f : sm_l[w][r] * fast_exp2(sm_m[w][r] - Mu);
-      sm_ML[0][r] = M;
-      sm_ML[1][r] = L;
-    }
-  }
-#pragma unroll 1
-  for (int w = 0; w < W; ++w) {
-    if (wave == w) {
-#pragma unroll
-      for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-        for (int dt = 0; dt < NDT; ++dt) {
-          float* dst = sm_acc + (rt * 16 + lr) * kPitch + 16 * dt + 4 * lg;
-          const f32x4 val = acc[rt][dt] * fac[rt];
-          if (w == 0) *reinterpret_cast<f32x4*>(dst) = val;
-          else *reinterpret_cast<f32x4*>(dst) = *reinterpret_cast<f32x4*>(dst) + val;
-        }
-    }
+      for (int rt = 0; rt < RT; ++rt) {
+        sm_m[wave][rt * 16 + lr] = m_ref[rt];
+        sm_l[wave][rt * 16 + lr] = accl[rt][0];
+      }
+  };
+  put_stats();
+  __syncthreads();  // every wave is past its token loop: the tiles are free
+  if constexpr (kNB < kW) {
+    // not enough LDS for one buffer per wave: waves kNB.. fold into waves 0.. first
+    if (wave >= kNB) put_acc(bufs + (wave - kNB) * kBufFloats);
     __syncthreads();
-  }
-
-  const int nthreads = W * kWave;
-  if (a.splits == 1) {
-    for (int u = threadIdx.x; u < rows * (DH / 8); u += nthreads) {
-      const int r = u / (DH / 8), c0 = (u % (DH / 8)) * 8;
-      const int t = r / a.group_size, hh = r - t * a.group_size;
-      const float L = sm_ML[1][r];
-      const float inv = L > 0.f ? 1.f / L : 0.f;
-      const float* src = sm_acc + r * kPitch + c0;
-      u32x4 o;
+    if (wave < kNB) {
+      const int p = wave + kNB;
+      const float* pb = bufs + wave * kBufFloats;
 #pragma unroll
-      for (int e2 = 0; e2 < 4; ++e2) o[e2] = cvt_pk_bf16(src[2 * e2] * inv, src[2 * e2 + 1] * inv);
-      uint16_t* op = a.out + (int64_t)b * a.o_sb + (int64_t)t * a.o_st +
-                     (int64_t)(g * a.group_size + hh) * a.o_sh + dbase + c0;
-      *reinterpret_cast<u32x4*>(op) = o;
+      for (int rt = 0; rt < RT; ++rt) {
+        const int r = rt * 16 + lr;
+        const float mp = sm_m[p][r], lp = sm_l[p][r];
+        const float M = fmaxf(m_ref[rt], mp), Mu = M == -INFINITY ? 0.f : M;
+        const float fa = m_ref[rt] == -INFINITY ? 0.f : fast_exp2(m_ref[rt] - Mu);
+        const float fb = mp == -INFINITY ? 0.f : fast_exp2(mp - Mu);
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt)
+          acc[rt][dt] = acc[rt][dt] * fa + *reinterpret_cast<const f32x4*>(pb + r * kPitch + 16 * dt + 4 * lg) * fb;
+        accl[rt][0] = accl[rt][0] * fa + lp * fb;
+        m_ref[rt] = M;
+      }
     }
-    return;
+    __syncthreads();  // the folded buffers have been read
+    if (wave < kNB) put_stats();
   }
-  // several token splits: publish this split's partial; verify_attn_combine merges them
-  const int64_t prow = ((int64_t)pair * a.splits + split) * a.rows_pad;
-  for (int u = threadIdx.x; u < rows * (DH / 4); u += nthreads) {
-    const int r = u / (DH / 4), c0 = (u % (DH / 4)) * 4;
-    *reinterpret_cast<f32x4*>(a.part_acc + (prow + r) * kD + dbase + c0) =
-        *reinterpret_cast<const f32x4*>(sm_acc + r * kPitch + c0);
-  }
-  if (half == 0)
-    for (int r = threadIdx.x; r < rows; r += nthreads) {
-      a.part_ml[(prow + r) * 2] = sm_ML[0][r];
-      a.part_ml[(prow + r) * 2 + 1] = sm_ML[1][r];
-    }
-}
+  if (wave < kNB) put_acc(bufs + wave * kBufFloats);
+  __syncthreads();
 
-// Merges the token splits of every (b, g): one workgroup per unit, fixed split order.
-__global__ __launch_bounds__(256) void verify_attn_combine(AttnArgs a) {
-  const int pair = blockIdx.x;
-  const int b = pair / a.num_kv_heads, g = pair - b * a.num_kv_heads;
-  const int T = a.dims.nq(b);
-  const int rows = T * a.group_size;
-  const int64_t base = (int64_t)pair * a.splits * a.rows_pad;
-  extern __shared__ float fac[];  // [splits][rows_pad]
-  for (int r = threadIdx.x; r < rows; r += blockDim.x) {
+  // thread element k: row e / 32, columns 4 (e % 32) .. + 3, e = threadIdx.x + 256 k
+  constexpr int nthreads = kW * kWave;
+  constexpr int KE = (RT * 16 * (kD / 4) + nthreads - 1) / nthreads;
+  const int nel = rows * (kD / 4);
+  f32x4 o[KE];
+  float Mk[KE], Lk[KE];
+#pragma unroll
+  for (int k = 0; k < KE; ++k) {
+    const int e = min((int)threadIdx.x + k * nthreads, nel - 1);
+    const int r = e / (kD / 4), c0 = (e % (kD / 4)) * 4;
     float M = -INFINITY;
-    for (int sp = 0; sp < a.splits; ++sp) M = fmaxf(M, a.part_ml[(base + (int64_t)sp * a.rows_pad + r) * 2]);
+#pragma unroll
+    for (int w = 0; w < kNB; ++w) M = fmaxf(M, sm_m[w][r]);
     const float Mu = M == -INFINITY ? 0.f : M;
     float L = 0.f;
-    for (int sp = 0; sp < a.splits; ++sp) {
-      const float* ml = a.part_ml + (base + (int64_t)sp * a.rows_pad + r) * 2;
-      const float f = ml[0] == -INFINITY ? 0.f : exp2f(ml[0] - Mu);
-      fac[sp * a.rows_pad + r] = f;
-      L += ml[1] * f;
-    }
-    const float inv = L > 0.f ? 1.f / L : 0.f;
-    for (int sp = 0; sp < a.splits; ++sp) fac[sp * a.rows_pad + r] *= inv;
-  }
-  __syncthreads();
-  for (int u = threadIdx.x; u < rows * (kD / 8); u += blockDim.x) {
-    const int r = u / (kD / 8), c0 = (u % (kD / 8)) * 8;
-    float o8[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    for (int sp = 0; sp < a.splits; ++sp) {
-      const float f = fac[sp * a.rows_pad + r];
-      const float* src = a.part_acc + (base + (int64_t)sp * a.rows_pad + r) * kD + c0;
-      const f32x4 x0 = *reinterpret_cast<const f32x4*>(src);
-      const f32x4 x1 = *reinterpret_cast<const f32x4*>(src + 4);
+    f32x4 sum = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        o8[e] += f * x0[e];
-        o8[4 + e] += f * x1[e];
+    for (int w = 0; w < kNB; ++w) {
+      const float mw = sm_m[w][r];
+      const float f = mw == -INFINITY ? 0.f : fast_exp2(mw - Mu);
+      L += sm_l[w][r] * f;
+      sum += *reinterpret_cast<const f32x4*>(bufs + w * kBufFloats + r * kPitch + c0) * f;
+    }
+    o[k] = sum;
+    Mk[k] = M;
+    Lk[k] = L;
+  }
+
+  auto out_ptr = [&](int r) {
+    const int t = r / a.group_size, hh = r - t * a.group_size;
+    return a.out + (int64_t)b * a.o_sb + (int64_t)t * a.o_st + (int64_t)(g * a.group_size + hh) * a.o_sh;
+  };
+  auto store_out = [&](int k, const f32x4& v) {
+    const int e = (int)threadIdx.x + k * nthreads;
+    if (e < nel) {
+      const int r = e / (kD / 4), c0 = (e % (kD / 4)) * 4;
+      *reinterpret_cast<u32x2*>(out_ptr(r) + c0) = u32x2{cvt_pk_bf16(v[0], v[1]), cvt_pk_bf16(v[2], v[3])};
+    }
+  };
+  if (nsplit == 1) {
+#pragma unroll
+    for (int k = 0; k < KE; ++k) store_out(k, o[k] * (Lk[k] > 0.f ? 1.f / Lk[k] : 0.f));
+    return;
+  }
+
+  // ---- several splits: publish (write-through), count in; the last one merges ----
+  // A split's partial is [rows][128] fp32 (unnormalised, relative to its row maxima) plus
+  // (max, sum) per row, reached through buffer resources whose stores and loads carry the
+  // agent-scope (sc1) cache policy, so they are coherent across XCDs without cache flushes.
+  constexpr int kSC1 = 16;
+  auto part_rsrc = [&](int sp) {
+    return __builtin_amdgcn_make_buffer_rsrc(a.part_acc + ((int64_t)pair * a.splits + sp) * a.rows_pad * kD, 0,
+                                             a.rows_pad * kD * 4, 0x00020000);
+  };
+  auto ml_rsrc = [&](int sp) {
+    return __builtin_amdgcn_make_buffer_rsrc(a.part_ml + ((int64_t)pair * a.splits + sp) * a.rows_pad * 2, 0,
+                                             a.rows_pad * 2 * 4, 0x00020000);
+  };
+  {
+    const auto ra = part_rsrc(split), rm = ml_rsrc(split);
+#pragma unroll
+    for (int k = 0; k < KE; ++k) {
+      const int e = (int)threadIdx.x + k * nthreads;
+      if (e < nel) {
+        const int r = e / (kD / 4), c0 = (e % (kD / 4)) * 4;
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, o[k]), ra, (r * kD + c0) * 4, 0, kSC1);
+        if (c0 == 0)
+          __builtin_amdgcn_raw_buffer_store_b64(u32x2{__float_as_uint(Mk[k]), __float_as_uint(Lk[k])}, rm, r * 8, 0,
+                                                kSC1);
       }
     }
-    const int t = r / a.group_size, hh = r - t * a.group_size;
-    u32x4 o;
-#pragma unroll
-    for (int e2 = 0; e2 < 4; ++e2) o[e2] = cvt_pk_bf16(o8[2 * e2], o8[2 * e2 + 1]);
-    uint16_t* op = a.out + (int64_t)b * a.o_sb + (int64_t)t * a.o_st +
-                   (int64_t)(g * a.group_size + hh) * a.o_sh + c0;
-    *reinterpret_cast<u32x4*>(op) = o;
   }
+  wait_vmem_all();  // this thread's write-through stores have completed
+  __syncthreads();  // ... and every other thread's
+  if (threadIdx.x == 0)
+    sm_last = __hip_atomic_fetch_add(a.counters + pair, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == nsplit - 1;
+  __syncthreads();
+  if (!sm_last) return;
+  if (threadIdx.x == 0) __hip_atomic_store(a.counters + pair, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+
+  // merge the splits online in split order (the same order whichever workgroup is last):
+  // this workgroup's own partial from registers, every other one read back with one
+  // batch of loads
+  f32x4 res[KE];
+  float Mr[KE], Lr[KE];
+  for (int sp = 0; sp < nsplit; ++sp) {
+    f32x4 x[KE];
+    float ms[KE], ls[KE];
+    if (sp == split) {
+#pragma unroll
+      for (int k = 0; k < KE; ++k) {
+        x[k] = o[k];
+        ms[k] = Mk[k];
+        ls[k] = Lk[k];
+      }
+    } else {
+      const auto ra = part_rsrc(sp), rm = ml_rsrc(sp);
+#pragma unroll
+      for (int k = 0; k < KE; ++k) {
+        const int e = min((int)threadIdx.x + k * nthreads, nel - 1);
+        const int r = e / (kD / 4), c0 = (e % (kD / 4)) * 4;
+        x[k] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(ra, (r * kD + c0) * 4, 0, kSC1));
+        const u32x2 ml = __builtin_amdgcn_raw_buffer_load_b64(rm, r * 8, 0, kSC1);
+        ms[k] = __uint_as_float(ml[0]);
+        ls[k] = __uint_as_float(ml[1]);
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < KE; ++k) {
+      if (sp == 0) {
+        res[k] = x[k];
+        Mr[k] = ms[k];
+        Lr[k] = ls[k];
+      } else {
+        const float M = fmaxf(Mr[k], ms[k]), Mu = M == -INFINITY ? 0.f : M;
+        const float fa = Mr[k] == -INFINITY ? 0.f : fast_exp2(Mr[k] - Mu);
+        const float fb = ms[k] == -INFINITY ? 0.f : fast_exp2(ms[k] - Mu);
+        res[k] = res[k] * fa + x[k] * fb;
+        Lr[k] = Lr[k] * fa + ls[k] * fb;
+        Mr[k] = M;
+      }
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < KE; ++k) store_out(k, res[k] * (Lr[k] > 0.f ? 1.f / Lr[k] : 0.f));
 }
 
 // ------------------------------------------------------------------------- host side
 
-template <int RT, int W, int DH, bool kStage, bool kPaged>
+template <int RT, bool kSparse, bool kPaged>
 static hipError_t launch_rt(const AttnArgs& a, hipStream_t stream) {
-  constexpr int NH = kD / DH;
   const int units = a.splits * a.pairs;
-  const int blocks = ((units + 7) / 8) * 8 * NH;
-  hipLaunchKernelGGL((verify_attn_kernel<RT, W, DH, kStage, kPaged>), dim3(blocks), dim3(W * kWave), 0,
+  const int blocks = (units + 7) / 8 * 8;
+  constexpr bool kQReg = RT <= 5;
+  hipLaunchKernelGGL((verify_attn_kernel<RT, kSparse, kPaged, kQReg>), dim3(blocks), dim3(kW * kWave), 0,
                      stream, a);
   return hipGetLastError();
 }
 
-template <int DH, bool kStage, bool kPaged>
+template <bool kSparse, bool kPaged>
 static hipError_t launch_kind(const AttnArgs& a, int rt, hipStream_t stream) {
-  constexpr int W = kAttnWavesPerGroup;
   switch (rt) {
-    case 1: return launch_rt<1, W, DH, kStage, kPaged>(a, stream);
-    case 2: return launch_rt<2, W, DH, kStage, kPaged>(a, stream);
-    case 3: return launch_rt<3, W, DH, kStage, kPaged>(a, stream);
-    case 4: return launch_rt<4, W, DH, kStage, kPaged>(a, stream);
-    case 5: return launch_rt<5, W, DH, kStage, kPaged>(a, stream);
-    case 6: return launch_rt<6, W, DH, kStage, kPaged>(a, stream);
+    case 1: return launch_rt<1, kSparse, kPaged>(a, stream);
+    case 2: return launch_rt<2, kSparse, kPaged>(a, stream);
+    case 3: return launch_rt<3, kSparse, kPaged>(a, stream);
+    case 4: return launch_rt<4, kSparse, kPaged>(a, stream);
+    case 5: return launch_rt<5, kSparse, kPaged>(a, stream);
+    case 6: return launch_rt<6, kSparse, kPaged>(a, stream);
     case 7:
-    case 8: return launch_rt<8, W, DH, kStage, kPaged>(a, stream);
+    case 8: return launch_rt<8, kSparse, kPaged>(a, stream);
     default: return hipErrorInvalidValue;
   }
 }
 
-hipError_t launch_verify_attn(const AttnArgs& a, int rt, int slices, bool sparse, bool paged,
-                              hipStream_t stream) {
-  const bool stage = sparse || paged;
-  hipError_t e;
-  if (slices == 2) {
-    if (paged) e = launch_kind<64, true, true>(a, rt, stream);
-    else if (stage) e = launch_kind<64, true, false>(a, rt, stream);
-    else e = launch_kind<64, false, false>(a, rt, stream);
-  } else {
-    if (paged) e = launch_kind<128, true, true>(a, rt, stream);
-    else if (stage) e = launch_kind<128, true, false>(a, rt, stream);
-    else e = launch_kind<128, false, false>(a, rt, stream);
-  }
-  if (e != hipSuccess || a.splits == 1) return e;
-  hipLaunchKernelGGL(verify_attn_combine, dim3(a.pairs), dim3(256),
-                     (size_t)a.splits * a.rows_pad * sizeof(float), stream, a);
-  return hipGetLastError();
+hipError_t launch_verify_attn(const AttnArgs& a, int rt, bool sparse, bool paged, hipStream_t stream) {
+  if (sparse) return paged ? launch_kind<true, true>(a, rt, stream) : launch_kind<true, false>(a, rt, stream);
+  return paged ? launch_kind<false, true>(a, rt, stream) : launch_kind<false, false>(a, rt, stream);
 }
 
 }  // namespace dustin

@@ -6,6 +6,8 @@
 namespace dustin {
 
 // ---- verification attention (attn.hip) ----
+constexpr int kAttnMaxSplits = 32;  // token splits per (b, g)
+
 struct AttnArgs {
   const uint16_t* q;
   int64_t q_sb, q_st, q_sh;
@@ -20,15 +22,15 @@ struct AttnArgs {
   int32_t num_kv_heads, group_size;
   int32_t pairs;        // B * num_kv_heads
   float scale_log2;
-  int32_t splits;       // token splits per (b, g)
+  int32_t splits;       // workgroups per (b, g): the most any sequence uses
+  int32_t split_steps;  // 32-token steps per split
   int32_t rows_pad;
   float* part_acc;      // [pairs, splits, rows_pad, 128]  (splits > 1 only)
   float* part_ml;       // [pairs, splits, rows_pad, 2]
+  int32_t* counters;    // [pairs], zero between calls
 };
 
-// slices: workgroups per (split, b, g), each producing 128 / slices output columns
-hipError_t launch_verify_attn(const AttnArgs& a, int rt, int slices, bool sparse, bool paged,
-                              hipStream_t stream);
+hipError_t launch_verify_attn(const AttnArgs& a, int rt, bool sparse, bool paged, hipStream_t stream);
 
 // ---- scoring-head importance (score.hip) ----
 constexpr int kScoreWaves = 4;
