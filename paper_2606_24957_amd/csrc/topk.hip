@@ -16,6 +16,12 @@
 //   3. in position order, every free key above tau and the first `remaining` equal to it
 //      are marked.
 // A final ordered pass over the bitmap writes the set in ascending position order.
+//
+// Steps 1-3 as written take five full scans of the row per tier; they remain as the
+// general path (select_tier).  The tier normally runs select_tier_fast instead: the first
+// digit over the whole row, then one pass that marks every key above the boundary digit
+// and collects the keys of that digit as candidates; the lower digits and the tie order
+// are then resolved among the candidates alone.
 #include "kernels.hpp"
 
 namespace dustin {
@@ -245,6 +251,168 @@ __device__ void select_tier(TopkSmem& s, KeyStage& ks, uint32_t need, uint32_t* 
   __syncthreads();
 }
 
+// Fast tier: two streamed passes over the row (from global memory; a row is L2-resident
+// after the first) instead of five over LDS-staged keys.
+//   A. 12-bit histogram of the top digit over the free keys -> boundary digit d1 and how
+//      many keys r1 still fit inside it;
+//   B. every free key above d1 is marked; the free keys of bin d1 are appended, unordered,
+//      to a candidate list of (key, position);
+// then the two lower digits run over the candidates only, the candidates above the exact
+// threshold tau are marked, and the ties at tau are taken in position order by ranking them
+// among themselves.  If the candidate list or the tie set is too large (heavily tied
+// rows), the rest of the tier runs through select_tier, which only ever sees what is still
+// free, so the chosen set is the same either way.
+constexpr int kMaxRankedTies = 1024;
+constexpr int kFastBatch = 8;  // 64-position groups of a wave loaded together
+
+__device__ void select_tier_fast(TopkSmem& s, KeyStage& ks, uint32_t need, uint32_t* bm, uint32_t* cand,
+                                 int cap) {
+  if (need == 0) return;
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+  const int N = ks.N;
+  const float* row = ks.row;
+  const int ngroups = (N + kWave - 1) / kWave;  // 64-position groups; wave w takes w, w + 16, ...
+
+  // Keys of this wave's groups, kFastBatch groups at a time (a row of up to kFastBatch
+  // groups per wave is loaded once for both passes).
+  const int iters = (ngroups + kTopkWaves - 1) / kTopkWaves;
+  const bool resident = iters <= kFastBatch;
+  uint32_t kb[kFastBatch];
+  auto load_batch = [&](int i0) {
+    float v[kFastBatch];
+#pragma unroll
+    for (int u = 0; u < kFastBatch; ++u) v[u] = row[min((wave + kTopkWaves * (i0 + u)) * kWave + lane, N - 1)];
+#pragma unroll
+    for (int u = 0; u < kFastBatch; ++u) kb[u] = order_key(v[u]);
+  };
+  // keys and free flags of kScanBatch groups of the batch loaded at i0 (sub-batch j0)
+  auto fetch = [&](int i0, int j0, uint32_t* key, bool* fr) {
+    uint32_t word[kScanBatch];
+#pragma unroll
+    for (int u = 0; u < kScanBatch; ++u) {
+      const int n = min((wave + kTopkWaves * (i0 + j0 + u)) * kWave + lane, N - 1);
+      word[u] = bm[n >> 5];
+    }
+#pragma unroll
+    for (int u = 0; u < kScanBatch; ++u) {
+      const int g = wave + kTopkWaves * (i0 + j0 + u);
+      const int n = g * kWave + lane;
+      key[u] = kb[j0 + u];
+      fr[u] = g < ngroups && n < N && !((word[u] >> (n & 31)) & 1u);
+    }
+  };
+  if (resident) load_batch(0);
+
+  // ---- A
+  for (int i = tid; i < kBins1; i += kTopkThreads) s.hist[i] = 0u;
+  __syncthreads();
+  for (int i0 = 0; i0 < iters; i0 += kFastBatch) {
+    if (!resident) load_batch(i0);
+#pragma unroll
+    for (int j0 = 0; j0 < kFastBatch; j0 += kScanBatch) {
+      uint32_t key[kScanBatch];
+      bool fr[kScanBatch];
+      fetch(i0, j0, key, fr);
+#pragma unroll
+      for (int u = 0; u < kScanBatch; ++u) hist_add(s.hist, key[u] >> 20, fr[u]);
+    }
+  }
+  __syncthreads();
+  find_digit(s, kBins1, need);
+  const uint32_t d1 = s.misc[0], r1 = s.misc[1];
+
+  // ---- B (each wave appends to its own slice of the candidate list)
+  const int wcap = cap / kTopkWaves;
+  uint32_t* const wlist = cand + 2 * wave * wcap;
+  uint32_t wcount = 0;  // wave-uniform
+  for (int i0 = 0; i0 < iters; i0 += kFastBatch) {
+    if (!resident) load_batch(i0);
+#pragma unroll
+    for (int j0 = 0; j0 < kFastBatch; j0 += kScanBatch) {
+    uint32_t key[kScanBatch];
+    bool fr[kScanBatch];
+    fetch(i0, j0, key, fr);
+    uint64_t take[kScanBatch];
+#pragma unroll
+    for (int u = 0; u < kScanBatch; ++u) {
+      take[u] = __ballot(fr[u] && (key[u] >> 20) > d1);
+      const bool inbin = fr[u] && (key[u] >> 20) == d1;
+      const uint64_t cm = __ballot(inbin);
+      const uint32_t at = wcount + __popcll(cm & lanemask_lt(lane));
+      if (inbin && at < (uint32_t)wcap) {
+        wlist[2 * at] = key[u];
+        wlist[2 * at + 1] = (uint32_t)((wave + kTopkWaves * (i0 + j0 + u)) * kWave + lane);
+      }
+      wcount += __popcll(cm);
+    }
+    // the two bitmap words of a group belong to the wave that owns the group
+#pragma unroll
+    for (int u = 0; u < kScanBatch; ++u) {
+      const int g = wave + kTopkWaves * (i0 + j0 + u);
+      if (g < ngroups) mark64(bm, g * kWave, N, take[u]);
+    }
+    }
+  }
+  if (lane == 0) s.wave_cnt[wave] = wcount;
+  __syncthreads();
+  bool overflow = false;
+#pragma unroll
+  for (int w = 0; w < kTopkWaves; ++w) overflow |= s.wave_cnt[w] > (uint32_t)wcap;
+  if (overflow) {
+    ks.loaded = -1;
+    select_tier(s, ks, r1, bm);
+    return;
+  }
+  // from here on every wave works through its own candidates
+
+  // ---- the lower digits among the candidates
+  uint32_t prefix = d1 << 20, pmask = 4095u << 20, remaining = r1;
+  for (int pass = 0; pass < 2; ++pass) {
+    const int sh = pass == 0 ? 10 : 0;
+    for (int i = tid; i < kBins; i += kTopkThreads) s.hist[i] = 0u;
+    __syncthreads();
+    for (uint32_t c = lane; c < wcount; c += kWave) {
+      const uint32_t key = wlist[2 * c];
+      if ((key & pmask) == prefix) atomicAdd(&s.hist[(key >> sh) & 1023u], 1u);
+    }
+    __syncthreads();
+    find_digit(s, kBins, remaining);
+    prefix |= s.misc[0] << sh;
+    pmask |= 1023u << sh;
+    remaining = s.misc[1];
+  }
+  const uint32_t tau = prefix;
+
+  // ---- candidates above tau are taken; the ties at tau are collected
+  uint32_t* const ties = s.hist;  // positions of the candidates equal to tau
+  if (tid == 0) s.misc[3] = 0u;
+  __syncthreads();
+  for (uint32_t c = lane; c < wcount; c += kWave) {
+    const uint32_t key = wlist[2 * c], n = wlist[2 * c + 1];
+    if (key > tau) {
+      atomicOr(&bm[n >> 5], 1u << (n & 31));
+    } else if (key == tau) {
+      const uint32_t at = atomicAdd(&s.misc[3], 1u);
+      if (at < (uint32_t)kMaxRankedTies) ties[at] = n;
+    }
+  }
+  __syncthreads();
+  const uint32_t nt = s.misc[3];
+  if (nt > (uint32_t)kMaxRankedTies) {  // many equal keys: the ordered full-row path
+    ks.loaded = -1;
+    select_tier(s, ks, remaining, bm);
+    return;
+  }
+  // tie t is taken iff fewer than `remaining` ties precede it in position
+  for (uint32_t t = tid; t < nt; t += kTopkThreads) {
+    const uint32_t n = ties[t];
+    uint32_t rank = 0;
+    for (uint32_t o = 0; o < nt; ++o) rank += ties[o] < n;
+    if (rank < remaining) atomicOr(&bm[n >> 5], 1u << (n & 31));
+  }
+  __syncthreads();
+}
+
 // Key-segment length for rows of up to max_len positions: the LDS left beside the
 // static state and the bitmap, a multiple of kSegQuantum, at most the row rounded up.
 static int topk_segment(int max_len) {
@@ -288,15 +456,17 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(TopkArgs a, int seg)
   const int rseg = min(seg, (N + kSegQuantum - 1) / kSegQuantum * kSegQuantum);
   KeyStage ks{nullptr, dyn, bm, N, rseg, (N + rseg - 1) / rseg, -1};
   __syncthreads();
+  // the candidate list of the fast tier uses the key-staging area: (key, position) pairs
+  const int cap = rseg / 2;
   if (a.s_draft) {
     ks.row = a.s_draft + (int64_t)b * a.d_sb + (int64_t)go * a.d_sg;
     ks.loaded = -1;
-    select_tier(s, ks, (uint32_t)m, bm);
+    select_tier_fast(s, ks, (uint32_t)m, bm, dyn, cap);
   }
   if (a.s_target) {
     ks.row = a.s_target + (int64_t)b * a.t_sb + (int64_t)go * a.t_sg;
     ks.loaded = -1;
-    select_tier(s, ks, (uint32_t)(k - m - P), bm);
+    select_tier_fast(s, ks, (uint32_t)(k - m - P), bm, dyn, cap);
   }
 
   // ascending write-out: wave w owns bitmap words [w W, (w + 1) W), one word per lane
