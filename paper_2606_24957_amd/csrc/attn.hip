@@ -103,14 +103,16 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
   constexpr int kPitch = kD + 4;   // LDS row pitch (fp32) of the merged accumulator
   constexpr int kTilesBytes = kW * 2 * kTile;                    // K and V tiles of every wave
   constexpr int kStageBytes = kStage ? kStageSteps * kStep * 4 : 0;
-  constexpr int kQBytes = kQReg ? 0 : RT * 16 * kQPitch * 2;
-  constexpr int kLoopBytes = kTilesBytes + kStageBytes + kQBytes;
+  constexpr int kLoopBytes = kTilesBytes + kStageBytes;
   constexpr int kBufFloats = RT * 16 * kPitch;                  // one wave's accumulator
-  constexpr int kNB = RT <= 4 ? kW : 2;                          // wave accumulators LDS holds
+  constexpr int kNB = RT <= 4 ? kW : (RT <= 6 ? 2 : 1);          // wave accumulators LDS holds
   constexpr int kFinalBytes = kNB * kBufFloats * 4;
   __shared__ __attribute__((aligned(1024))) char smem[kLoopBytes > kFinalBytes ? kLoopBytes : kFinalBytes];
   uint32_t* const sm_phys = reinterpret_cast<uint32_t*>(smem + kTilesBytes);
-  uint16_t* const sm_q = reinterpret_cast<uint16_t*>(smem + kTilesBytes + kStageBytes);
+  // staged queries live in an LDS object of their own: the compiler can then see that
+  // the direct-to-LDS row loads in flight never write them, and reads them without
+  // waiting for those loads
+  __shared__ __attribute__((aligned(16))) uint16_t sm_q[kQReg ? 8 : RT * 16 * kQPitch];
 
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);  // wave-uniform
@@ -142,7 +144,7 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
     return a.q + (int64_t)b * a.q_sb + (int64_t)t * a.q_st + (int64_t)(g * a.group_size + hh) * a.q_sh;
   };
   // Q^T as B operands: lane holds Q[row rt*16+lr][32 ks + 8 lg + e] (row r = t G + hh),
-  // in registers for up to 5 row tiles, else staged in LDS and read per step.
+  // in registers for up to 3 row tiles, else staged in LDS and read per step.
   bf16x8 qreg[kQReg ? RT : 1][4];
   constexpr int kQChunks = RT * 16 * (kD / 8), kQPer = (kQChunks + kW * kWave - 1) / (kW * kWave);
   u32x4 qx[kQReg ? 1 : kQPer];
@@ -296,9 +298,26 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
     issue_rows(ph);
   };
 
+  // With up to four row tiles a wave reads all of a step's operands into registers and
+  // starts the next step's loads before computing.  With more, the registers are needed
+  // for the accumulators: the wave computes first, reading V^T from its tile as it goes,
+  // and only then starts the next step (the other waves of the CU keep loads in flight).
+  constexpr bool kOverlap = RT <= 4;
   struct Operands {
-    bf16x8 k[2][4];    // K rows of the step's two 16-token tiles (MFMA A layout)
-    bf16x8 vt[NDT];    // V^T of each 16-column tile over the 32 tokens (MFMA A layout)
+    bf16x8 k[2][4];                // K rows of the step's two 16-token tiles (MFMA A layout)
+    bf16x8 vt[kOverlap ? NDT : 1];  // V^T of each 16-column tile over the 32 tokens (MFMA A layout)
+  };
+
+  // V^T operand of 16-column tile dt: lane lr of a 16-lane group addresses token
+  // 4 lg + lr / 4 (+16 for the second half of k), columns 16 dt + 4 (lr % 4) .. + 3; it
+  // receives V[token 4 lg + e (+16)][16 dt + lr]
+  auto read_vt = [&](int dt) -> bf16x8 {
+    const int j0 = 4 * lg + (lr >> 2), j1 = j0 + 16;
+    const int c = 2 * dt + ((lr >> 1) & 1);
+    const v4i16 lo = lds_read_tr16(vtile + tile_row(j0) * 256 + 8 * (lr & 1) + 16 * v_chunk(j0, c));
+    const v4i16 hi = lds_read_tr16(vtile + tile_row(j1) * 256 + 8 * (lr & 1) + 16 * v_chunk(j1, c));
+    return as_bf16x8(u32x4{__builtin_bit_cast(u32x2, lo)[0], __builtin_bit_cast(u32x2, lo)[1],
+                           __builtin_bit_cast(u32x2, hi)[0], __builtin_bit_cast(u32x2, hi)[1]});
   };
 
   // Reads the step's operands out of this wave's tiles (after its loads completed).
@@ -311,87 +330,68 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
       for (int ks = 0; ks < 4; ++ks)
         op.k[t2][ks] = as_bf16x8(*reinterpret_cast<const u32x4*>(row + 16 * k_chunk(j, 4 * ks + lg)));
     }
-    // lane lr of a 16-lane group addresses token 4 lg + lr / 4 (+16 for the second half of
-    // k), columns 16 dt + 4 (lr % 4) .. + 3; it receives V[token 4 lg + e (+16)][16 dt + lr]
-    const int j0 = 4 * lg + (lr >> 2), j1 = j0 + 16;
-    const char* r0 = vtile + tile_row(j0) * 256 + 8 * (lr & 1);
-    const char* r1 = vtile + tile_row(j1) * 256 + 8 * (lr & 1);
+    if constexpr (kOverlap)
 #pragma unroll
-    for (int dt = 0; dt < NDT; ++dt) {
-      const int c = 2 * dt + ((lr >> 1) & 1);
-      const v4i16 lo = lds_read_tr16(r0 + 16 * v_chunk(j0, c));
-      const v4i16 hi = lds_read_tr16(r1 + 16 * v_chunk(j1, c));
-      op.vt[dt] = as_bf16x8(u32x4{__builtin_bit_cast(u32x2, lo)[0], __builtin_bit_cast(u32x2, lo)[1],
-                                  __builtin_bit_cast(u32x2, hi)[0], __builtin_bit_cast(u32x2, hi)[1]});
-    }
+      for (int dt = 0; dt < NDT; ++dt) op.vt[dt] = read_vt(dt);
   };
 
-  // One 32-token step on register operands: (1) the score tiles of every 16-row tile;
-  // (2) the softmax of each (one wave-uniform decision to move the reference maxima);
-  // (3) the value product.  Scores stay in raw units until one FMA forms
-  // (s * scale * log2 e - m) inside exp2; the reference max m is in scaled units.
+  // One 32-token step on register operands, one 16-row tile at a time (its scores,
+  // probabilities and softmax decision live only while the tile is processed, which keeps
+  // five row tiles inside the register file): (1) the score tile; (2) its softmax, with
+  // one wave-uniform decision whether to move the tile's reference maxima; (3) its value
+  // product.  Scores stay in raw units until one FMA forms (s * scale * log2 e - m) inside
+  // exp2; the reference max m is in scaled units.
   auto compute = [&](int st, const Operands& op) {
     const int v0 = st * kStep;
     const bool edge = v0 + kStep - 1 >= wstart;  // wave-uniform: masking only near the window
-    // (1) S^T tiles: lane holds tokens v0 + 16 i + 4 lg + e for query row rt*16 + lr
-    f32x4 sc[RT][2];
 #pragma unroll
-    for (int rt = 0; rt < RT; ++rt)
+    for (int rt = 0; rt < RT; ++rt) {
+      // (1) S^T tile: lane holds tokens v0 + 16 i + 4 lg + e for query row rt*16 + lr
+      f32x4 sc[2];
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
         f32x4 c = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int ks = 0; ks < 4; ++ks) c = mfma16x16x32(op.k[i][ks], q_operand(rt, ks), c);
-        sc[rt][i] = c;
+        sc[i] = c;
       }
-    // (2) masked row maxima, lazy rescale, probabilities
-    float mx[RT];
-    bool grow = false;
-#pragma unroll
-    for (int rt = 0; rt < RT; ++rt) {
+      // (2) masked row maxima, lazy rescale, probabilities
       if (edge) {
 #pragma unroll
         for (int i = 0; i < 2; ++i)
 #pragma unroll
           for (int e = 0; e < 4; ++e)
-            if (v0 + 16 * i + 4 * lg + e > limit[rt]) sc[rt][i][e] = -INFINITY;
+            if (v0 + 16 * i + 4 * lg + e > limit[rt]) sc[i][e] = -INFINITY;
       }
-      const float m = fmaxf(fmaxf(fmaxf(sc[rt][0][0], sc[rt][0][1]), fmaxf(sc[rt][0][2], sc[rt][0][3])),
-                            fmaxf(fmaxf(sc[rt][1][0], sc[rt][1][1]), fmaxf(sc[rt][1][2], sc[rt][1][3])));
-      mx[rt] = max_over_lane_groups(m) * a.scale_log2;
-      grow |= mx[rt] > m_ref[rt] + kRescaleLog2;
-    }
-    if (__any(grow)) {  // wave-uniform, rare after the first step
-#pragma unroll
-      for (int rt = 0; rt < RT; ++rt) {
-        const float mn = fmaxf(m_ref[rt], mx[rt]);
+      const float m = fmaxf(fmaxf(fmaxf(sc[0][0], sc[0][1]), fmaxf(sc[0][2], sc[0][3])),
+                            fmaxf(fmaxf(sc[1][0], sc[1][1]), fmaxf(sc[1][2], sc[1][3])));
+      const float mx = max_over_lane_groups(m) * a.scale_log2;
+      if (__any(mx > m_ref[rt] + kRescaleLog2)) {  // wave-uniform, rare after the first step
+        const float mn = fmaxf(m_ref[rt], mx);
         const float alpha = m_ref[rt] == -INFINITY ? 0.f : fast_exp2(m_ref[rt] - mn);
         m_ref[rt] = mn;
         accl[rt] *= alpha;
 #pragma unroll
         for (int dt = 0; dt < NDT; ++dt) acc[rt][dt] *= alpha;
       }
-    }
-    bf16x8 pT[RT];
-#pragma unroll
-    for (int rt = 0; rt < RT; ++rt) {
       const float nmu = m_ref[rt] == -INFINITY ? 0.f : -m_ref[rt];
       float p[2][4];
 #pragma unroll
       for (int i = 0; i < 2; ++i)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) p[i][e] = fast_exp2(fmaf(sc[rt][i][e], a.scale_log2, nmu));
+        for (int e = 0; e < 4; ++e) p[i][e] = fast_exp2(fmaf(sc[i][e], a.scale_log2, nmu));
       // B operand of the PV product: k slot 8 lg + e <-> token 4 lg + e (e < 4, tile 0)
       // and token 16 + 4 lg + e - 4 (e >= 4, tile 1)
-      pT[rt] = as_bf16x8(u32x4{cvt_pk_bf16(p[0][0], p[0][1]), cvt_pk_bf16(p[0][2], p[0][3]),
-                               cvt_pk_bf16(p[1][0], p[1][1]), cvt_pk_bf16(p[1][2], p[1][3])});
-      accl[rt] = mfma16x16x32(ones, pT[rt], accl[rt]);
+      const bf16x8 pT = as_bf16x8(u32x4{cvt_pk_bf16(p[0][0], p[0][1]), cvt_pk_bf16(p[0][2], p[0][3]),
+                                        cvt_pk_bf16(p[1][0], p[1][1]), cvt_pk_bf16(p[1][2], p[1][3])});
+      accl[rt] = mfma16x16x32(ones, pT, accl[rt]);
+      // (3) O^T tiles
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt) {
+        if constexpr (kOverlap) acc[rt][dt] = mfma16x16x32(op.vt[dt], pT, acc[rt][dt]);
+        else acc[rt][dt] = mfma16x16x32(read_vt(dt), pT, acc[rt][dt]);
+      }
     }
-    // (3) O^T tiles
-#pragma unroll
-    for (int dt = 0; dt < NDT; ++dt)
-#pragma unroll
-      for (int rt = 0; rt < RT; ++rt) acc[rt][dt] = mfma16x16x32(op.vt[dt], pT[rt], acc[rt][dt]);
   };
 
   // Physical rows of this thread's tokens in chunk cs (reads sel, and the page table).
@@ -458,11 +458,19 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
       Operands op;
       read_tiles(op);
       const int next = st + kW;
-      if (next < ce) {
-        wait_lds_all();  // the tiles have been read out before the next loads overwrite them
-        issue(next);
+      if constexpr (kOverlap) {
+        if (next < ce) {
+          wait_lds_all();  // the tiles have been read out before the next loads overwrite them
+          issue(next);
+        }
+        compute(st, op);
+      } else {
+        compute(st, op);
+        if (next < ce) {
+          wait_lds_all();
+          issue(next);
+        }
       }
-      compute(st, op);
       if (next >= ce) break;
       st = next;
     }
@@ -492,28 +500,31 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
   put_stats();
   __syncthreads();  // every wave is past its token loop: the tiles are free
   if constexpr (kNB < kW) {
-    // not enough LDS for one buffer per wave: waves kNB.. fold into waves 0.. first
-    if (wave >= kNB) put_acc(bufs + (wave - kNB) * kBufFloats);
-    __syncthreads();
-    if (wave < kNB) {
-      const int p = wave + kNB;
-      const float* pb = bufs + wave * kBufFloats;
+    // not enough LDS for one buffer per wave: in rounds, waves [top - kNB, top) hand their
+    // partials to waves [top - 2 kNB, top - kNB) until only kNB waves hold one
+    for (int top = kW; top > kNB; top -= kNB) {
+      if (wave >= top - kNB && wave < top) put_acc(bufs + (wave - (top - kNB)) * kBufFloats);
+      __syncthreads();
+      if (wave >= top - 2 * kNB && wave < top - kNB) {
+        const int p = wave + kNB;
+        const float* pb = bufs + (wave - (top - 2 * kNB)) * kBufFloats;
 #pragma unroll
-      for (int rt = 0; rt < RT; ++rt) {
-        const int r = rt * 16 + lr;
-        const float mp = sm_m[p][r], lp = sm_l[p][r];
-        const float M = fmaxf(m_ref[rt], mp), Mu = M == -INFINITY ? 0.f : M;
-        const float fa = m_ref[rt] == -INFINITY ? 0.f : fast_exp2(m_ref[rt] - Mu);
-        const float fb = mp == -INFINITY ? 0.f : fast_exp2(mp - Mu);
+        for (int rt = 0; rt < RT; ++rt) {
+          const int r = rt * 16 + lr;
+          const float mp = sm_m[p][r], lp = sm_l[p][r];
+          const float M = fmaxf(m_ref[rt], mp), Mu = M == -INFINITY ? 0.f : M;
+          const float fa = m_ref[rt] == -INFINITY ? 0.f : fast_exp2(m_ref[rt] - Mu);
+          const float fb = mp == -INFINITY ? 0.f : fast_exp2(mp - Mu);
 #pragma unroll
-        for (int dt = 0; dt < NDT; ++dt)
-          acc[rt][dt] = acc[rt][dt] * fa + *reinterpret_cast<const f32x4*>(pb + r * kPitch + 16 * dt + 4 * lg) * fb;
-        accl[rt][0] = accl[rt][0] * fa + lp * fb;
-        m_ref[rt] = M;
+          for (int dt = 0; dt < NDT; ++dt)
+            acc[rt][dt] = acc[rt][dt] * fa + *reinterpret_cast<const f32x4*>(pb + r * kPitch + 16 * dt + 4 * lg) * fb;
+          accl[rt][0] = accl[rt][0] * fa + lp * fb;
+          m_ref[rt] = M;
+        }
+        put_stats();
       }
+      __syncthreads();  // the handed-over buffers have been read, the new stats written
     }
-    __syncthreads();  // the folded buffers have been read
-    if (wave < kNB) put_stats();
   }
   if (wave < kNB) put_acc(bufs + wave * kBufFloats);
   __syncthreads();
@@ -651,7 +662,7 @@ template <int RT, bool kSparse, bool kPaged>
 static hipError_t launch_rt(const AttnArgs& a, hipStream_t stream) {
   const int units = a.splits * a.pairs;
   const int blocks = (units + 7) / 8 * 8;
-  constexpr bool kQReg = RT <= 5;
+  constexpr bool kQReg = RT <= 3;
   hipLaunchKernelGGL((verify_attn_kernel<RT, kSparse, kPaged, kQReg>), dim3(blocks), dim3(kW * kWave), 0,
                      stream, a);
   return hipGetLastError();
