@@ -93,14 +93,17 @@ int attn_row_tiles(int nq_max, int group_size) {
   return rt < 1 ? 1 : rt;
 }
 
-// Token splits per (b, g): enough workgroups for one per CU (256 CUs, one workgroup of
-// four waves each), each split at least 8 steps of 32 tokens (two per wave).
+// Unit slots per (b, g): enough workgroups for one per CU (256 CUs, one workgroup of four
+// waves each), each split at least 8 steps of 32 tokens (two per wave) for the longest
+// pair.  The kernel then sizes the splits from the actual per-pair lengths, so that longer
+// pairs take more of the slots; beyond kAttnBalancePairs pairs each pair is one workgroup.
 int attn_splits(int batch, int num_kv_heads, int64_t tokens_per_pair) {
   const int64_t pairs = (int64_t)batch * num_kv_heads;
   if (pairs <= 0) return 1;
   const int64_t steps = (tokens_per_pair + 31) / 32;
   int64_t s;
   const int forced = env_int("DUSTIN_ATTN_SPLITS", 0);
+  if (pairs > kAttnBalancePairs) return 1;
   if (forced > 0) {
     s = forced;
   } else {
@@ -212,6 +215,7 @@ dustin_status run_attention(bool sparse, const void* q, int64_t q_sb, int64_t q_
   a.splits = attn_splits(B, Hkv, tokens_max);
   const int64_t steps_max = (tokens_max + 31) / 32;
   a.split_steps = (int)((steps_max + a.splits - 1) / a.splits);
+  a.min_split_steps = env_int("DUSTIN_ATTN_SPLITS", 0) > 0 ? 1 : 8;
   if (a.splits > 1) {
     const AttnWs w = attn_ws_layout(B, Hkv, a.rows_pad, a.splits);
     char* base = static_cast<char*>(ws);

@@ -85,6 +85,28 @@ __device__ __forceinline__ void lds_barrier() {
 __device__ __forceinline__ void wait_vmem_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }  // vmcnt(0)
 __device__ __forceinline__ void wait_lds_all() { __builtin_amdgcn_s_waitcnt(0xC07F); }   // lgkmcnt(0)
 
+// Inclusive prefix sum over the 64 lanes of a wave: a Hillis-Steele scan inside each row of
+// 16 lanes (DPP row shifts; lanes without a source add 0), then lane 15 of rows 0 and 2 is
+// added to rows 1 and 3 (row_bcast:15) and lane 31 to rows 2 and 3 (row_bcast:31).
+__device__ __forceinline__ int wave_inclusive_sum(int v) {
+  v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xf, 0xf, false);  // row_shr:1
+  v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xf, 0xf, false);  // row_shr:2
+  v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xf, 0xf, false);  // row_shr:4
+  v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xf, 0xf, false);  // row_shr:8
+  v += __builtin_amdgcn_update_dpp(0, v, 0x142, 0xa, 0xf, false);  // row_bcast:15
+  v += __builtin_amdgcn_update_dpp(0, v, 0x143, 0xc, 0xf, false);  // row_bcast:31
+  return v;
+}
+
+// floor(a / b) for 0 <= a < 2^22 and b >= 1: the fp32 reciprocal estimate is within one of
+// the quotient there, and one correction each way makes it exact.
+__device__ __forceinline__ int small_div(int a, int b) {
+  int q = (int)((float)a * __builtin_amdgcn_rcpf((float)b));
+  q -= q * b > a ? 1 : 0;
+  q += (q + 1) * b <= a ? 1 : 0;
+  return q;
+}
+
 // Placement of a step's rows in a wave's 8 KB tile.  Load instruction i (0..7) fills LDS
 // rows 4 i .. 4 i + 3 with tokens i, 8 + i, 16 + i, 24 + i (lanes 16 q .. 16 q + 15 move
 // token 8 q + i), so token j of the step sits in LDS row 4 (j & 7) + (j >> 3).  Within a
@@ -119,25 +141,47 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
   const int lr = lane & 15, lg = lane >> 4;
   char* const ktile = smem + wave * 2 * kTile;
   char* const vtile = ktile + kTile;
+  // Every kernel argument the prologue reads is held in SGPRs from here on: the arguments
+  // then arrive as one batch with one wait, instead of in dependent batches between the
+  // first global loads.
+  asm volatile("" ::"s"(a.q), "s"(a.q_sb), "s"(a.q_st), "s"(a.q_sh), "s"(a.idx), "s"(a.idx_sb),
+               "s"(a.idx_sg), "s"(a.count), "s"(a.dims.seq_lens), "s"(a.dims.n_query),
+               "s"(a.dims.max_len), "s"(a.dims.nq_max), "s"(a.dims.k_max), "s"(a.groups),
+               "s"(a.num_kv_heads), "s"(a.group_size), "s"(a.pairs), "s"(a.splits),
+               "s"(a.split_steps), "s"(a.min_split_steps));
+  asm volatile("" ::"s"(a.k.data), "s"(a.k.stride_b), "s"(a.k.stride_n), "s"(a.k.stride_h),
+               "s"(a.k.capacity), "s"(a.v.data), "s"(a.v.stride_b), "s"(a.v.stride_n), "s"(a.v.stride_h),
+               "s"(a.out), "s"(a.counters), "s"(a.part_acc), "s"(a.part_ml), "s"(a.rows_pad),
+               "s"(a.scale_log2));
 
-  // every XCD owns a contiguous run of (pair, split) units: the splits of a pair, and the
-  // KV heads of a sequence, share an XCD (its L2 and its address translations)
-  const int units = a.pairs * a.splits;
-  const int per_xcd = (units + 7) >> 3;
-  const int u = blockIdx.x >> 3, lin = (blockIdx.x & 7) * per_xcd + u;
-  if (u >= per_xcd || lin >= units) return;
-  const int pair = lin / a.splits, split = lin - pair * a.splits;
-  const int b = pair / a.num_kv_heads, g = pair - b * a.num_kv_heads;
+  // ---- which (pair, split) this workgroup runs.  The grid holds U = pairs * splits unit
+  // slots; XCD x (blockIdx % 8) runs units ceil(x A / 8) .. ceil((x + 1) A / 8) - 1 of the A
+  // units there are, a contiguous run, so that the splits of a pair and the KV heads of a
+  // sequence share an XCD (its L2 and its address translations).
+  const int xcd = blockIdx.x & 7, xslot = blockIdx.x >> 3;
+  const int U = a.pairs * a.splits;
+  auto unit_of = [&](int A, int& unit) {
+    unit = (xcd * A + 7) / 8 + xslot;
+    return unit < ((xcd + 1) * A + 7) / 8;
+  };
+  // With one split per pair, unit = pair.  With several, wave 0 sizes the splits from the
+  // actual per-pair token counts below.  Meanwhile the prologue loads of the uniform guess
+  // (every pair `splits` splits of split_steps steps, exact when the lengths are equal) are
+  // already in flight; they are issued again only if the guess was wrong.
+  const bool balance = a.splits > 1;  // kernel-uniform
+  int unit = 0;
+  const bool guess_ok = unit_of(U, unit);
+  int pair = guess_ok ? unit / a.splits : 0;
+  int split = unit - pair * a.splits;
+  int s_begin = split * a.split_steps;
+  int split_steps = a.split_steps, nsplit = 1, slot0 = 0;
 
   // ---- prologue: one round trip.  The per-sequence sizes, the queries and the selected
   // positions of the first chunk are loaded together; the latter two speculatively (every
   // query slot, positions below k_max), which stays in bounds whatever the sizes are.
-  const int gi = a.groups == 1 ? 0 : g;
-  const int32_t* idx_row = kSparse ? a.idx + (int64_t)b * a.idx_sb + (int64_t)gi * a.idx_sg : nullptr;
-  const int n_raw = a.dims.seq_lens[b];
-  const int t_raw = a.dims.n_query ? a.dims.n_query[b] : a.dims.nq_max;
-  const int c_raw = kSparse ? a.count[b * a.groups + gi] : 0;
-  const int s_begin = split * a.split_steps;
+  int b = 0, g = 0, gi = 0;
+  const int32_t* idx_row = nullptr;
+  int n_raw = 0, t_raw = 0, c_raw = 0;
   const int rows_mem = a.dims.nq_max * a.group_size;  // query rows present in memory
   auto q_row_ptr = [&](int r) {
     const int t = r / a.group_size, hh = r - t * a.group_size;
@@ -148,23 +192,6 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
   bf16x8 qreg[kQReg ? RT : 1][4];
   constexpr int kQChunks = RT * 16 * (kD / 8), kQPer = (kQChunks + kW * kWave - 1) / (kW * kWave);
   u32x4 qx[kQReg ? 1 : kQPer];
-  if constexpr (kQReg) {
-#pragma unroll
-    for (int rt = 0; rt < RT; ++rt) {
-      const int r = rt * 16 + lr;
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks)
-        qreg[rt][ks] = r < rows_mem ? as_bf16x8(load16(q_row_ptr(r) + 8 * lg + 32 * ks))
-                                    : as_bf16x8(u32x4{0u, 0u, 0u, 0u});
-    }
-  } else {
-#pragma unroll
-    for (int j = 0; j < kQPer; ++j) {
-      const int e = threadIdx.x + j * kW * kWave;
-      const int r = e / (kD / 8), c0 = (e % (kD / 8)) * 8;
-      qx[j] = (e < kQChunks && r < rows_mem) ? load16(q_row_ptr(r) + c0) : u32x4{0u, 0u, 0u, 0u};
-    }
-  }
   int32_t sel[kStageBatch];  // selected positions of this thread's tokens in a chunk
   auto load_selection = [&](int cs) {
 #pragma unroll
@@ -173,15 +200,186 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
       sel[j] = kSparse ? idx_row[min(v, a.dims.k_max - 1)] : 0;
     }
   };
-  if constexpr (kStage) load_selection(s_begin);
   // the positions of this lane's tokens in the wave's first step, so that its loads can
   // start before the block-wide staging pass (contiguous caches; a paged one needs the
   // staged translation)
-  const int first_v0 = (s_begin + wave) * kStep + 8 * lg;
+  int first_v0 = 0;
   int32_t first_sel[8];
-  if constexpr (kStage && !kPaged) {
+  int own_sizes = 0;  // lane 0: N_b, lane 1: T_b (if given), lane 2: the selection count
+  auto prologue_loads = [&]() {
+    b = pair / a.num_kv_heads;
+    g = pair - b * a.num_kv_heads;
+    gi = a.groups == 1 ? 0 : g;
+    idx_row = kSparse ? a.idx + (int64_t)b * a.idx_sb + (int64_t)gi * a.idx_sg : nullptr;
+    // one gather by three lanes (read back lane by lane where first needed, so that no
+    // wait for it lands among the loads below)
+    {
+      const int32_t* src = lane == 1 && a.dims.n_query ? a.dims.n_query + b
+                           : lane == 2 && kSparse ? a.count + b * a.groups + gi
+                           : a.dims.seq_lens + b;
+      own_sizes = *src;
+    }
+    if constexpr (kQReg) {
 #pragma unroll
-    for (int i = 0; i < 8; ++i) first_sel[i] = idx_row[min(first_v0 + i, a.dims.k_max - 1)];
+      for (int rt = 0; rt < RT; ++rt) {
+        const int r = rt * 16 + lr;
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks)
+          qreg[rt][ks] = r < rows_mem ? as_bf16x8(load16(q_row_ptr(r) + 8 * lg + 32 * ks))
+                                      : as_bf16x8(u32x4{0u, 0u, 0u, 0u});
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < kQPer; ++j) {
+        const int e = threadIdx.x + j * kW * kWave;
+        const int r = e / (kD / 8), c0 = (e % (kD / 8)) * 8;
+        qx[j] = (e < kQChunks && r < rows_mem) ? load16(q_row_ptr(r) + c0) : u32x4{0u, 0u, 0u, 0u};
+      }
+    }
+    if constexpr (kStage) load_selection(s_begin);
+    first_v0 = (s_begin + wave) * kStep + 8 * lg;
+    if constexpr (kStage && !kPaged) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) first_sel[i] = idx_row[min(first_v0 + i, a.dims.k_max - 1)];
+    }
+  };
+  prologue_loads();
+  // sizes of pairs 4 lane .. 4 lane + 3 (wave 0; issued with the prologue loads)
+  int pn[4], pt[4], pc[4];
+  if (balance && wave == 0) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int p = 4 * lane + j;
+      const bool ok = p < a.pairs;
+      const int pb = ok ? small_div(p, a.num_kv_heads) : 0, pg = ok ? p - pb * a.num_kv_heads : 0;
+      pn[j] = ok ? a.dims.seq_lens[pb] : 0;
+      pt[j] = ok ? (a.dims.n_query ? a.dims.n_query[pb] : a.dims.nq_max) : 0;
+      pc[j] = ok && kSparse ? a.count[pb * a.groups + (a.groups == 1 ? 0 : pg)] : 0;
+    }
+  }
+
+  // 32-token steps of a pair: its selected (or all) positions, then its window
+  auto steps_of = [&](int n, int t, int c) {
+    const int Nc = clampi(n, 0, a.dims.max_len), Tc = clampi(t, 0, a.dims.nq_max);
+    const int tot = (kSparse ? clampi(c, 0, a.dims.k_max) : Nc) + Tc;
+    return Tc == 0 ? 0 : (tot + kStep - 1) / kStep;
+  };
+  if (balance) {
+    // The smallest split size s (at least min_split_steps) whose splits fit the U slots:
+    // pair p takes ceil(steps_p / s) splits of equal size.  s = ceil(W / U) (W = total steps)
+    // fits when the lengths are equal; otherwise a binary search up to ceil(W / (U - pairs)),
+    // which always fits (sum ceil(steps_p / s) <= W / s + pairs).
+    __shared__ int sm_sched[8];
+    if (wave == 0) {
+      int st[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) st[j] = steps_of(pn[j], pt[j], pc[j]);
+      // ceil(x / s) splits of size ceil(x / k), and with that size no empty trailing split
+      auto splits_for = [](int x, int s, int& size) {
+        const int k0 = x ? small_div(x + s - 1, s) : 0;
+        size = k0 ? small_div(x + k0 - 1, k0) : 0;
+        return k0 ? small_div(x + size - 1, size) : 0;
+      };
+      const int st0 = __builtin_amdgcn_readfirstlane(st[0]);
+      bool differs = false;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) differs |= 4 * lane + j < a.pairs && st[j] != st0;
+      if (!__any(differs)) {
+        // equal lengths (the common case): every pair takes the same splits, no scan
+        int sz0;
+        const int k = splits_for(st0, max(small_div(st0 + a.splits - 1, a.splits), a.min_split_steps), sz0);
+        if (lane == 0) {
+          int my = 0;
+          sm_sched[0] = -1;
+          if (k && unit_of(a.pairs * k, my)) {
+            const int p = small_div(my, k);
+            sm_sched[0] = p;
+            sm_sched[1] = my - p * k;
+            sm_sched[2] = k;
+            sm_sched[3] = sz0;
+            sm_sched[4] = p * k;
+          }
+        }
+      } else {
+        int kk[4], sz[4], start[4];
+        int loc = 0;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) loc += st[j];
+        const int W = __builtin_amdgcn_readlane(wave_inclusive_sum(loc), 63);
+        // splits per pair for split size s, each pair's first unit, and the total
+        auto plan = [&](int s) {
+          int tot = 0;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            kk[j] = splits_for(st[j], s, sz[j]);
+            start[j] = tot;
+            tot += kk[j];
+          }
+          const int incl = wave_inclusive_sum(tot);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) start[j] += incl - tot;
+          return __builtin_amdgcn_readlane(incl, 63);
+        };
+        int s = max((W + U - 1) / U, a.min_split_steps);
+        int A = plan(s);
+        if (A > U) {
+          int lo = s + 1, hi = max(lo, (W + (U - a.pairs) - 1) / (U - a.pairs));
+          while (lo < hi) {
+            const int mid = (lo + hi) >> 1;
+            if (plan(mid) <= U) hi = mid;
+            else lo = mid + 1;
+          }
+          A = plan(lo);
+        }
+        int my = 0;
+        const bool ok = A <= U && unit_of(A, my);
+        if (lane == 0) sm_sched[0] = -1;  // no unit here (overwritten below by its owner)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          if (ok && kk[j] && my >= start[j] && my < start[j] + kk[j]) {
+            sm_sched[0] = 4 * lane + j;
+            sm_sched[1] = my - start[j];
+            sm_sched[2] = kk[j];
+            sm_sched[3] = sz[j];
+            sm_sched[4] = start[j];
+          }
+        }
+      }
+      // the owner pair's sizes, from the lane that loaded them (the pair index is read
+      // back by the same wave: its own LDS write precedes the read)
+      wait_lds_all();
+      const int p = __builtin_amdgcn_readfirstlane(sm_sched[0]);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        if (p >= 0 && 4 * lane + j == p) {
+          sm_sched[5] = pn[j];
+          sm_sched[6] = pt[j];
+          sm_sched[7] = pc[j];
+        }
+      }
+    }
+    lds_barrier();
+    // (read back as wave-uniform values, so that everything derived stays scalar)
+    const int p_new = __builtin_amdgcn_readfirstlane(sm_sched[0]);
+    const int split_new = __builtin_amdgcn_readfirstlane(sm_sched[1]);
+    nsplit = __builtin_amdgcn_readfirstlane(sm_sched[2]);
+    split_steps = __builtin_amdgcn_readfirstlane(sm_sched[3]);
+    slot0 = __builtin_amdgcn_readfirstlane(sm_sched[4]);
+    if (p_new < 0 || p_new >= a.pairs || slot0 < 0 || nsplit < 1 || slot0 + nsplit > U) return;
+    n_raw = __builtin_amdgcn_readfirstlane(sm_sched[5]);
+    t_raw = __builtin_amdgcn_readfirstlane(sm_sched[6]);
+    c_raw = __builtin_amdgcn_readfirstlane(sm_sched[7]);
+    if (p_new != pair || split_new * split_steps != s_begin) {  // the guess was wrong
+      pair = p_new;
+      s_begin = split_new * split_steps;
+      prologue_loads();
+    }
+    split = split_new;
+  } else {
+    if (!guess_ok) return;
+    n_raw = __builtin_amdgcn_readlane(own_sizes, 0);
+    t_raw = a.dims.n_query ? __builtin_amdgcn_readlane(own_sizes, 1) : a.dims.nq_max;
+    c_raw = kSparse ? __builtin_amdgcn_readlane(own_sizes, 2) : 0;
   }
 
   const int N = clampi(n_raw, 0, a.dims.max_len);
@@ -191,11 +389,8 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
   const int total = wstart + T;        // virtual tokens: selected (or all) then window
   const int rows = T * a.group_size;   // <= RT * 16 (checked on the host via nq_max)
   const int nsteps = (total + kStep - 1) / kStep;
-  // this sequence's split count: ranges of split_steps steps (the host sizes them for the
-  // longest sequence); splits past the end have nothing to do
-  const int nsplit = (nsteps + a.split_steps - 1) / a.split_steps;
-  if (split >= nsplit) return;
-  const int s_end = min(nsteps, s_begin + a.split_steps);
+  if (s_begin >= nsteps) return;
+  const int s_end = min(nsteps, s_begin + split_steps);
 
   // Rows are addressed as uniform base + 32-bit byte offset phys * stride_n (the host
   // checks that every offset fits): phys is the position (contiguous) or
@@ -580,11 +775,11 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
   // agent-scope (sc1) cache policy, so they are coherent across XCDs without cache flushes.
   constexpr int kSC1 = 16;
   auto part_rsrc = [&](int sp) {
-    return __builtin_amdgcn_make_buffer_rsrc(a.part_acc + ((int64_t)pair * a.splits + sp) * a.rows_pad * kD, 0,
+    return __builtin_amdgcn_make_buffer_rsrc(a.part_acc + (int64_t)(slot0 + sp) * a.rows_pad * kD, 0,
                                              a.rows_pad * kD * 4, 0x00020000);
   };
   auto ml_rsrc = [&](int sp) {
-    return __builtin_amdgcn_make_buffer_rsrc(a.part_ml + ((int64_t)pair * a.splits + sp) * a.rows_pad * 2, 0,
+    return __builtin_amdgcn_make_buffer_rsrc(a.part_ml + (int64_t)(slot0 + sp) * a.rows_pad * 2, 0,
                                              a.rows_pad * 2 * 4, 0x00020000);
   };
   {

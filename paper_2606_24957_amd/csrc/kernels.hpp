@@ -22,13 +22,18 @@ struct AttnArgs {
   int32_t num_kv_heads, group_size;
   int32_t pairs;        // B * num_kv_heads
   float scale_log2;
-  int32_t splits;       // workgroups per (b, g): the most any sequence uses
-  int32_t split_steps;  // 32-token steps per split
+  int32_t splits;           // unit slots per (b, g) on average: the grid holds pairs * splits
+  int32_t split_steps;      // 32-token steps per split when every pair is as long as the longest
+  int32_t min_split_steps;  // smallest split the kernel's balancing may choose
   int32_t rows_pad;
-  float* part_acc;      // [pairs, splits, rows_pad, 128]  (splits > 1 only)
-  float* part_ml;       // [pairs, splits, rows_pad, 2]
-  int32_t* counters;    // [pairs], zero between calls
+  float* part_acc;          // [pairs * splits, rows_pad, 128], by unit  (splits > 1 only)
+  float* part_ml;           // [pairs * splits, rows_pad, 2]
+  int32_t* counters;        // [pairs], zero between calls
 };
+
+// Pairs the attention kernel's split balancing handles (four per lane of one wave); with
+// more pairs there is one workgroup per pair.
+constexpr int kAttnBalancePairs = 256;
 
 hipError_t launch_verify_attn(const AttnArgs& a, int rt, bool sparse, bool paged, hipStream_t stream);
 

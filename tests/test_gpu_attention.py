@@ -158,6 +158,20 @@ def test_split_counts_agree_and_are_deterministic(splits, monkeypatch):
     assert torch.equal(dn.view(torch.int16), dn2.view(torch.int16))
 
 
+@pytest.mark.parametrize("nq,paged,splits", [((5, 9, 2), True, None), ((3, 5, 4), False, None),
+                                             ((3, 5, 4), False, 3), ((5, 9, 2), False, 7)])
+def test_ragged_lengths_share_balanced_splits(nq, paged, splits, monkeypatch):
+    """Sequences of very different lengths (and per-KV-head selection sizes) split their
+    tokens into a number of workgroups that grows with their length; every split count and
+    size must give the same rows as the oracle."""
+    if splits:
+        monkeypatch.setenv("DUSTIN_ATTN_SPLITS", str(splits))
+    s = _shape(3, [9000, 1500, 4000], list(nq), 64, 8, 1400, paged=paged,
+               name=f"ragged_balance_{nq}_{paged}_{splits}")
+    _run_sparse_case(s, G=8, seed=13, short=(1,))
+    _run_dense_case(s)
+
+
 def _sample_rows(s, n, seed):
     rng = np.random.default_rng(seed)
     rows = []
