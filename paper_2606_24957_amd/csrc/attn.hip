@@ -56,13 +56,12 @@ typedef __attribute__((address_space(3))) void lds_void;
 // gfx950 LDS transpose load: within each 16-lane group, lane i receives element i % 4 of
 // the 8 bytes addressed by group lane 4 e + i / 4, for e = 0..3.
 __device__ __forceinline__ v4i16 lds_read_tr16(const char* p) {
-  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-      (__attribute__((address_space(3))) v4i16*)(reinterpret_cast<uintptr_t>(p)));
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4i16*)(const_cast<char*>(p)));
 }
 
 // gfx950 direct-to-LDS load: lane l's 16 bytes at src land at lds + 16 l.
 __device__ __forceinline__ void load_lds16(const void* src, char* lds) {
-  __builtin_amdgcn_global_load_lds(src, (lds_void*)(reinterpret_cast<uintptr_t>(lds)), 16, 0, 0);
+  __builtin_amdgcn_global_load_lds(src, (lds_void*)(lds), 16, 0, 0);
 }
 
 __device__ __forceinline__ uint32_t cvt_pk_bf16(float lo, float hi) {
