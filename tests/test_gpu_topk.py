@@ -111,3 +111,12 @@ def test_topk_deterministic_repeat():
     a, _ = _compare(sd, st, [N] * B, k)
     b, _ = _compare(sd, st, [N] * B, k)
     assert np.array_equal(a, b)
+
+
+def test_topk_calls_of_different_shapes_in_turn():
+    """Calls of different (batch, groups, length) in turn each match the oracle."""
+    shapes = [(2, 1, 40000, 1500), (5, 4, 6000, 300), (2, 1, 40000, 1500), (1, 2, 3000, 64)]
+    for t, (B, G, N, k) in enumerate(shapes):
+        sd = _scores("uniform", B, N, 30 + t)
+        st = np.random.default_rng(40 + t).random((B, G, N)).astype(np.float32)
+        _compare(sd, st, [N - b for b in range(B)], k, groups=G)
