@@ -11,7 +11,9 @@
  *                                       every target layer with the same I (global,
  *                                       layer-invariant selection, method section 4.1)
  * and dense_verify_attn is the full-cache verification attention the paper compares
- * against (Efficiency baselines; Appendix G).
+ * against (Efficiency baselines; Appendix G).  Around the attention, dustin_kv_append
+ * writes the verification window's K and V into the caches (per layer, before step 4)
+ * and dustin_kv_commit keeps the accepted window tokens after verification.
  *
  * Conventions shared by every entry point
  *   - All tensor pointers are DEVICE pointers unless a name ends in _host.  The caller
@@ -204,6 +206,37 @@ dustin_status dense_verify_attn(const void* q, int64_t q_sb, int64_t q_st, int64
                                 const dustin_batch* bt, float scale, void* out, int64_t o_sb,
                                 int64_t o_st, int64_t o_sh, void* workspace,
                                 size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------------
+ * dustin_kv_append -- the target K and V of the verification window into the caches,
+ * before the verification attention reads them (Sec. 3.2, sparse verification workflow:
+ * the window tokens are verified against the cache, and accepted ones are appended).
+ * For every b < B, t < T_b, h < Hkv:
+ *   K[b, N_b + t, h, :] = k_new[b, t, h, :],  V[b, N_b + t, h, :] = v_new[b, t, h, :]
+ * through the page table when the caches are paged.  Positions without a page
+ * (t beyond max_pages * page_size) or past a contiguous cache's capacity are not written.
+ *   k_new, v_new  bf16 [B, nq_max, Hkv, d] (strides *_sb, *_st, *_sh in elements, inner
+ *       stride 1, 16-byte aligned rows); read only for t < T_b
+ *   k, v          the caches (as for the attention; d a multiple of 8; one page table);
+ *                 must address max_len + nq_max positions per sequence
+ *   bt            seq_lens (N_b), n_query (T_b, NULL = nq_max), max_len, nq_max
+ * Device arrays are read on the stream; nothing is read back on the host.
+ * --------------------------------------------------------------------------------- */
+dustin_status dustin_kv_append(const void* k_new, int64_t k_sb, int64_t k_st, int64_t k_sh,
+                               const void* v_new, int64_t v_sb, int64_t v_st, int64_t v_sh,
+                               const dustin_kv* k, const dustin_kv* v, const dustin_batch* bt,
+                               void* stream);
+
+/* ---------------------------------------------------------------------------------
+ * dustin_kv_commit -- after verification, keep the accepted window tokens and discard the
+ * rest (Sec. 3.2): seq_lens[b] += clamp(accepted[b], 0, T_b) for b < batch, with
+ * T_b = n_query[b] clamped to [0, nq_max] (n_query NULL: T_b = nq_max).  The rejected
+ * window rows stay in the cache beyond the new N_b, where no kernel reads them and the
+ * next step's dustin_kv_append overwrites them.
+ *   seq_lens  device int32 [batch], updated in place; accepted, n_query device int32 [batch]
+ * --------------------------------------------------------------------------------- */
+dustin_status dustin_kv_commit(int32_t* seq_lens, const int32_t* accepted, const int32_t* n_query,
+                               int32_t batch, int32_t nq_max, void* stream);
 
 #ifdef __cplusplus
 }

@@ -200,3 +200,35 @@ def overhead_ratio(hd_sel, ld_sel, gamma, ht_sel, lt_sel, hd, ld, ht, lt):
     """Appendix A estimator cost ratio."""
     return float(_load().oracle_overhead_ratio(hd_sel, ld_sel, gamma, ht_sel, lt_sel,
                                                hd, ld, ht, lt))
+
+
+# ----------------------------------------------------------------------------- KV append / commit
+# Sec. 3.2 (sparse verification workflow): the verification window's target KV sits in the
+# cache at positions [N_b, N_b + T_b) while it is verified; afterwards the accepted tokens
+# are appended (kept) and the rejected draft tokens discarded.
+
+def kv_append(cache, new, seq_lens, n_query, page_table=None):
+    """The cache after writing the window rows: for every b and t < T_b, logical position
+    N_b + t of sequence b holds new[b, t].  cache: uint16 [B, N_cap, Hkv, d] (contiguous) or
+    [P, page_size, Hkv, d] with page_table int32 [B, max_pages] (paged); new: uint16
+    [B, T_max, Hkv, d].  Positions past the capacity (or without a page) are not written.
+    Returns a new array."""
+    out = np.array(cache, copy=True)
+    for b in range(new.shape[0]):
+        for t in range(int(n_query[b])):
+            pos = int(seq_lens[b]) + t
+            if page_table is None:
+                if pos < out.shape[1]:
+                    out[b, pos] = new[b, t]
+            else:
+                ps = out.shape[1]
+                if pos // ps < page_table.shape[1]:
+                    out[int(page_table[b, pos // ps]), pos % ps] = new[b, t]
+    return out
+
+
+def kv_commit(seq_lens, accepted, n_query):
+    """N_b + clamp(accepted_b, 0, T_b): the accepted window tokens become history."""
+    seq = np.asarray(seq_lens, dtype=np.int64)
+    acc = np.clip(np.asarray(accepted, dtype=np.int64), 0, np.asarray(n_query, dtype=np.int64))
+    return (seq + acc).astype(np.int32)

@@ -27,7 +27,7 @@ OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_LAUNCH = range(5)
 
 EXPORTED = ("dustin_status_string", "dustin_version", "dustin_score_workspace", "dustin_score",
             "dustin_topk_workspace", "dustin_topk", "dustin_attn_workspace",
-            "dustin_sparse_verify_attn", "dense_verify_attn")
+            "dustin_sparse_verify_attn", "dense_verify_attn", "dustin_kv_append", "dustin_kv_commit")
 
 
 class DustinError(RuntimeError):
@@ -89,6 +89,11 @@ def lib():
         L.dense_verify_attn.restype = ctypes.c_int
         L.dense_verify_attn.argtypes = [_vp, _i64, _i64, _i64, _i32, P_KV, P_KV, P_BT,
                                         ctypes.c_float, _vp, _i64, _i64, _i64, _vp, _sz, _vp]
+        L.dustin_kv_append.restype = ctypes.c_int
+        L.dustin_kv_append.argtypes = [_vp, _i64, _i64, _i64, _vp, _i64, _i64, _i64, P_KV, P_KV,
+                                       P_BT, _vp]
+        L.dustin_kv_commit.restype = ctypes.c_int
+        L.dustin_kv_commit.argtypes = [_vp, _vp, _vp, _i32, _i32, _vp]
         _lib = L
     return _lib
 
@@ -348,3 +353,51 @@ def plan_dense_verify_attn(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, se
 def dense_verify_attn(q, k, v, seq_lens, **kw):
     """Full-cache verification attention over [0, N_b) plus the causal window."""
     return plan_dense_verify_attn(q, k, v, seq_lens, **kw)()
+
+
+# ----------------------------------------------------------------------------- KV append / commit
+
+def plan_kv_append(k_new: torch.Tensor, v_new: torch.Tensor, k: torch.Tensor, v: torch.Tensor,
+                   seq_lens, *, n_query=None, page_table: Optional[torch.Tensor] = None,
+                   max_len: Optional[int] = None, stream=None) -> Call:
+    """Prepared dustin_kv_append: k_new / v_new bf16 [B, T_max, Hkv, d] go to cache
+    positions [N_b, N_b + T_b) of k / v (contiguous [B, N_cap, Hkv, d] or paged)."""
+    _on_gpu(k_new, v_new, k, v, page_table)
+    B, nq_max = k_new.shape[0], k_new.shape[1]
+    dev = k_new.device
+    kv, vv = kv_view(k, page_table), kv_view(v, page_table)
+    if max_len is None:
+        max_len = _capacity(kv) - nq_max
+    seq = _i32_dev(seq_lens, dev)
+    nqa = _i32_dev(n_query, dev)
+    bt = _batch(B, max_len, nq_max, 0, seq, nqa)
+    args = (_ptr(k_new), k_new.stride(0), k_new.stride(1), k_new.stride(2), _ptr(v_new),
+            v_new.stride(0), v_new.stride(1), v_new.stride(2), ctypes.byref(kv), ctypes.byref(vv),
+            ctypes.byref(bt), _stream(stream))
+    return Call(lib().dustin_kv_append, args, "dustin_kv_append", (k_new, v_new, k, v, kv, vv, bt), None)
+
+
+def kv_append(k_new, v_new, k, v, seq_lens, **kw):
+    """Writes the verification window's K and V into the caches at [N_b, N_b + T_b)."""
+    return plan_kv_append(k_new, v_new, k, v, seq_lens, **kw)()
+
+
+def plan_kv_commit(seq_lens: torch.Tensor, accepted: torch.Tensor, *, n_query=None,
+                   nq_max: Optional[int] = None, stream=None) -> Call:
+    """Prepared dustin_kv_commit: seq_lens += clamp(accepted, 0, T_b), in place."""
+    _on_gpu(seq_lens, accepted, n_query)
+    for t in (seq_lens, accepted) + (() if n_query is None else (n_query,)):
+        if t.dtype != torch.int32 or not t.is_contiguous():
+            raise ValueError("seq_lens, accepted and n_query must be contiguous int32 tensors")
+    B = seq_lens.numel()
+    if nq_max is None:
+        if n_query is None:
+            raise ValueError("kv_commit needs n_query or nq_max")
+        nq_max = int(n_query.max().item())
+    args = (_ptr(seq_lens), _ptr(accepted), _ptr(n_query), int(B), int(nq_max), _stream(stream))
+    return Call(lib().dustin_kv_commit, args, "dustin_kv_commit", (seq_lens, accepted, n_query), seq_lens)
+
+
+def kv_commit(seq_lens, accepted, **kw):
+    """N_b += accepted_b (clamped to [0, T_b]); returns seq_lens."""
+    return plan_kv_commit(seq_lens, accepted, **kw)()

@@ -384,6 +384,55 @@ dustin_status dustin_topk(const float* s_draft, int64_t d_sb, int64_t d_sg,
   return e == hipSuccess ? DUSTIN_OK : DUSTIN_ERR_LAUNCH;
 }
 
+// ------------------------------------------------------------------ KV append / commit
+
+dustin_status dustin_kv_append(const void* k_new, int64_t k_sb, int64_t k_st, int64_t k_sh,
+                               const void* v_new, int64_t v_sb, int64_t v_st, int64_t v_sh,
+                               const dustin_kv* k, const dustin_kv* v, const dustin_batch* bt,
+                               void* stream) {
+  if (!batch_ok(bt) || !k_new || !v_new || !k || !v) return DUSTIN_ERR_INVALID_ARG;
+  if (bt->batch == 0 || bt->nq_max == 0) return DUSTIN_OK;
+  const int d = k->head_dim, H = k->num_kv_heads;
+  if (d <= 0 || d % 8 || v->head_dim != d || v->num_kv_heads != H || H <= 0) return DUSTIN_ERR_INVALID_ARG;
+  if (k->page_table != v->page_table) return DUSTIN_ERR_INVALID_ARG;
+  if (!rows_aligned(k_new, k_sb, k_st, k_sh) || !rows_aligned(v_new, v_sb, v_st, v_sh))
+    return DUSTIN_ERR_INVALID_ARG;
+  if (k_sb < 0 || k_st < 0 || k_sh < 0 || v_sb < 0 || v_st < 0 || v_sh < 0) return DUSTIN_ERR_INVALID_ARG;
+  KvAppendArgs a;
+  memset(&a, 0, sizeof a);
+  const int64_t need = (int64_t)bt->max_len + bt->nq_max;
+  dustin_status st = kv_of(k, d, need, &a.k);
+  if (st != DUSTIN_OK) return st;
+  st = kv_of(v, d, need, &a.v);
+  if (st != DUSTIN_OK) return st;
+  a.k_new = static_cast<const uint16_t*>(k_new);
+  a.k_sb = k_sb;
+  a.k_st = k_st;
+  a.k_sh = k_sh;
+  a.v_new = static_cast<const uint16_t*>(v_new);
+  a.v_sb = v_sb;
+  a.v_st = v_st;
+  a.v_sh = v_sh;
+  a.dims = dims_of(bt);
+  a.batch = bt->batch;
+  a.num_kv_heads = H;
+  a.head_dim = d;
+  const hipError_t e = launch_kv_append(a, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? DUSTIN_OK : DUSTIN_ERR_LAUNCH;
+}
+
+dustin_status dustin_kv_commit(int32_t* seq_lens, const int32_t* accepted, const int32_t* n_query,
+                               int32_t batch, int32_t nq_max, void* stream) {
+  if (batch < 0 || nq_max < 0) return DUSTIN_ERR_INVALID_ARG;
+  if (batch == 0) return DUSTIN_OK;
+  if (!seq_lens || !accepted || !aligned(seq_lens, 4) || !aligned(accepted, 4) ||
+      (n_query && !aligned(n_query, 4)))
+    return DUSTIN_ERR_INVALID_ARG;
+  const hipError_t e =
+      launch_kv_commit(seq_lens, accepted, n_query, nq_max, batch, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? DUSTIN_OK : DUSTIN_ERR_LAUNCH;
+}
+
 // ------------------------------------------------------------------ attention
 
 size_t dustin_attn_workspace(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,

@@ -83,4 +83,19 @@ struct TopkArgs {
 
 hipError_t launch_topk(const TopkArgs& a, int B, hipStream_t stream);
 
+// ---- verification window K/V into the caches, and the commit of accepted tokens (kv.hip) ----
+struct KvAppendArgs {
+  const uint16_t* k_new;
+  int64_t k_sb, k_st, k_sh;
+  const uint16_t* v_new;
+  int64_t v_sb, v_st, v_sh;
+  KvView k, v;   // the caches (written)
+  SeqDims dims;  // seq_lens (N_b), n_query (T_b), max_len, nq_max
+  int32_t batch, num_kv_heads, head_dim;
+};
+
+hipError_t launch_kv_append(const KvAppendArgs& a, hipStream_t stream);
+hipError_t launch_kv_commit(int32_t* seq_lens, const int32_t* accepted, const int32_t* n_query, int nq_max,
+                            int batch, hipStream_t stream);
+
 }  // namespace dustin

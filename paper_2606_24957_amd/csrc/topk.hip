@@ -513,10 +513,18 @@ hipError_t launch_topk(const TopkArgs& a, int B, hipStream_t stream) {
   if (seg < kSegQuantum) return hipErrorInvalidValue;
   const int nwords = (a.dims.max_len + 31) / 32;
   const size_t dyn = (size_t)(seg + nwords) * sizeof(uint32_t);
-  const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(topk_kernel),
-                                           hipFuncAttributeMaxDynamicSharedMemorySize,
-                                           kTopkLds - (int)sizeof(TopkSmem));
+  // the dynamic-LDS limit is raised once per device (not per launch, so that launches can
+  // be recorded in a graph after the first one)
+  static bool lds_raised[64] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= 64 || !lds_raised[dev]) {
+    e = hipFuncSetAttribute(reinterpret_cast<const void*>(topk_kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
+                            kTopkLds - (int)sizeof(TopkSmem));
+    if (e != hipSuccess) return e;
+    if (dev >= 0 && dev < 64) lds_raised[dev] = true;
+  }
   dim3 grid(a.groups, B);
   hipLaunchKernelGGL(topk_kernel, grid, dim3(kTopkThreads), dyn, stream, a, seg);
   return hipGetLastError();

@@ -1,0 +1,97 @@
+"""One verification step of long-context speculative decoding on the GPU, planned once and
+replayed: the target scoring-head score, the draft scores (accumulated over the draft
+layers), the tiered top-k, and for every target layer the window's K/V append followed by
+the sparse verification attention with the one index set (Sec. 3.2: a global, layer-invariant
+selection; accepted tokens are appended to the cache).  Every launch is a prepared libdustin
+call on one stream, so the whole step can be captured in a HIP graph and replayed.
+"""
+from typing import List, Optional
+
+import torch
+
+from . import (plan_kv_append, plan_kv_commit, plan_score, plan_sparse_verify_attn,
+               plan_topk)
+
+
+def window_kv(s, layer) -> tuple:
+    """K and V of the verification window, [B, T_max, Hkv, d] each: the rows the layer's cache
+    holds at [N_b, N_b + T_b) (what the target model's projections of the window tokens give)."""
+    kk, vv = layer.contiguous_kv(s)
+    B, T = s.B, s.t_max
+    k_new = torch.zeros((B, T, s.num_kv_heads, s.head_dim), dtype=torch.bfloat16, device=kk.device)
+    v_new = torch.zeros_like(k_new)
+    for b in range(B):
+        n, t = s.seq_lens[b], s.n_query[b]
+        k_new[b, :t] = kk[b, n:n + t]
+        v_new[b, :t] = vv[b, n:n + t]
+    return k_new, v_new
+
+
+class VerifyStep:
+    """The step's launches over fixed buffers: run() enqueues them eagerly, capture() records
+    them in a HIP graph and replay() launches the graph."""
+
+    def __init__(self, s, layers, est, device, windows: Optional[list] = None, append: bool = True):
+        self.s, self.layers, self.est, self.append = s, layers, est, append
+        i32 = lambda x: torch.tensor(list(x), dtype=torch.int32, device=device)
+        self.seq, self.nq, self.gam = i32(s.seq_lens), i32(s.n_query), i32(s.draft_gamma)
+        self.bud, self.mm = i32(s.budget), i32(s.m)
+        N = s.n_max
+        self.s_t = torch.zeros((s.B, 1, N), dtype=torch.float32, device=device)
+        self.s_d = torch.zeros((s.B, 1, N), dtype=torch.float32, device=device)
+        self.idx = torch.zeros((s.B, s.groups, s.k_max), dtype=torch.int32, device=device)
+        self.cnt = torch.zeros((s.B, s.groups), dtype=torch.int32, device=device)
+        self.outs = [torch.empty_like(l.q) for l in layers]
+        self.windows = windows if windows is not None else [window_kv(s, l) for l in layers]
+        self.graph = None
+        self.ops = self._plan()
+
+    def _plan(self) -> List:
+        """The step's operations, bound to the current stream."""
+        s, est, N = self.s, self.est, self.s.n_max
+        ops = [plan_score(est.q_target, self.layers[0].k, self.seq, s.target_heads,
+                          init=est.init_target, out=self.s_t, max_len=N,
+                          page_table=self.layers[0].page_table)]
+        if est.s_draft_given is not None:
+            given = est.s_draft_given
+            ops.append(lambda: self.s_d.copy_(given))
+        else:
+            for l in range(s.draft.layers):
+                ops.append(plan_score(est.draft_q[l], est.draft_k[l], self.seq, s.draft.heads,
+                                      n_query=self.gam, init=None if l == 0 else self.s_d,
+                                      out=self.s_d, max_len=N))
+        ops.append(plan_topk(self.s_d, self.s_t, self.seq, s.k_max, budget=self.bud, m=self.mm,
+                             n_sink=s.n_sink, n_window=s.n_window, groups=s.groups, idx=self.idx,
+                             count=self.cnt))
+        for L, o, (k_new, v_new) in zip(self.layers, self.outs, self.windows):
+            if self.append:
+                ops.append(plan_kv_append(k_new, v_new, L.k, L.v, self.seq, n_query=self.nq,
+                                          page_table=L.page_table, max_len=N))
+            ops.append(plan_sparse_verify_attn(L.q, L.k, L.v, self.idx, self.cnt, self.seq,
+                                               n_query=self.nq, page_table=L.page_table, out=o))
+        return ops
+
+    def run(self):
+        for op in self.ops:
+            op()
+
+    def capture(self):
+        """Records the step in a HIP graph (after one eager run, so that every workspace
+        exists before capture)."""
+        self.run()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            ops = self._plan()
+            for op in ops:
+                op()
+        self._graph_ops = ops  # keeps the marshalled arguments alive
+        self.graph = g
+        return g
+
+    def replay(self):
+        self.graph.replay()
+
+    def commit(self, accepted: torch.Tensor):
+        """After verification: N_b += accepted_b (clamped to [0, T_b])."""
+        plan_kv_commit(self.seq, accepted, n_query=self.nq, nq_max=self.s.t_max)()

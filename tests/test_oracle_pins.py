@@ -540,3 +540,51 @@ def test_arr_full_set_is_one_and_oracle_policy_is_upper_bound():
     assert best == pytest.approx(A.mean(0)[top].sum(), abs=1e-14)
     for _ in range(300):
         assert O.arr_window(A, rng.choice(n, k, replace=False)) <= best + 1e-15
+
+
+# ----------------------------------------------------------------------------- KV append / commit
+
+def _kv_case(rng, B=3, cap=40, H=2, d=16, T=5):
+    cache = rng.integers(0, 1 << 16, (B, cap, H, d), dtype=np.uint16)
+    new = rng.integers(0, 1 << 16, (B, T, H, d), dtype=np.uint16)
+    return cache, new
+
+
+def test_kv_append_contiguous_is_a_splice():
+    """Rows [N_b, N_b + T_b) become the window rows; every other row is unchanged (checked
+    against a splice built from slices)."""
+    rng = np.random.default_rng(1)
+    cache, new = _kv_case(rng)
+    seq, nq = [10, 0, 35], [5, 3, 5]     # the last sequence runs past the capacity (40)
+    got = O.kv_append(cache, new, seq, nq)
+    for b in range(3):
+        N, T = seq[b], nq[b]
+        keep = min(T, cache.shape[1] - N)
+        want = np.concatenate([cache[b, :N], new[b, :keep], cache[b, N + keep:]])
+        np.testing.assert_array_equal(got[b], want)
+
+
+def test_kv_append_paged_matches_contiguous_through_the_page_table():
+    rng = np.random.default_rng(2)
+    B, ps, H, d, T = 3, 8, 2, 16, 6
+    maxp = 5
+    cache, new = _kv_case(rng, B=B, cap=maxp * ps, H=H, d=d, T=T)
+    perm = rng.permutation(B * maxp).astype(np.int32)
+    pt = perm.reshape(B, maxp)
+    paged = np.zeros((B * maxp, ps, H, d), dtype=np.uint16)
+    for b in range(B):
+        for j in range(maxp):
+            paged[pt[b, j]] = cache[b, j * ps:(j + 1) * ps]
+    seq, nq = [7, 30, 16], [6, 6, 0]
+    got = O.kv_append(paged, new, seq, nq, page_table=pt)
+    want = O.kv_append(cache, new, seq, nq)
+    for b in range(B):
+        back = np.concatenate([got[pt[b, j]] for j in range(maxp)])
+        np.testing.assert_array_equal(back, want[b])
+
+
+def test_kv_commit_closed_form():
+    seq = np.array([100, 0, 7, 9], np.int32)
+    acc = np.array([3, -2, 9, 0], np.int32)
+    nq = np.array([5, 4, 6, 2], np.int32)
+    np.testing.assert_array_equal(O.kv_commit(seq, acc, nq), [103, 0, 13, 9])
