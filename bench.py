@@ -313,6 +313,42 @@ def main():
         f"{est_us:.1f} us/step (target {mean(est_t) * 1e3:.1f}, draft {mean(est_d) * 1e3:.1f}, "
         f"topk {mean(est_k) * 1e3:.1f}); {ms_per_step:.3f} ms/step wall")
 
+    # the whole step (estimation, then per layer the window append and the sparse attention)
+    # enqueued eagerly and replayed as one HIP graph, timed over K steps without events
+    # between launches
+    vstep = None
+    if args.only == "all":
+        from paper_2606_24957_amd import step as S
+        try:
+            st = S.VerifyStep(s, layers, est, dev)
+            st.run()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(args.steps):
+                st.run()
+            e1.record()
+            torch.cuda.synchronize()
+            eager_us = e0.elapsed_time(e1) * 1e3 / args.steps
+            st.capture()
+            for _ in range(args.warmup):
+                st.replay()
+            torch.cuda.synchronize()
+            e0.record()
+            for _ in range(args.steps):
+                st.replay()
+            e1.record()
+            torch.cuda.synchronize()
+            graph_us = e0.elapsed_time(e1) * 1e3 / args.steps
+            vstep = {"layers": L, "launches": len(st.ops), "eager_us": round(eager_us, 2),
+                     "graph_us": round(graph_us, 2)}
+            log(f"[bench] verify step ({len(st.ops)} launches): eager {eager_us:.1f} us, "
+                f"graph {graph_us:.1f} us")
+            del st
+        except Exception as exc:  # reported, not fatal: the per-layer figures stand
+            vstep = {"error": str(exc)[:200]}
+            log(f"[bench] verify step graph: {exc}")
+
     cpu = None
     if not args.no_cpu_baseline and args.only == "all":
         log("[bench] timing the oracle on the host cores ...")
@@ -360,6 +396,7 @@ def main():
             f"per_step_L{L}": round(L * dn_us / (est_us + L * sp_us), 3) if sp else None,
             "per_step_L80": round(80 * dn_us / (est_us + 80 * sp_us), 3) if sp else None,
         },
+        "verify_step": vstep,
         "cpu_baseline": cpu,
     }
     print(json.dumps(rec), flush=True)
