@@ -225,10 +225,8 @@ def main():
     if est.s_draft_given is not None:
         s_d.copy_(est.s_draft_given)
     else:
-        for l in range(s.draft.layers):
-            score_d.append(D.plan_score(est.draft_q[l], est.draft_k[l], seq, s.draft.heads,
-                                        n_query=gam, init=None if l == 0 else s_d, out=s_d,
-                                        max_len=N))
+        score_d.append(D.plan_score_layers(est.draft_q, est.draft_k, seq, s.draft.heads,
+                                           n_query=gam, out=s_d, max_len=N))
     sel = D.plan_topk(s_d, s_t, seq, s.k_max, budget=bud, m=mm, n_sink=s.n_sink,
                       n_window=s.n_window, groups=s.groups, idx=idx, count=cnt)
     sparse = [D.plan_sparse_verify_attn(l.q, l.k, l.v, idx, cnt, seq, n_query=nq,

@@ -134,6 +134,26 @@ dustin_status dustin_score(const void* q, int64_t q_sb, int64_t q_sj, int64_t q_
                            size_t workspace_bytes, void* stream);
 
 /* ---------------------------------------------------------------------------------
+ * dustin_score_layers -- Eq. 5 summed over n_layers scored layers in one call (the draft
+ * side: S_D sums the scoring heads of the draft model's scoring layers, Eq. 5 upper):
+ *   out = init + sum over layers l of the dustin_score sum of layer l
+ * in two launches whatever n_layers is.  The layers share every shape and stride:
+ *   q_layers_host  host array of n_layers device pointers, each laid out as q above
+ *   k_layers_host  host array of n_layers dustin_kv that differ only in `data`
+ *   1 <= n_layers <= 8; n_layers * n_heads * nq_max <= 256; batch * n_layers <= 65535
+ *   workspace  dustin_score_workspace(batch, max_len, nq_max, n_heads * n_layers) bytes
+ * Every other argument is as for dustin_score.  The sum over layers is accumulated in
+ * fp32 together with the heads' and queries' terms and rounded once at the end.
+ * --------------------------------------------------------------------------------- */
+dustin_status dustin_score_layers(int32_t n_layers, const void* const* q_layers_host, int64_t q_sb,
+                                  int64_t q_sj, int64_t q_sh, int32_t num_q_heads,
+                                  const int32_t* heads_host, int32_t n_heads,
+                                  const dustin_kv* k_layers_host, const dustin_batch* bt, float scale,
+                                  int32_t groups, const float* init, int64_t init_sb, int64_t init_sg,
+                                  float* out, int64_t out_sb, int64_t out_sg, void* workspace,
+                                  size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------------
  * dustin_topk -- tiered hybrid selection, Eq. 6 (hybrid_selection), with the protected
  * set of the experimental setup (n_sink attention sinks and an n_window recent window,
  * counted inside the budget; Appendix C).  For every (b, go):

@@ -255,21 +255,36 @@ size_t dustin_score_workspace(int32_t batch, int32_t max_len, int32_t nq_max, in
   return round_up(rows * ld * sizeof(float), kAlign) + round_up(rows * n_chunks * 2 * sizeof(float), kAlign);
 }
 
-dustin_status dustin_score(const void* q, int64_t q_sb, int64_t q_sj, int64_t q_sh,
-                           int32_t num_q_heads, const int32_t* heads_host, int32_t n_heads,
-                           const dustin_kv* k, const dustin_batch* bt, float scale,
-                           int32_t groups, const float* init, int64_t init_sb, int64_t init_sg,
-                           float* out, int64_t out_sb, int64_t out_sg, void* workspace,
-                           size_t workspace_bytes, void* stream) {
-  if (!batch_ok(bt) || !q || !k || !out || !heads_host) return DUSTIN_ERR_INVALID_ARG;
+namespace {
+
+// Eq. 5 for n_layers layers that share shapes, summed into one output.
+dustin_status run_score(int32_t n_layers, const void* const* q_layers, int64_t q_sb, int64_t q_sj,
+                        int64_t q_sh, int32_t num_q_heads, const int32_t* heads_host, int32_t n_heads,
+                        const dustin_kv* k_layers, const dustin_batch* bt, float scale, int32_t groups,
+                        const float* init, int64_t init_sb, int64_t init_sg, float* out, int64_t out_sb,
+                        int64_t out_sg, void* workspace, size_t workspace_bytes, void* stream) {
+  if (!batch_ok(bt) || !q_layers || !k_layers || !out || !heads_host) return DUSTIN_ERR_INVALID_ARG;
+  if (n_layers < 1 || n_layers > kScoreMaxLayers) return DUSTIN_ERR_UNSUPPORTED;
   if (!isfinite(scale)) return DUSTIN_ERR_INVALID_ARG;
   if (n_heads < 1 || n_heads > kScoreMaxHeads) return DUSTIN_ERR_UNSUPPORTED;
+  const dustin_kv* k = &k_layers[0];
   const int Hkv = k->num_kv_heads;
   if (num_q_heads <= 0 || Hkv <= 0 || num_q_heads % Hkv) return DUSTIN_ERR_INVALID_ARG;
   if (k->head_dim != 64 && k->head_dim != 128) return DUSTIN_ERR_UNSUPPORTED;
   if (groups != 1 && groups != Hkv) return DUSTIN_ERR_INVALID_ARG;
   if (bt->nq_max < 1 || bt->nq_max > 16) return DUSTIN_ERR_UNSUPPORTED;
-  if (!rows_aligned(q, q_sb, q_sj, q_sh)) return DUSTIN_ERR_INVALID_ARG;
+  if ((int64_t)n_layers * n_heads * bt->nq_max > kScoreMaxPairs) return DUSTIN_ERR_UNSUPPORTED;
+  for (int l = 0; l < n_layers; ++l) {
+    if (!q_layers[l] || !rows_aligned(q_layers[l], q_sb, q_sj, q_sh)) return DUSTIN_ERR_INVALID_ARG;
+    const dustin_kv* kl = &k_layers[l];
+    // the layers' caches differ only in where they start
+    if (!kl->data || kl->num_kv_heads != Hkv || kl->head_dim != k->head_dim || kl->stride_b != k->stride_b ||
+        kl->stride_n != k->stride_n || kl->stride_h != k->stride_h || kl->capacity != k->capacity ||
+        kl->page_table != k->page_table || kl->page_size != k->page_size || kl->max_pages != k->max_pages ||
+        kl->num_pages != k->num_pages || kl->stride_page != k->stride_page)
+      return DUSTIN_ERR_INVALID_ARG;
+    if (!aligned(kl->data, 16)) return DUSTIN_ERR_INVALID_ARG;
+  }
   if (!aligned(out, 4) || out_sb < 0 || out_sg < 0) return DUSTIN_ERR_INVALID_ARG;
   if (init && (!aligned(init, 4) || init_sb < 0 || init_sg < 0)) return DUSTIN_ERR_INVALID_ARG;
   const int gs = num_q_heads / Hkv;
@@ -301,11 +316,17 @@ dustin_status dustin_score(const void* q, int64_t q_sb, int64_t q_sj, int64_t q_
   if (st != DUSTIN_OK) return st;
   const int B = bt->batch;
   if (B == 0 || bt->max_len == 0) return DUSTIN_OK;
-  const size_t need_ws = dustin_score_workspace(B, bt->max_len, bt->nq_max, n_heads);
+  if ((int64_t)B * n_layers > 65535) return DUSTIN_ERR_UNSUPPORTED;
+  const size_t need_ws = dustin_score_workspace(B, bt->max_len, bt->nq_max, n_heads * n_layers);
   if (!workspace || workspace_bytes < need_ws || !aligned(workspace, kAlign))
     return DUSTIN_ERR_WORKSPACE;
 
-  a.q = static_cast<const uint16_t*>(q);
+  for (int l = 0; l < n_layers; ++l) {
+    a.q_layers[l] = static_cast<const uint16_t*>(q_layers[l]);
+    a.k_layers[l] = static_cast<const uint16_t*>(k_layers[l].data);
+  }
+  a.n_layers = n_layers;
+  a.batch = B;
   a.q_sb = q_sb;
   a.q_sj = q_sj;
   a.q_sh = q_sh;
@@ -324,12 +345,38 @@ dustin_status dustin_score(const void* q, int64_t q_sb, int64_t q_sj, int64_t q_
   a.nq_max = bt->nq_max;
   a.ld = (int64_t)round_up((size_t)bt->max_len, 64);
   a.n_chunks = (bt->max_len + kScoreChunk - 1) / kScoreChunk;
-  const size_t rows = (size_t)B * n_heads * bt->nq_max;
+  const size_t rows = (size_t)n_layers * B * n_heads * bt->nq_max;
   a.logits = static_cast<float*>(workspace);
   a.stats = reinterpret_cast<float*>(static_cast<char*>(workspace) +
                                      round_up(rows * a.ld * sizeof(float), kAlign));
   const hipError_t e = launch_score(a, B, n_used, k->head_dim, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? DUSTIN_OK : DUSTIN_ERR_LAUNCH;
+}
+
+}  // namespace
+
+dustin_status dustin_score(const void* q, int64_t q_sb, int64_t q_sj, int64_t q_sh,
+                           int32_t num_q_heads, const int32_t* heads_host, int32_t n_heads,
+                           const dustin_kv* k, const dustin_batch* bt, float scale,
+                           int32_t groups, const float* init, int64_t init_sb, int64_t init_sg,
+                           float* out, int64_t out_sb, int64_t out_sg, void* workspace,
+                           size_t workspace_bytes, void* stream) {
+  if (!q || !k) return DUSTIN_ERR_INVALID_ARG;
+  const void* qs[1] = {q};
+  return run_score(1, qs, q_sb, q_sj, q_sh, num_q_heads, heads_host, n_heads, k, bt, scale, groups, init,
+                   init_sb, init_sg, out, out_sb, out_sg, workspace, workspace_bytes, stream);
+}
+
+dustin_status dustin_score_layers(int32_t n_layers, const void* const* q_layers_host, int64_t q_sb,
+                                  int64_t q_sj, int64_t q_sh, int32_t num_q_heads,
+                                  const int32_t* heads_host, int32_t n_heads,
+                                  const dustin_kv* k_layers_host, const dustin_batch* bt, float scale,
+                                  int32_t groups, const float* init, int64_t init_sb, int64_t init_sg,
+                                  float* out, int64_t out_sb, int64_t out_sg, void* workspace,
+                                  size_t workspace_bytes, void* stream) {
+  return run_score(n_layers, q_layers_host, q_sb, q_sj, q_sh, num_q_heads, heads_host, n_heads, k_layers_host,
+                   bt, scale, groups, init, init_sb, init_sg, out, out_sb, out_sg, workspace, workspace_bytes,
+                   stream);
 }
 
 // ------------------------------------------------------------------ top-k

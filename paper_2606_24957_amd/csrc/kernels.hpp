@@ -42,11 +42,15 @@ constexpr int kScoreWaves = 4;
 constexpr int kScoreChunk = 1024;        // positions per pass-1 workgroup
 constexpr int kScoreFinishChunk = 1024;  // positions per pass-2 workgroup (4 per thread)
 constexpr int kScoreMaxHeads = 16;
+constexpr int kScoreMaxLayers = 8;
+constexpr int kScoreMaxPairs = 256;  // (layer, head, query) rows one output sums
 
 struct ScoreArgs {
-  const uint16_t* q;
+  const uint16_t* q_layers[kScoreMaxLayers];  // queries of each scored layer (same strides)
   int64_t q_sb, q_sj, q_sh;
-  KvView k;
+  KvView k;                                  // K view shared by the layers, but for its data
+  const uint16_t* k_layers[kScoreMaxLayers];
+  int32_t n_layers, batch;
   SeqDims dims;
   int32_t heads[kScoreMaxHeads];
   int32_t n_heads;
@@ -60,8 +64,8 @@ struct ScoreArgs {
   int64_t init_sb, init_sg;
   float* out;
   int64_t out_sb, out_sg;
-  float* logits;  // [B, n_heads, nq_max, ld]  scaled logits, log2 domain
-  float* stats;   // [B, n_heads, nq_max, n_chunks, 2]  (max, sum of exp2) per chunk
+  float* logits;  // [n_layers, B, n_heads, nq_max, ld]  scaled logits, log2 domain
+  float* stats;   // [n_layers, B, n_heads, nq_max, n_chunks, 2]  (max, sum of exp2) per chunk
   int64_t ld;
   int32_t nq_max, n_chunks;
 };

@@ -1,14 +1,16 @@
 // score.hip -- scoring-head importance (Eq. 5 restricted to the semantic retrieval heads).
 //
+// Several layers (the draft model's scoring layers) are scored in the same two launches:
+// their logits rows sit side by side and pass 2 sums every layer's pairs into one output.
 // Pass 1 (score_logits_kernel): one workgroup per (chunk of positions, KV head used by a
-//   scoring head, sequence).  Each K row of that KV head is read once, with the same
+//   scoring head, sequence and layer).  Each K row of that KV head is read once, with the same
 //   16-byte-per-lane MFMA A-operand loads as the attention kernel, and multiplied by
 //   every (scoring head of this KV head, query) pair at once (up to 16 pairs = one MFMA
 //   column tile).  The scaled logits (log2 domain) go to the workspace together with the
 //   chunk's running (max, sum of exp2) per pair.
 // Pass 2 (score_finish_kernel): per (chunk, output group, sequence): merge the chunk
 //   statistics of every pair into its softmax normaliser, then
-//   out[n] = init[n] + sum_pairs exp2(logit - M) / Z, pairs in (head, query) order.
+//   out[n] = init[n] + sum_pairs exp2(logit - M) / Z, pairs in (layer, head, query) order.
 #include "kernels.hpp"
 
 namespace dustin {
@@ -18,7 +20,8 @@ __global__ __launch_bounds__(kScoreWaves * kWave) void score_logits_kernel(Score
   constexpr int KS = D / 32;
   // KV heads vary fastest: workgroups that run together read the same positions of every
   // used KV head (neighbouring 256-byte pieces of the same cache rows)
-  const int ug = blockIdx.x, chunk = blockIdx.y, b = blockIdx.z;
+  const int ug = blockIdx.x, chunk = blockIdx.y;
+  const int layer = blockIdx.z / a.batch, b = blockIdx.z - layer * a.batch;
   const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
   const int lr = lane & 15, lg = lane >> 4;
   const int g = a.used_kv[ug];
@@ -34,7 +37,7 @@ __global__ __launch_bounds__(kScoreWaves * kWave) void score_logits_kernel(Score
   const bool pair_ok = lr < npairs && pair_q < nq;
   bf16x8 qb[KS];
   if (pair_ok) {
-    const uint16_t* qp = a.q + (int64_t)b * a.q_sb + (int64_t)pair_q * a.q_sj +
+    const uint16_t* qp = a.q_layers[layer] + (int64_t)b * a.q_sb + (int64_t)pair_q * a.q_sj +
                          (int64_t)a.heads[pair_slot] * a.q_sh + 8 * lg;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) qb[ks] = as_bf16x8(load16(qp + 32 * ks));
@@ -42,7 +45,10 @@ __global__ __launch_bounds__(kScoreWaves * kWave) void score_logits_kernel(Score
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) qb[ks] = as_bf16x8(u32x4{0u, 0u, 0u, 0u});
   }
-  float* lrow = a.logits + (((int64_t)b * a.n_heads + pair_slot) * a.nq_max + pair_q) * a.ld;
+  KvView kv = a.k;
+  kv.data = a.k_layers[layer];
+  const int64_t rb = (int64_t)layer * a.batch + b;  // (layer, sequence) row block
+  float* lrow = a.logits + ((rb * a.n_heads + pair_slot) * a.nq_max + pair_q) * a.ld;
 
   float m_run = -INFINITY, s_run = 0.f;
   constexpr int U = 4;  // 16-position tiles per iteration (loads issued together)
@@ -51,7 +57,7 @@ __global__ __launch_bounds__(kScoreWaves * kWave) void score_logits_kernel(Score
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int p = min(p0 + 16 * u + lr, max(N - 1, 0));
-      const uint16_t* kp = a.k.row<kPaged>(b, p, g) + 8 * lg;
+      const uint16_t* kp = kv.row<kPaged>(b, p, g) + 8 * lg;
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) kr[u][ks] = load16(kp + 32 * ks);
     }
@@ -108,7 +114,7 @@ __global__ __launch_bounds__(kScoreWaves * kWave) void score_logits_kernel(Score
     const float mu = M == -INFINITY ? 0.f : M;
     float S = 0.f;
     for (int w = 0; w < kScoreWaves; ++w) S += sm[w][lr][1] * fast_exp2(sm[w][lr][0] - mu);
-    float* st = a.stats + ((((int64_t)b * a.n_heads + pair_slot) * a.nq_max + pair_q) * a.n_chunks + chunk) * 2;
+    float* st = a.stats + (((rb * a.n_heads + pair_slot) * a.nq_max + pair_q) * a.n_chunks + chunk) * 2;
     st[0] = M;
     st[1] = S;
   }
@@ -141,15 +147,16 @@ __global__ __launch_bounds__(kFinishThreads) void score_finish_kernel(ScoreArgs 
 
   // the (head slot, query) pairs feeding output group go, in that order, with their
   // logits row, softmax max M (log2 domain) and 1 / Z
-  __shared__ int sm_row[kScoreMaxHeads * 16];
-  __shared__ float sm_M[kScoreMaxHeads * 16], sm_iz[kScoreMaxHeads * 16];
+  __shared__ int sm_row[kScoreMaxPairs];
+  __shared__ float sm_M[kScoreMaxPairs], sm_iz[kScoreMaxPairs];
   __shared__ int sm_np;
   if (tid == 0) {
     int np = 0;
-    for (int slot = 0; slot < a.n_heads; ++slot) {
-      if (a.groups != 1 && a.heads[slot] / a.group_size != go) continue;
-      for (int j = 0; j < nq; ++j) sm_row[np++] = (b * a.n_heads + slot) * a.nq_max + j;
-    }
+    for (int l = 0; l < a.n_layers; ++l)
+      for (int slot = 0; slot < a.n_heads; ++slot) {
+        if (a.groups != 1 && a.heads[slot] / a.group_size != go) continue;
+        for (int j = 0; j < nq; ++j) sm_row[np++] = ((l * a.batch + b) * a.n_heads + slot) * a.nq_max + j;
+      }
     sm_np = np;
   }
   __syncthreads();
@@ -206,7 +213,7 @@ __global__ __launch_bounds__(kFinishThreads) void score_finish_kernel(ScoreArgs 
 }
 
 hipError_t launch_score(const ScoreArgs& a, int B, int n_used_kv, int head_dim, hipStream_t stream) {
-  dim3 grid1(n_used_kv, a.n_chunks, B);
+  dim3 grid1(n_used_kv, a.n_chunks, B * a.n_layers);
   const dim3 block(kScoreWaves * kWave);
   const bool paged = a.k.page_table != nullptr;
   if (head_dim == 128) {

@@ -9,8 +9,8 @@ from typing import List, Optional
 
 import torch
 
-from . import (plan_kv_append, plan_kv_commit, plan_score, plan_sparse_verify_attn,
-               plan_topk)
+from . import (plan_kv_append, plan_kv_commit, plan_score, plan_score_layers,
+               plan_sparse_verify_attn, plan_topk)
 
 
 def window_kv(s, layer) -> tuple:
@@ -56,10 +56,8 @@ class VerifyStep:
             given = est.s_draft_given
             ops.append(lambda: self.s_d.copy_(given))
         else:
-            for l in range(s.draft.layers):
-                ops.append(plan_score(est.draft_q[l], est.draft_k[l], self.seq, s.draft.heads,
-                                      n_query=self.gam, init=None if l == 0 else self.s_d,
-                                      out=self.s_d, max_len=N))
+            ops.append(plan_score_layers(est.draft_q, est.draft_k, self.seq, s.draft.heads,
+                                         n_query=self.gam, out=self.s_d, max_len=N))
         ops.append(plan_topk(self.s_d, self.s_t, self.seq, s.k_max, budget=self.bud, m=self.mm,
                              n_sink=s.n_sink, n_window=s.n_window, groups=s.groups, idx=self.idx,
                              count=self.cnt))

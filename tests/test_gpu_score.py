@@ -91,3 +91,54 @@ def test_score_full_size_target_and_draft():
         rd = O.score(bits(E.draft_q[0][b:b + 1]), bits(E.draft_k[0][b:b + 1]), [s.seq_lens[b]],
                      [s.draft_gamma[b]], s.draft.heads, scale_of(64), num_kv_heads=2)
         check_score(host(sd)[b, 0, :s.seq_lens[b]], rd[0, 0, :s.seq_lens[b]], s.seq_lens[b], f"draft b={b}")
+
+
+@pytest.mark.parametrize("n_layers,with_init,paged", [(3, False, False), (2, True, False), (3, False, True)])
+def test_score_layers_sums_layers_in_one_call(n_layers, with_init, paged):
+    """dustin_score_layers: Eq. 5 summed over layers in two launches equals init plus the
+    oracle's per-layer scores, summed in fp64."""
+    B, N, nq, Hq, Hkv, d, heads = 3, 3000, 4, 14, 2, 64, [0, 4, 7, 11]
+    g = torch.Generator(device=DEV).manual_seed(11)
+    seq_l = [N, N - 777, 1500]
+    seq = torch.tensor(seq_l, dtype=torch.int32, device=DEV)
+    nqt = torch.tensor([nq, 2, 3], dtype=torch.int32, device=DEV)
+    qs = [torch.randn((B, nq, Hq, d), generator=g, device=DEV).to(torch.bfloat16) for _ in range(n_layers)]
+    ks = [torch.randn((B, N, Hkv, d), generator=g, device=DEV).to(torch.bfloat16) for _ in range(n_layers)]
+    pt = None
+    if paged:  # the same page table for every layer, pages permuted
+        ps, maxp = 16, (N + 15) // 16
+        perm = torch.randperm(B * maxp, generator=torch.Generator().manual_seed(5)).to(torch.int32)
+        pt = perm.reshape(B, maxp).to(DEV)
+        kp = []
+        for k in ks:
+            pages = torch.zeros((B * maxp, ps, Hkv, d), dtype=torch.bfloat16, device=DEV)
+            pages[pt.reshape(-1).long()] = torch.nn.functional.pad(k, (0, 0, 0, 0, 0, maxp * ps - N)).reshape(
+                B * maxp, ps, Hkv, d)
+            kp.append(pages)
+        kin = kp
+    else:
+        kin = ks
+    init = torch.rand((B, 1, N), generator=g, device=DEV) / N if with_init else None
+    out = torch.full((B, 1, N), -5.0, device=DEV)
+    D.score_layers(qs, kin, seq, heads, n_query=nqt, init=init, out=out, max_len=N, page_table=pt)
+    torch.cuda.synchronize()
+    ref = np.zeros((B, 1, N), dtype=np.float64) if init is None else host(init).astype(np.float64)
+    for q, k in zip(qs, ks):
+        ref += O.score(bits(q), bits(k), seq_l, nqt.cpu().tolist(), heads, scale_of(d)).astype(np.float64)
+    got = host(out)
+    for b, n in enumerate(seq_l):
+        check_score(got[b, 0, :n], ref[b, 0, :n], n, f"layers b={b}")
+        assert np.all(got[b, 0, n:] == -5.0)
+
+
+def test_score_layers_one_layer_is_dustin_score():
+    B, N, nq, Hq, Hkv, d, heads = 2, 2100, 1, 64, 8, 128, [0, 17, 34, 51]
+    g = torch.Generator(device=DEV).manual_seed(12)
+    q = torch.randn((B, nq, Hq, d), generator=g, device=DEV).to(torch.bfloat16)
+    k = torch.randn((B, N, Hkv, d), generator=g, device=DEV).to(torch.bfloat16)
+    init = torch.rand((B, 1, N), generator=g, device=DEV) / N
+    seq = torch.tensor([N, 1000], dtype=torch.int32, device=DEV)
+    a = D.score(q, k, seq, heads, init=init, max_len=N).clone()
+    b = D.score_layers([q], [k], seq, heads, init=init, max_len=N)
+    torch.cuda.synchronize()
+    assert torch.equal(a[:, :, :1000], b[:, :, :1000]) and torch.equal(a[0], b[0])
