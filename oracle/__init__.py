@@ -49,6 +49,13 @@ def _load():
         lib.oracle_arr_window.argtypes = [_ptr, _i32, _i32, _ptr, _i32]
         lib.oracle_overhead_ratio.restype = ctypes.c_double
         lib.oracle_overhead_ratio.argtypes = [_i32] * 9
+        lib.oracle_page_meta.restype = _i32
+        lib.oracle_page_meta.argtypes = [_ptr, _i64, _i64, _i64, _i32, _ptr, _i32, _i32, _i32,
+                                         _ptr, _i64, _i64, _i64]
+        lib.oracle_page_score.restype = _i32
+        lib.oracle_page_score.argtypes = [_ptr, _i64, _i64, _i64, _ptr, _i64, _i64, _i64, _i32,
+                                          _ptr, _ptr, _i32, _i32, _i32, _i32, _ptr, _i32, _i32,
+                                          ctypes.c_double, _ptr, _i64, _i64, _ptr, _i64, _i64]
         lib.oracle_max_threads.restype = _i32
         lib.oracle_set_threads.argtypes = [_i32]
         _lib = lib
@@ -116,6 +123,55 @@ def score(q, k, seq_lens, n_query, heads, scale, num_kv_heads=None, groups=1, in
                           float(scale), _p(init), ins[0], ins[1], _p(out), os_[0], os_[1])
     if rc:
         raise ValueError(f"oracle_score rejected its arguments ({rc})")
+    return out
+
+
+def page_meta(k, seq_lens, page_size, num_pages=None):
+    """Page key statistics (the Quest-style page estimator).  k: uint16 [B, N, Hkv, d].
+    Returns uint16 [B, num_pages, Hkv, 2d]: per page, the channel-wise maximum then minimum
+    of K over the page's positions below N_b; rows of pages past N_b stay zero."""
+    lib = _load()
+    B, N, Hkv, d = k.shape
+    _check_inner(k, "k")
+    seq = _i32arr(seq_lens, B)
+    if num_pages is None:
+        num_pages = (N + page_size - 1) // page_size
+    meta = np.zeros((B, num_pages, Hkv, 2 * d), dtype=np.uint16)
+    ks, ms = _st(k), _st(meta)
+    rc = lib.oracle_page_meta(_p(k), ks[0], ks[1], ks[2], B, _p(seq), Hkv, d, int(page_size),
+                              _p(meta), ms[0], ms[1], ms[2])
+    if rc:
+        raise ValueError(f"oracle_page_meta rejected its arguments ({rc})")
+    return meta
+
+
+def page_score(q, meta, seq_lens, n_query, heads, scale, page_size, groups=1, init=None,
+               out=None, length=None):
+    """Page-estimator importance: Eq. 5 over pages with each page's key bound in place of
+    q . k, broadcast to the page's positions.  q: uint16 [B, nq, Hq, d]; meta: uint16
+    [B, P, Hkv, 2d] from page_meta; init/out float32 [B, G, >= max N_b]."""
+    lib = _load()
+    B, _, Hq, d = q.shape
+    Hkv = meta.shape[2]
+    _check_inner(q, "q")
+    _check_inner(meta, "meta")
+    seq = _i32arr(seq_lens, B)
+    nqa = _i32arr(n_query, B)
+    hd = _i32arr(heads)
+    if out is None:
+        n_out = length if length is not None else max(int(seq.max(initial=0)), 1)
+        out = np.zeros((B, groups, n_out), dtype=np.float32)
+    if init is not None:
+        _check_inner(init, "init")
+    _check_inner(out, "out")
+    qs, ms, os_ = _st(q), _st(meta), _st(out)
+    ins = _st(init) if init is not None else [0, 0, 0]
+    rc = lib.oracle_page_score(_p(q), qs[0], qs[1], qs[2], _p(meta), ms[0], ms[1], ms[2], B,
+                               _p(seq), _p(nqa), Hq, Hkv, d, int(page_size), _p(hd), len(hd),
+                               groups, float(scale), _p(init), ins[0], ins[1], _p(out), os_[0],
+                               os_[1])
+    if rc:
+        raise ValueError(f"oracle_page_score rejected its arguments ({rc})")
     return out
 
 

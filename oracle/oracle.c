@@ -371,3 +371,125 @@ double oracle_overhead_ratio(int hd_sel, int ld_sel, int gamma, int ht_sel, int 
   const double den = (double)hd * ld * gamma + (double)ht * lt;
   return den > 0 ? num / den : NAN;
 }
+
+/* -------------------------------------------------------------------------------
+ * Page estimator: the query-aware page scoring of Quest, which the paper names as the
+ * estimator that shrinks the context dimension (related work; the estimation-overhead
+ * analysis, where Quest-16 is Quest with 16-position pages; Appendix A's note that it
+ * could be combined with the scoring heads).  The paper describes it only as page-level
+ * key minima and maxima that bound a page's relevance in one computation; the steps
+ * below are that description written out, with these readings:
+ *   - pages are the aligned spans [p * page_size, (p + 1) * page_size) of the committed
+ *     positions [0, N_b); the last page holds only its positions below N_b;
+ *   - a page's relevance to a query is the largest value q . k can take over keys whose
+ *     every channel lies between the page's minimum and maximum of that channel:
+ *       u = sum_c max(q_c * max_c, q_c * min_c);
+ *   - several heads and queries are combined as Eq. 5 combines them: a softmax over the
+ *     pages per (head, query), summed; every position of a page carries its page's sum.
+ * ------------------------------------------------------------------------------- */
+
+/* meta[b, p, g, 0:d] = channel-wise maximum and meta[b, p, g, d:2d] = minimum of
+ * K[b, n, g, :] over the positions n of page p (bf16 patterns of the chosen keys; of
+ * equal values, the earliest position's pattern, which decides only the sign of a zero).
+ * Pages p < ceil(N_b / page_size) are written, others are not.
+ *   k    : bf16 [B, >= N_b, num_kv_heads, head_dim]     strides k_sb, k_sn, k_sh
+ *   meta : bf16 [B, >= pages, num_kv_heads, 2 * head_dim] strides m_sb, m_sp, m_sh */
+int oracle_page_meta(const uint16_t* k, int64_t k_sb, int64_t k_sn, int64_t k_sh, int B,
+                     const int32_t* seq_lens, int num_kv_heads, int head_dim, int page_size,
+                     uint16_t* meta, int64_t m_sb, int64_t m_sp, int64_t m_sh) {
+  if (!k || !seq_lens || !meta || B < 0 || num_kv_heads <= 0 || head_dim <= 0 || page_size <= 0)
+    return -1;
+#pragma omp parallel for collapse(2) schedule(dynamic)
+  for (int b = 0; b < B; ++b) {
+    for (int g = 0; g < num_kv_heads; ++g) {
+      const int N = seq_lens[b];
+      const int pages = N > 0 ? (N + page_size - 1) / page_size : 0;
+      for (int p = 0; p < pages; ++p) {
+        const int n0 = p * page_size;
+        const int n1 = n0 + page_size < N ? n0 + page_size : N;
+        uint16_t* row = meta + b * m_sb + (int64_t)p * m_sp + g * m_sh;
+        for (int c = 0; c < head_dim; ++c) {
+          uint16_t hi = k[b * k_sb + (int64_t)n0 * k_sn + g * k_sh + c], lo = hi;
+          for (int n = n0 + 1; n < n1; ++n) {
+            const uint16_t x = k[b * k_sb + (int64_t)n * k_sn + g * k_sh + c];
+            if (oracle_bf16_to_double(x) > oracle_bf16_to_double(hi)) hi = x;
+            if (oracle_bf16_to_double(x) < oracle_bf16_to_double(lo)) lo = x;
+          }
+          row[c] = hi;
+          row[head_dim + c] = lo;
+        }
+      }
+    }
+  }
+  return 0;
+}
+
+/* out[b, go, n] = init[b, go, n] + sum_{h in H(go)} sum_{j < nq_b}
+ *                 softmax_{p < P_b}(scale * sum_c max(q_c * max_{p,c}, q_c * min_{p,c}))[n / page_size]
+ * for n < N_b, P_b = ceil(N_b / page_size), with H(go) as in oracle_score.  One fp32
+ * rounding at the end; positions n >= N_b are not written.
+ *   q    : bf16 [B, nq_max, num_q_heads, head_dim]   strides q_sb, q_sj, q_sh
+ *   meta : as written by oracle_page_meta            strides m_sb, m_sp, m_sh */
+int oracle_page_score(const uint16_t* q, int64_t q_sb, int64_t q_sj, int64_t q_sh,
+                      const uint16_t* meta, int64_t m_sb, int64_t m_sp, int64_t m_sh, int B,
+                      const int32_t* seq_lens, const int32_t* n_query, int num_q_heads,
+                      int num_kv_heads, int head_dim, int page_size, const int32_t* heads,
+                      int n_heads, int groups, double scale, const float* init, int64_t init_sb,
+                      int64_t init_sg, float* out, int64_t out_sb, int64_t out_sg) {
+  if (!q || !meta || !seq_lens || !n_query || !out || (n_heads > 0 && !heads)) return -1;
+  if (B < 0 || num_q_heads <= 0 || num_kv_heads <= 0 || head_dim <= 0 || page_size <= 0) return -1;
+  if (num_q_heads % num_kv_heads) return -2;
+  if (groups != 1 && groups != num_kv_heads) return -3;
+  for (int i = 0; i < n_heads; ++i)
+    if (heads[i] < 0 || heads[i] >= num_q_heads) return -4;
+  const int group_size = num_q_heads / num_kv_heads;
+  int rc = 0;
+#pragma omp parallel for collapse(2) schedule(dynamic)
+  for (int b = 0; b < B; ++b) {
+    for (int go = 0; go < groups; ++go) {
+      const int N = seq_lens[b];
+      const int nq = n_query[b];
+      if (N <= 0) continue;
+      const int P = (N + page_size - 1) / page_size;
+      double* acc = (double*)calloc((size_t)P, sizeof(double));
+      double* u = (double*)malloc((size_t)P * sizeof(double));
+      if (!acc || !u) {
+        free(acc);
+        free(u);
+#pragma omp atomic write
+        rc = -9;
+        continue;
+      }
+      for (int hi = 0; hi < n_heads; ++hi) {
+        const int h = heads[hi];
+        const int g = h / group_size;
+        if (groups != 1 && g != go) continue;
+        for (int j = 0; j < nq; ++j) {
+          const uint16_t* qv = q + b * q_sb + j * q_sj + h * q_sh;
+          double mx = -INFINITY;
+          for (int p = 0; p < P; ++p) {
+            const uint16_t* row = meta + b * m_sb + (int64_t)p * m_sp + g * m_sh;
+            double bound = 0.0;
+            for (int c = 0; c < head_dim; ++c) {
+              const double qc = oracle_bf16_to_double(qv[c]);
+              const double a = qc * oracle_bf16_to_double(row[c]);
+              const double z = qc * oracle_bf16_to_double(row[head_dim + c]);
+              bound += a > z ? a : z;
+            }
+            u[p] = scale * bound;
+            if (u[p] > mx) mx = u[p];
+          }
+          double zsum = 0.0;
+          for (int p = 0; p < P; ++p) zsum += exp(u[p] - mx);
+          for (int p = 0; p < P; ++p) acc[p] += exp(u[p] - mx) / zsum;
+        }
+      }
+      float* o = out + b * out_sb + go * out_sg;
+      const float* in = init ? init + b * init_sb + go * init_sg : NULL;
+      for (int n = 0; n < N; ++n) o[n] = (float)((in ? (double)in[n] : 0.0) + acc[n / page_size]);
+      free(acc);
+      free(u);
+    }
+  }
+  return rc;
+}

@@ -588,3 +588,102 @@ def test_kv_commit_closed_form():
     acc = np.array([3, -2, 9, 0], np.int32)
     nq = np.array([5, 4, 6, 2], np.int32)
     np.testing.assert_array_equal(O.kv_commit(seq, acc, nq), [103, 0, 13, 9])
+
+
+# ----------------------------------------------------------------------------- page estimator
+
+def test_page_meta_is_library_min_max_over_valid_positions():
+    """Channel-wise max and min of K per page over positions < N_b, checked against numpy's
+    max/min on the reshaped valid prefix; positions >= N_b hold huge values that must not leak."""
+    rng = np.random.default_rng(40)
+    B, N, Hkv, d, ps = 3, 70, 2, 8, 16
+    kf = rng.standard_normal((B, N, Hkv, d))
+    seq = [70, 33, 16]
+    for b, n in enumerate(seq):
+        kf[b, n:] = 1e30 * np.sign(rng.standard_normal((N - n, Hkv, d)))
+    k = bits(kf)
+    meta = O.page_meta(k, seq, ps)
+    kv = val(k)
+    for b, n in enumerate(seq):
+        P = -(-n // ps)
+        for p in range(P):
+            blk = kv[b, p * ps:min(n, (p + 1) * ps)]
+            np.testing.assert_array_equal(val(meta[b, p, :, :d]), blk.max(axis=0))
+            np.testing.assert_array_equal(val(meta[b, p, :, d:]), blk.min(axis=0))
+        assert not meta[b, P:].any()
+
+
+def test_page_meta_earliest_pattern_of_equal_values():
+    """-0 and +0 compare equal: the earliest position's pattern is kept, for max and min."""
+    k = np.array([0x8000, 0x0000, 0x0000, 0x8000], dtype=np.uint16).reshape(1, 4, 1, 1)
+    meta = O.page_meta(k, [4], 2)
+    assert meta[0, 0, 0].tolist() == [0x8000, 0x8000] and meta[0, 1, 0].tolist() == [0x0000, 0x0000]
+
+
+def test_page_score_hand_worked_example():
+    """d = 2, page size 2, N = 3.  Page 0 holds keys (1, -2) and (3, 0.5): max (3, 0.5),
+    min (1, -2).  For q = (1, -1): u0 = max(3, 1) + max(-0.5, 2) = 5.  Page 1 holds (-1, 1)
+    alone: u1 = q . k = -2.  Softmax over the two pages at scale 1."""
+    q = bits(np.array([1, -1], dtype=np.float64).reshape(1, 1, 1, 2))
+    k = bits(np.array([[1, -2], [3, 0.5], [-1, 1]], dtype=np.float64).reshape(1, 3, 1, 2))
+    meta = O.page_meta(k, [3], 2)
+    s = O.page_score(q, meta, [3], [1], [0], 1.0, 2)[0, 0]
+    p0 = 1 / (1 + math.exp(-2 - 5))
+    assert s.tolist() == [np.float32(p0), np.float32(p0), np.float32(1 - p0)]
+
+
+def test_page_score_page_size_one_is_eq5():
+    """With one position per page min = max = K, the bound is q . k, and the page score is
+    Eq. 5 itself: bit-identical to oracle.score (same fp64 sums, one rounding)."""
+    rng = np.random.default_rng(41)
+    B, nq, Hq, Hkv, d, N = 2, 3, 8, 2, 32, 45
+    q = rand_bits(rng, (B, nq, Hq, d))
+    k = rand_bits(rng, (B, N, Hkv, d))
+    init = rng.random((B, Hkv, N)).astype(np.float32)
+    seq, nqs, heads = [45, 20], [3, 2], [1, 4, 6]
+    want = O.score(q, k, seq, nqs, heads, 0.2, groups=Hkv, init=init.copy())
+    got = O.page_score(q, O.page_meta(k, seq, 1), seq, nqs, heads, 0.2, 1, groups=Hkv,
+                       init=init.copy(), length=N)
+    for b, n in enumerate(seq):
+        np.testing.assert_array_equal(got[b, :, :n], want[b, :, :n])
+
+
+def test_page_bound_dominates_every_key_of_its_page():
+    """The page bound is an upper bound: q . k_n <= u(page of n) for every position, by
+    brute force over the keys, with equality for a page whose keys are all equal."""
+    rng = np.random.default_rng(42)
+    N, d, ps = 64, 16, 8
+    q = rand_bits(rng, (1, 1, 1, d))
+    kf = rng.standard_normal((1, N, 1, d))
+    kf[0, 8:16] = kf[0, 8]  # page 1: eight equal keys
+    k = bits(kf)
+    meta = O.page_meta(k, [N], ps)
+    qv, kv, mv = val(q)[0, 0, 0], val(k)[0, :, 0], val(meta)[0, :, 0]
+    u = np.array([np.maximum(qv * mv[p, :d], qv * mv[p, d:]).sum() for p in range(N // ps)])
+    assert np.all(kv @ qv <= u[np.arange(N) // ps] + 1e-12)
+    assert u[1] == pytest.approx(kv[8] @ qv, abs=1e-12)
+    # the page scores are the softmax of u: log-ratios are differences of u
+    s = O.page_score(q, meta, [N], [1], [0], 1.0, ps)[0, 0].astype(np.float64)
+    assert math.log(s[0] / s[ps * 5]) == pytest.approx(u[0] - u[5], abs=1e-6)
+
+
+def test_page_score_row_sum_and_broadcast():
+    """Every position of a page carries the page's value; summing one position per page
+    gives nq * |H(go)| per output group; positions past N_b are not written."""
+    rng = np.random.default_rng(43)
+    B, nq, Hq, Hkv, d, N, ps = 2, 2, 4, 2, 16, 50, 8
+    q = rand_bits(rng, (B, nq, Hq, d))
+    k = rand_bits(rng, (B, N, Hkv, d))
+    seq = [50, 9]
+    meta = O.page_meta(k, seq, ps)
+    out = np.full((B, Hkv, N), -7.0, dtype=np.float32)
+    O.page_score(q, meta, seq, [nq, 1], [0, 1, 3], 0.3, ps, groups=Hkv, out=out)
+    for b, n in enumerate(seq):
+        P = -(-n // ps)
+        for go, nh in enumerate([2, 1]):  # heads 0, 1 read KV head 0; head 3 reads KV head 1
+            row = out[b, go, :n].reshape(-1)
+            for p in range(P):
+                assert np.all(row[p * ps:min(n, (p + 1) * ps)] == row[p * ps])
+            tot = sum(float(row[p * ps]) for p in range(P))
+            assert tot == pytest.approx([nq, 1][b] * nh, abs=1e-5)
+            assert np.all(out[b, go, n:] == -7.0)
