@@ -14,6 +14,10 @@
  * against (Efficiency baselines; Appendix G).  Around the attention, dustin_kv_append
  * writes the verification window's K and V into the caches (per layer, before step 4)
  * and dustin_kv_commit keeps the accepted window tokens after verification.
+ * dustin_page_meta and dustin_page_score are the page estimator the paper compares its
+ * scoring heads with (page-level key minima and maxima; Quest-16 in the estimation
+ * overhead analysis): they produce an importance array that step 3 takes in place of,
+ * or on top of, S_T.
  *
  * Conventions shared by every entry point
  *   - All tensor pointers are DEVICE pointers unless a name ends in _host.  The caller
@@ -116,7 +120,8 @@ int32_t dustin_version(void);
  * last generated token (nq_b = 1, init = the historical score or NULL) and once per draft
  * scoring layer (nq_b = Gamma_b draft tokens; chaining init = out accumulates layers).
  *   q        bf16 [B, nq_max, num_q_heads, head_dim], strides q_sb, q_sj, q_sh
- *   heads_host  host int32 [n_heads], 1 <= n_heads <= 16, distinct, in [0, num_q_heads)
+ *   heads_host  host int32 [n_heads], 1 <= n_heads <= 64, distinct, in [0, num_q_heads);
+ *               the (head, query) pairs, split by KV head into tiles of 16, fit 64 tiles
  *   k        the layer's K cache; head_dim in {64, 128}
  *   bt       seq_lens, n_query (1 <= nq_max <= 16), max_len
  *   groups   1 or k->num_kv_heads
@@ -140,7 +145,7 @@ dustin_status dustin_score(const void* q, int64_t q_sb, int64_t q_sj, int64_t q_
  * in two launches whatever n_layers is.  The layers share every shape and stride:
  *   q_layers_host  host array of n_layers device pointers, each laid out as q above
  *   k_layers_host  host array of n_layers dustin_kv that differ only in `data`
- *   1 <= n_layers <= 8; n_layers * n_heads * nq_max <= 256; batch * n_layers <= 65535
+ *   1 <= n_layers <= 8; n_layers * n_heads * nq_max <= 1024; batch * n_layers <= 65535
  *   workspace  dustin_score_workspace(batch, max_len, nq_max, n_heads * n_layers) bytes
  * Every other argument is as for dustin_score.  The sum over layers is accumulated in
  * fp32 together with the heads' and queries' terms and rounded once at the end.
@@ -152,6 +157,64 @@ dustin_status dustin_score_layers(int32_t n_layers, const void* const* q_layers_
                                   int32_t groups, const float* init, int64_t init_sb, int64_t init_sg,
                                   float* out, int64_t out_sb, int64_t out_sg, void* workspace,
                                   size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------------
+ * dustin_page_meta -- page statistics of the page estimator.  The paper describes it
+ * (related work; estimation overhead analysis; Appendix A's note on shrinking the
+ * context dimension) as page-level minima and maxima of the keys that bound a page's
+ * relevance in one computation.  For every sequence b, KV head g and page
+ * p < ceil(N_b / page_size) that holds a position >= from_b:
+ *   meta[b, p, g, 0:d]  = max over n in page p, n < N_b, of K[b, n, g, :]   (per channel)
+ *   meta[b, p, g, d:2d] = min over the same positions
+ * bf16 values of K, exact (of equal values the earliest position's, which decides only the
+ * sign of a zero).  Pages are [p * page_size, (p + 1) * page_size); the last one holds
+ * its positions below N_b only.  Other pages are not written.
+ *   k          the layer's K cache (contiguous or paged); head_dim in {64, 128}
+ *   bt         seq_lens (N_b), max_len; the other fields are not read
+ *   from       device int32 [B]: first position whose page is rebuilt (clamped to
+ *              [0, N_b]); NULL = 0 (build every page)
+ *   max_span   host bound of N_b - from_b (of N_b when from is NULL), 0 <= max_span <=
+ *              max_len; pages past from_b + max_span are not rebuilt.  After an append of
+ *              T_b tokens, from = the old N_b and max_span = the largest T_b.
+ *   page_size  a power of two, 1 ... 4096
+ *   meta       bf16 [B, meta_pages, num_kv_heads, 2 * head_dim], strides meta_sb
+ *              (sequences) and meta_sp (pages) in elements; meta_sp >= num_kv_heads * 2 *
+ *              head_dim; meta_pages >= ceil(max_len / page_size)
+ * Errors: DUSTIN_ERR_INVALID_ARG for a bad pointer, size, stride or page size;
+ * DUSTIN_ERR_UNSUPPORTED for another head_dim or batch > 65535.
+ * --------------------------------------------------------------------------------- */
+dustin_status dustin_page_meta(const dustin_kv* k, const dustin_batch* bt, const int32_t* from, int32_t max_span,
+                               int32_t page_size, void* meta, int64_t meta_sb, int64_t meta_sp,
+                               int32_t meta_pages, void* stream);
+
+/* ---------------------------------------------------------------------------------
+ * dustin_page_score -- page-estimator importance: Eq. 5's sum of softmaxes, taken over
+ * pages with each page's bound on q . k in place of q . k, and given to every position of
+ * the page.  With P_b = ceil(N_b / page_size) and u = sum_c max(q_c max_{p,c}, q_c min_{p,c})
+ * (the largest q . k over keys inside the page's channel ranges):
+ *   out[b, go, n] = init[b, go, n] + sum_{h in heads of go} sum_{j < nq_b}
+ *                   softmax_{p < P_b}(scale * u(q[b, j, h], page p of KV head g(h)))[n / page_size]
+ * for n < N_b; positions n >= N_b are not written.  "heads of go" is every head when
+ * groups == 1, else those whose KV head is go.  With page_size 1 this is dustin_score.
+ * Quest's all-heads estimator passes every query head; combined with the scoring heads,
+ * heads_host holds those only.
+ *   q, heads_host, bt (seq_lens, n_query, nq_max <= 16, max_len), scale, groups, init,
+ *   out           as for dustin_score; n_heads * nq_max <= 1024
+ *   meta, meta_sb, meta_sp, meta_pages   as written by dustin_page_meta with this
+ *                 page_size, num_kv_heads and head_dim (64 or 128)
+ *   workspace     dustin_page_score_workspace(batch, max_len, page_size, nq_max, n_heads)
+ *                 bytes, 256-byte aligned
+ * Rounding: the bound's products are exact in fp32 (bf16 times bf16) and summed in fp32;
+ * fp32 exp and sums, as dustin_score.
+ * --------------------------------------------------------------------------------- */
+size_t dustin_page_score_workspace(int32_t batch, int32_t max_len, int32_t page_size, int32_t nq_max,
+                                   int32_t n_heads);
+dustin_status dustin_page_score(const void* q, int64_t q_sb, int64_t q_sj, int64_t q_sh, int32_t num_q_heads,
+                                const int32_t* heads_host, int32_t n_heads, const void* meta, int64_t meta_sb,
+                                int64_t meta_sp, int32_t meta_pages, int32_t num_kv_heads, int32_t head_dim,
+                                int32_t page_size, const dustin_batch* bt, float scale, int32_t groups,
+                                const float* init, int64_t init_sb, int64_t init_sg, float* out, int64_t out_sb,
+                                int64_t out_sg, void* workspace, size_t workspace_bytes, void* stream);
 
 /* ---------------------------------------------------------------------------------
  * dustin_topk -- tiered hybrid selection, Eq. 6 (hybrid_selection), with the protected

@@ -28,7 +28,8 @@ OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_LAUNCH = range(5)
 EXPORTED = ("dustin_status_string", "dustin_version", "dustin_score_workspace", "dustin_score",
             "dustin_topk_workspace", "dustin_topk", "dustin_attn_workspace",
             "dustin_sparse_verify_attn", "dense_verify_attn", "dustin_kv_append", "dustin_kv_commit",
-            "dustin_score_layers")
+            "dustin_score_layers", "dustin_page_meta", "dustin_page_score_workspace",
+            "dustin_page_score")
 
 
 class DustinError(RuntimeError):
@@ -97,6 +98,14 @@ def lib():
         L.dustin_kv_append.restype = ctypes.c_int
         L.dustin_kv_append.argtypes = [_vp, _i64, _i64, _i64, _vp, _i64, _i64, _i64, P_KV, P_KV,
                                        P_BT, _vp]
+        L.dustin_page_meta.restype = ctypes.c_int
+        L.dustin_page_meta.argtypes = [P_KV, P_BT, _vp, _i32, _i32, _vp, _i64, _i64, _i32, _vp]
+        L.dustin_page_score_workspace.restype = _sz
+        L.dustin_page_score_workspace.argtypes = [_i32, _i32, _i32, _i32, _i32]
+        L.dustin_page_score.restype = ctypes.c_int
+        L.dustin_page_score.argtypes = [_vp, _i64, _i64, _i64, _i32, _vp, _i32, _vp, _i64, _i64, _i32,
+                                        _i32, _i32, _i32, P_BT, ctypes.c_float, _i32, _vp, _i64, _i64,
+                                        _vp, _i64, _i64, _vp, _sz, _vp]
         L.dustin_kv_commit.restype = ctypes.c_int
         L.dustin_kv_commit.argtypes = [_vp, _vp, _vp, _i32, _i32, _vp]
         _lib = L
@@ -287,6 +296,83 @@ def plan_score_layers(qs: Sequence[torch.Tensor], ks: Sequence[torch.Tensor], se
 def score_layers(qs, ks, seq_lens, heads, **kw):
     """Eq. 5 summed over layers; returns out (positions >= N_b untouched)."""
     return plan_score_layers(qs, ks, seq_lens, heads, **kw)()
+
+
+# ----------------------------------------------------------------------------- page estimator
+
+def page_meta_empty(B: int, max_len: int, num_kv_heads: int, head_dim: int, page_size: int,
+                    device) -> torch.Tensor:
+    """A zeroed page-statistics array bf16 [B, ceil(max_len / page_size), Hkv, 2 d]."""
+    P = (int(max_len) + page_size - 1) // page_size
+    return torch.zeros((B, P, num_kv_heads, 2 * head_dim), dtype=torch.bfloat16, device=device)
+
+
+def plan_page_meta(k: torch.Tensor, seq_lens, page_size: int, meta: torch.Tensor, *,
+                   from_=None, max_span: Optional[int] = None, max_len: Optional[int] = None,
+                   page_table: Optional[torch.Tensor] = None, stream=None) -> Call:
+    """Prepared dustin_page_meta: per page of page_size positions and KV head, the channel
+    max then min of K over the page's positions < N_b, into meta bf16 [B, P, Hkv, 2d].
+    from_ (int32 [B]) limits the rebuild to pages holding a position >= from_b, with
+    max_span bounding N_b - from_b (after an append: the old lengths and the largest T_b)."""
+    _on_gpu(k, meta, page_table)
+    dev = k.device
+    seq = _i32_dev(seq_lens, dev)
+    frm = _i32_dev(from_, dev)
+    kv = kv_view(k, page_table)
+    max_len = _capacity(kv) if max_len is None else int(max_len)
+    max_span = max_len if max_span is None else int(max_span)
+    if meta.dtype != torch.bfloat16 or meta.dim() != 4 or meta.stride(3) != 1 or meta.stride(2) != meta.shape[3]:
+        raise ValueError("meta must be bf16 [B, pages, Hkv, 2d] with contiguous (Hkv, 2d) rows")
+    bt = _batch(seq.shape[0], max_len, 0, 0, seq)
+    args = (ctypes.byref(kv), ctypes.byref(bt), _ptr(frm), max_span, int(page_size), _ptr(meta),
+            meta.stride(0), meta.stride(1), meta.shape[1], _stream(stream))
+    return Call(lib().dustin_page_meta, args, "dustin_page_meta", (k, meta, kv, bt, frm), meta)
+
+
+def page_meta(k, seq_lens, page_size, meta=None, **kw):
+    """Page statistics of K; returns meta (allocated when None)."""
+    if meta is None:
+        kv = kv_view(k, kw.get("page_table"))
+        max_len = kw.get("max_len") or _capacity(kv)
+        B = len(seq_lens) if not isinstance(seq_lens, torch.Tensor) else seq_lens.shape[0]
+        meta = page_meta_empty(B, max_len, k.shape[2], k.shape[3], page_size, k.device)
+    return plan_page_meta(k, seq_lens, page_size, meta, **kw)()
+
+
+def plan_page_score(q: torch.Tensor, meta: torch.Tensor, seq_lens, heads: Sequence[int],
+                    page_size: int, *, max_len: int, n_query=None, scale: Optional[float] = None,
+                    groups: int = 1, init: Optional[torch.Tensor] = None,
+                    out: Optional[torch.Tensor] = None, stream=None) -> Call:
+    """Prepared dustin_page_score: Eq. 5 over pages with each page's bound on q . k, given
+    to the page's positions.  q bf16 [B, nq_max, Hq, d]; meta from page_meta; init / out
+    fp32 [B, groups, >= max_len]."""
+    _on_gpu(q, meta, init, out)
+    B, nq_max, Hq, d = q.shape
+    dev = q.device
+    Hkv = meta.shape[2]
+    if meta.shape[3] != 2 * d or meta.dtype != torch.bfloat16 or meta.stride(3) != 1 or meta.stride(2) != 2 * d:
+        raise ValueError("meta must be bf16 [B, pages, Hkv, 2d] matching q's head_dim")
+    seq = _i32_dev(seq_lens, dev)
+    nqa = _i32_dev(n_query, dev)
+    max_len = int(max_len)
+    if out is None:
+        out = torch.empty((B, groups, max_len), dtype=torch.float32, device=dev)
+    heads_host = (ctypes.c_int32 * len(heads))(*[int(h) for h in heads])
+    bt = _batch(B, max_len, nq_max, 0, seq, nqa)
+    nbytes = lib().dustin_page_score_workspace(B, max_len, int(page_size), nq_max, len(heads))
+    ws = workspace(nbytes, dev, "page_score")
+    scale = 1.0 / math.sqrt(d) if scale is None else scale
+    ins = (init.stride(0), init.stride(1)) if init is not None else (0, 0)
+    args = (_ptr(q), q.stride(0), q.stride(1), q.stride(2), Hq, heads_host, len(heads), _ptr(meta),
+            meta.stride(0), meta.stride(1), meta.shape[1], Hkv, d, int(page_size), ctypes.byref(bt),
+            float(scale), int(groups), _ptr(init), ins[0], ins[1], _ptr(out), out.stride(0),
+            out.stride(1), _ptr(ws), nbytes, _stream(stream))
+    return Call(lib().dustin_page_score, args, "dustin_page_score", (q, meta, init, bt, ws, heads_host), out)
+
+
+def page_score(q, meta, seq_lens, heads, page_size, **kw):
+    """Page-estimator importance; returns out (positions >= N_b untouched)."""
+    return plan_page_score(q, meta, seq_lens, heads, page_size, **kw)()
 
 
 # ----------------------------------------------------------------------------- top-k

@@ -247,15 +247,84 @@ int32_t dustin_version(void) { return (1 << 16) | 0; }
 
 // ------------------------------------------------------------------ score
 
-size_t dustin_score_workspace(int32_t batch, int32_t max_len, int32_t nq_max, int32_t n_heads) {
-  if (batch <= 0 || max_len <= 0 || nq_max <= 0 || n_heads <= 0) return 0;
-  const size_t ld = round_up((size_t)max_len, 64);
-  const size_t n_chunks = ((size_t)max_len + kScoreChunk - 1) / kScoreChunk;
-  const size_t rows = (size_t)batch * n_heads * nq_max;
+namespace {
+
+// workspace of one score call: fp32 logits rows of `cols` entries (a multiple of 64) and
+// per-chunk statistics, for `rows` (layer, sequence, head, query) rows
+size_t score_ws_bytes(size_t rows, size_t cols, size_t chunk) {
+  const size_t ld = round_up(cols, 64);
+  const size_t n_chunks = (cols + chunk - 1) / chunk;
   return round_up(rows * ld * sizeof(float), kAlign) + round_up(rows * n_chunks * 2 * sizeof(float), kAlign);
 }
 
-namespace {
+int log2_exact(int x) {
+  int s = 0;
+  while ((1 << s) < x) ++s;
+  return s;
+}
+
+// The scoring heads and their pass-1 column tiles: every (head, query) pair, grouped by
+// the KV head it reads, at most 16 pairs per tile.
+dustin_status score_pairs(ScoreArgs& a, const int32_t* heads_host, int32_t n_heads, int32_t num_q_heads,
+                          int32_t gs, int32_t nq_max, int* n_tiles) {
+  int nt = 0;
+  for (int i = 0; i < n_heads; ++i) {
+    const int h = heads_host[i];
+    if (h < 0 || h >= num_q_heads) return DUSTIN_ERR_INVALID_ARG;
+    for (int j = 0; j < i; ++j)
+      if (heads_host[j] == h) return DUSTIN_ERR_INVALID_ARG;
+    a.heads[i] = h;
+    const int g = h / gs;
+    for (int jq = 0; jq < nq_max; ++jq) {
+      int u = nt - 1;
+      while (u >= 0 && a.used_kv[u] != g) --u;
+      if (u < 0 || a.pairs_per_kv[u] >= 16) {
+        if (nt == kScoreMaxEntries) return DUSTIN_ERR_UNSUPPORTED;
+        u = nt++;
+        a.used_kv[u] = g;
+      }
+      a.pair_head[u * 16 + a.pairs_per_kv[u]] = (uint8_t)i;
+      a.pair_query[u * 16 + a.pairs_per_kv[u]] = (uint8_t)jq;
+      a.pairs_per_kv[u]++;
+    }
+  }
+  *n_tiles = nt;
+  return DUSTIN_OK;
+}
+
+bool score_io_ok(const float* init, int64_t init_sb, int64_t init_sg, const float* out, int64_t out_sb,
+                 int64_t out_sg) {
+  if (!out || !aligned(out, 4) || out_sb < 0 || out_sg < 0) return false;
+  return !init || (aligned(init, 4) && init_sb >= 0 && init_sg >= 0);
+}
+
+// Fills the output, size and workspace fields of a (heads, layers, k view, dims already
+// set) and launches both passes over `cols` rows per sequence at most.
+dustin_status score_launch(ScoreArgs& a, int n_tiles, int row_dim, int B, int32_t nq_max, int64_t cols,
+                           float scale, int32_t groups, const float* init, int64_t init_sb, int64_t init_sg,
+                           float* out, int64_t out_sb, int64_t out_sg, void* workspace, size_t workspace_bytes,
+                           void* stream) {
+  const size_t rows = (size_t)a.n_layers * B * a.n_heads * nq_max;
+  const size_t need_ws = score_ws_bytes(rows, (size_t)cols, (size_t)a.chunk);
+  if (!workspace || workspace_bytes < need_ws || !aligned(workspace, kAlign)) return DUSTIN_ERR_WORKSPACE;
+  a.batch = B;
+  a.groups = groups;
+  a.scale_log2 = scale * kLog2e;
+  a.init = init;
+  a.init_sb = init_sb;
+  a.init_sg = init_sg;
+  a.out = out;
+  a.out_sb = out_sb;
+  a.out_sg = out_sg;
+  a.nq_max = nq_max;
+  a.ld = (int64_t)round_up((size_t)cols, 64);
+  a.n_chunks = (int32_t)((cols + a.chunk - 1) / a.chunk);
+  a.logits = static_cast<float*>(workspace);
+  a.stats = reinterpret_cast<float*>(static_cast<char*>(workspace) +
+                                     round_up(rows * a.ld * sizeof(float), kAlign));
+  const hipError_t e = launch_score(a, B, n_tiles, row_dim, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? DUSTIN_OK : DUSTIN_ERR_LAUNCH;
+}
 
 // Eq. 5 for n_layers layers that share shapes, summed into one output.
 dustin_status run_score(int32_t n_layers, const void* const* q_layers, int64_t q_sb, int64_t q_sj,
@@ -285,75 +354,42 @@ dustin_status run_score(int32_t n_layers, const void* const* q_layers, int64_t q
       return DUSTIN_ERR_INVALID_ARG;
     if (!aligned(kl->data, 16)) return DUSTIN_ERR_INVALID_ARG;
   }
-  if (!aligned(out, 4) || out_sb < 0 || out_sg < 0) return DUSTIN_ERR_INVALID_ARG;
-  if (init && (!aligned(init, 4) || init_sb < 0 || init_sg < 0)) return DUSTIN_ERR_INVALID_ARG;
-  const int gs = num_q_heads / Hkv;
+  if (!score_io_ok(init, init_sb, init_sg, out, out_sb, out_sg)) return DUSTIN_ERR_INVALID_ARG;
 
   ScoreArgs a;
   memset(&a, 0, sizeof a);
-  int n_used = 0;
-  for (int i = 0; i < n_heads; ++i) {
-    const int h = heads_host[i];
-    if (h < 0 || h >= num_q_heads) return DUSTIN_ERR_INVALID_ARG;
-    for (int j = 0; j < i; ++j)
-      if (heads_host[j] == h) return DUSTIN_ERR_INVALID_ARG;
-    a.heads[i] = h;
-    const int g = h / gs;
-    int u = 0;
-    while (u < n_used && a.used_kv[u] != g) ++u;
-    if (u == n_used) {
-      a.used_kv[n_used++] = g;
-    }
-    for (int jq = 0; jq < bt->nq_max; ++jq) {
-      if (a.pairs_per_kv[u] >= 16) return DUSTIN_ERR_UNSUPPORTED;  // one MFMA column tile
-      a.pair_head[u * 16 + a.pairs_per_kv[u]] = (uint8_t)i;
-      a.pair_query[u * 16 + a.pairs_per_kv[u]] = (uint8_t)jq;
-      a.pairs_per_kv[u]++;
-    }
-  }
+  a.n_heads = n_heads;
+  a.group_size = num_q_heads / Hkv;
+  int n_tiles = 0;
+  dustin_status st = score_pairs(a, heads_host, n_heads, num_q_heads, a.group_size, bt->nq_max, &n_tiles);
+  if (st != DUSTIN_OK) return st;
   KvView kv;
-  const dustin_status st = kv_of(k, k->head_dim, bt->max_len, &kv);
+  st = kv_of(k, k->head_dim, bt->max_len, &kv);
   if (st != DUSTIN_OK) return st;
   const int B = bt->batch;
   if (B == 0 || bt->max_len == 0) return DUSTIN_OK;
   if ((int64_t)B * n_layers > 65535) return DUSTIN_ERR_UNSUPPORTED;
-  const size_t need_ws = dustin_score_workspace(B, bt->max_len, bt->nq_max, n_heads * n_layers);
-  if (!workspace || workspace_bytes < need_ws || !aligned(workspace, kAlign))
-    return DUSTIN_ERR_WORKSPACE;
-
   for (int l = 0; l < n_layers; ++l) {
     a.q_layers[l] = static_cast<const uint16_t*>(q_layers[l]);
     a.k_layers[l] = static_cast<const uint16_t*>(k_layers[l].data);
   }
   a.n_layers = n_layers;
-  a.batch = B;
   a.q_sb = q_sb;
   a.q_sj = q_sj;
   a.q_sh = q_sh;
   a.k = kv;
   a.dims = dims_of(bt);
-  a.n_heads = n_heads;
-  a.group_size = gs;
-  a.groups = groups;
-  a.scale_log2 = scale * kLog2e;
-  a.init = init;
-  a.init_sb = init_sb;
-  a.init_sg = init_sg;
-  a.out = out;
-  a.out_sb = out_sb;
-  a.out_sg = out_sg;
-  a.nq_max = bt->nq_max;
-  a.ld = (int64_t)round_up((size_t)bt->max_len, 64);
-  a.n_chunks = (bt->max_len + kScoreChunk - 1) / kScoreChunk;
-  const size_t rows = (size_t)n_layers * B * n_heads * bt->nq_max;
-  a.logits = static_cast<float*>(workspace);
-  a.stats = reinterpret_cast<float*>(static_cast<char*>(workspace) +
-                                     round_up(rows * a.ld * sizeof(float), kAlign));
-  const hipError_t e = launch_score(a, B, n_used, k->head_dim, static_cast<hipStream_t>(stream));
-  return e == hipSuccess ? DUSTIN_OK : DUSTIN_ERR_LAUNCH;
+  a.chunk = kScoreChunk;
+  return score_launch(a, n_tiles, k->head_dim, B, bt->nq_max, bt->max_len, scale, groups, init, init_sb,
+                      init_sg, out, out_sb, out_sg, workspace, workspace_bytes, stream);
 }
 
 }  // namespace
+
+size_t dustin_score_workspace(int32_t batch, int32_t max_len, int32_t nq_max, int32_t n_heads) {
+  if (batch <= 0 || max_len <= 0 || nq_max <= 0 || n_heads <= 0) return 0;
+  return score_ws_bytes((size_t)batch * n_heads * nq_max, (size_t)max_len, kScoreChunk);
+}
 
 dustin_status dustin_score(const void* q, int64_t q_sb, int64_t q_sj, int64_t q_sh,
                            int32_t num_q_heads, const int32_t* heads_host, int32_t n_heads,
@@ -377,6 +413,117 @@ dustin_status dustin_score_layers(int32_t n_layers, const void* const* q_layers_
   return run_score(n_layers, q_layers_host, q_sb, q_sj, q_sh, num_q_heads, heads_host, n_heads, k_layers_host,
                    bt, scale, groups, init, init_sb, init_sg, out, out_sb, out_sg, workspace, workspace_bytes,
                    stream);
+}
+
+// ------------------------------------------------------------------ page estimator
+
+namespace {
+
+bool page_size_ok(int32_t page_size) {
+  return page_size >= 1 && page_size <= kMaxPageSize && (page_size & (page_size - 1)) == 0;
+}
+
+int32_t pages_of(int32_t n, int32_t page_size) { return (int32_t)(((int64_t)n + page_size - 1) / page_size); }
+
+// a page-statistics array as a K view whose rows (pages) hold 2 * head_dim values
+dustin_status meta_view(const void* meta, int64_t meta_sb, int64_t meta_sp, int32_t meta_pages, int32_t Hkv,
+                        int32_t head_dim, int32_t need_pages, KvView* out) {
+  if (!meta || !aligned(meta, 16) || meta_sb < 0 || meta_sb % 8 || meta_sp % 8) return DUSTIN_ERR_INVALID_ARG;
+  if (meta_sp < (int64_t)Hkv * 2 * head_dim || meta_pages < need_pages) return DUSTIN_ERR_INVALID_ARG;
+  if (meta_pages <= 0) return DUSTIN_ERR_INVALID_ARG;
+  memset(out, 0, sizeof *out);
+  out->data = static_cast<const uint16_t*>(meta);
+  out->stride_b = meta_sb;
+  out->stride_n = meta_sp;
+  out->stride_h = 2 * head_dim;
+  out->capacity = meta_pages;
+  return DUSTIN_OK;
+}
+
+}  // namespace
+
+dustin_status dustin_page_meta(const dustin_kv* k, const dustin_batch* bt, const int32_t* from, int32_t max_span,
+                               int32_t page_size, void* meta, int64_t meta_sb, int64_t meta_sp,
+                               int32_t meta_pages, void* stream) {
+  if (!batch_ok(bt) || !k) return DUSTIN_ERR_INVALID_ARG;
+  if (!page_size_ok(page_size)) return DUSTIN_ERR_INVALID_ARG;
+  if (k->head_dim != 64 && k->head_dim != 128) return DUSTIN_ERR_UNSUPPORTED;
+  if (k->num_kv_heads <= 0 || k->num_kv_heads > 65535) return DUSTIN_ERR_INVALID_ARG;
+  if (max_span < 0 || max_span > bt->max_len) return DUSTIN_ERR_INVALID_ARG;
+  if (from && !aligned(from, 4)) return DUSTIN_ERR_INVALID_ARG;
+  KvView kv, mv;
+  dustin_status st = kv_of(k, k->head_dim, bt->max_len, &kv);
+  if (st != DUSTIN_OK) return st;
+  const int32_t P = pages_of(bt->max_len, page_size);
+  st = meta_view(meta, meta_sb, meta_sp, meta_pages, k->num_kv_heads, k->head_dim, P, &mv);
+  if (st != DUSTIN_OK) return st;
+  const int B = bt->batch;
+  if (B > 65535) return DUSTIN_ERR_UNSUPPORTED;
+  if (B == 0 || bt->max_len == 0 || max_span == 0) return DUSTIN_OK;
+  PageMetaArgs a;
+  memset(&a, 0, sizeof a);
+  a.k = kv;
+  a.dims = dims_of(bt);
+  a.from = from;
+  a.meta = static_cast<uint16_t*>(meta);
+  a.m_sb = meta_sb;
+  a.m_sp = meta_sp;
+  a.num_kv_heads = k->num_kv_heads;
+  a.page_shift = log2_exact(page_size);
+  // the span's pages, plus the partly filled page it may start in
+  const int32_t span = pages_of(max_span, page_size) + (from ? 1 : 0);
+  a.span_pages = span < P ? span : P;
+  const hipError_t e = launch_page_meta(a, B, k->head_dim, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? DUSTIN_OK : DUSTIN_ERR_LAUNCH;
+}
+
+size_t dustin_page_score_workspace(int32_t batch, int32_t max_len, int32_t page_size, int32_t nq_max,
+                                   int32_t n_heads) {
+  if (batch <= 0 || max_len <= 0 || nq_max <= 0 || n_heads <= 0 || !page_size_ok(page_size)) return 0;
+  return score_ws_bytes((size_t)batch * n_heads * nq_max, (size_t)pages_of(max_len, page_size), kScorePageChunk);
+}
+
+dustin_status dustin_page_score(const void* q, int64_t q_sb, int64_t q_sj, int64_t q_sh, int32_t num_q_heads,
+                                const int32_t* heads_host, int32_t n_heads, const void* meta, int64_t meta_sb,
+                                int64_t meta_sp, int32_t meta_pages, int32_t num_kv_heads, int32_t head_dim,
+                                int32_t page_size, const dustin_batch* bt, float scale, int32_t groups,
+                                const float* init, int64_t init_sb, int64_t init_sg, float* out, int64_t out_sb,
+                                int64_t out_sg, void* workspace, size_t workspace_bytes, void* stream) {
+  if (!batch_ok(bt) || !q || !heads_host) return DUSTIN_ERR_INVALID_ARG;
+  if (!isfinite(scale) || !page_size_ok(page_size)) return DUSTIN_ERR_INVALID_ARG;
+  if (n_heads < 1 || n_heads > kScoreMaxHeads) return DUSTIN_ERR_UNSUPPORTED;
+  if (num_q_heads <= 0 || num_kv_heads <= 0 || num_q_heads % num_kv_heads) return DUSTIN_ERR_INVALID_ARG;
+  if (head_dim != 64 && head_dim != 128) return DUSTIN_ERR_UNSUPPORTED;
+  if (groups != 1 && groups != num_kv_heads) return DUSTIN_ERR_INVALID_ARG;
+  if (bt->nq_max < 1 || bt->nq_max > 16) return DUSTIN_ERR_UNSUPPORTED;
+  if ((int64_t)n_heads * bt->nq_max > kScoreMaxPairs) return DUSTIN_ERR_UNSUPPORTED;
+  if (!rows_aligned(q, q_sb, q_sj, q_sh)) return DUSTIN_ERR_INVALID_ARG;
+  if (!score_io_ok(init, init_sb, init_sg, out, out_sb, out_sg)) return DUSTIN_ERR_INVALID_ARG;
+  const int32_t P = pages_of(bt->max_len, page_size);
+  ScoreArgs a;
+  memset(&a, 0, sizeof a);
+  dustin_status st = meta_view(meta, meta_sb, meta_sp, meta_pages, num_kv_heads, head_dim, P, &a.k);
+  if (st != DUSTIN_OK) return st;
+  a.n_heads = n_heads;
+  a.group_size = num_q_heads / num_kv_heads;
+  int n_tiles = 0;
+  st = score_pairs(a, heads_host, n_heads, num_q_heads, a.group_size, bt->nq_max, &n_tiles);
+  if (st != DUSTIN_OK) return st;
+  const int B = bt->batch;
+  if (B > 65535) return DUSTIN_ERR_UNSUPPORTED;
+  if (B == 0 || bt->max_len == 0) return DUSTIN_OK;
+  a.q_layers[0] = static_cast<const uint16_t*>(q);
+  a.k_layers[0] = a.k.data;
+  a.n_layers = 1;
+  a.q_sb = q_sb;
+  a.q_sj = q_sj;
+  a.q_sh = q_sh;
+  a.dims = dims_of(bt);
+  a.page_mode = 1;
+  a.page_shift = log2_exact(page_size);
+  a.chunk = kScorePageChunk;
+  return score_launch(a, n_tiles, 2 * head_dim, B, bt->nq_max, P, scale, groups, init, init_sb, init_sg, out,
+                      out_sb, out_sg, workspace, workspace_bytes, stream);
 }
 
 // ------------------------------------------------------------------ top-k

@@ -39,12 +39,17 @@ hipError_t launch_verify_attn(const AttnArgs& a, int rt, bool sparse, bool paged
 
 // ---- scoring-head importance (score.hip) ----
 constexpr int kScoreWaves = 4;
-constexpr int kScoreChunk = 1024;        // positions per pass-1 workgroup
+constexpr int kScoreChunk = 1024;        // positions per pass-1 workgroup (256 pages in page mode)
+constexpr int kScorePageChunk = 256;
 constexpr int kScoreFinishChunk = 1024;  // positions per pass-2 workgroup (4 per thread)
-constexpr int kScoreMaxHeads = 16;
+constexpr int kScoreFinishPages = 64;    // pages per pass-2 workgroup in page mode
+constexpr int kScoreMaxHeads = 64;
+constexpr int kScoreMaxEntries = 64;     // pass-1 column tiles: (KV head, up to 16 pairs)
 constexpr int kScoreMaxLayers = 8;
-constexpr int kScoreMaxPairs = 256;  // (layer, head, query) rows one output sums
+constexpr int kScoreMaxPairs = 1024;     // (layer, head, query) rows one output sums
 
+// Eq. 5 over the positions of a cache, or (page mode) over the pages of a page-statistics
+// array, whose rows [max | min] of length 2d meet the sign-split query [q+ | q-].
 struct ScoreArgs {
   const uint16_t* q_layers[kScoreMaxLayers];  // queries of each scored layer (same strides)
   int64_t q_sb, q_sj, q_sh;
@@ -52,12 +57,15 @@ struct ScoreArgs {
   const uint16_t* k_layers[kScoreMaxLayers];
   int32_t n_layers, batch;
   SeqDims dims;
+  int32_t page_mode;   // 0: rows of k are positions; 1: rows are pages of page statistics
+  int32_t page_shift;  // page mode: log2 of the page size (0 otherwise)
+  int32_t chunk;       // rows per pass-1 workgroup
   int32_t heads[kScoreMaxHeads];
   int32_t n_heads;
-  int32_t used_kv[kScoreMaxHeads];       // KV heads read by pass 1
-  int32_t pairs_per_kv[kScoreMaxHeads];  // (head, query) pairs of each used KV head
-  uint8_t pair_head[kScoreMaxHeads * 16];   // head slot of pair i of used KV head u
-  uint8_t pair_query[kScoreMaxHeads * 16];  // query of that pair
+  int32_t used_kv[kScoreMaxEntries];       // KV head of each pass-1 column tile
+  int32_t pairs_per_kv[kScoreMaxEntries];  // (head, query) pairs of that tile
+  uint8_t pair_head[kScoreMaxEntries * 16];   // head slot of pair i of tile u
+  uint8_t pair_query[kScoreMaxEntries * 16];  // query of that pair
   int32_t group_size, groups;
   float scale_log2;
   const float* init;
@@ -69,8 +77,23 @@ struct ScoreArgs {
   int64_t ld;
   int32_t nq_max, n_chunks;
 };
+static_assert(sizeof(ScoreArgs) <= 4096, "kernel arguments stay within 4 KiB");
 
-hipError_t launch_score(const ScoreArgs& a, int B, int n_used_kv, int head_dim, hipStream_t stream);
+// row_dim: length of a K row (head_dim, or 2 * head_dim for page statistics)
+hipError_t launch_score(const ScoreArgs& a, int B, int n_used_kv, int row_dim, hipStream_t stream);
+
+// ---- page statistics for the page estimator (page.hip) ----
+constexpr int kMaxPageSize = 4096;
+struct PageMetaArgs {
+  KvView k;
+  SeqDims dims;
+  const int32_t* from;  // device [B]: first position that changed, or NULL (= 0)
+  uint16_t* meta;       // [B, pages, Hkv, 2 d]: per page, channel max then min
+  int64_t m_sb, m_sp;
+  int32_t num_kv_heads, page_shift, span_pages;
+};
+
+hipError_t launch_page_meta(const PageMetaArgs& a, int B, int head_dim, hipStream_t stream);
 
 // ---- tiered selection (topk.hip) ----
 struct TopkArgs {

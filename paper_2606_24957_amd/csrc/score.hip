@@ -1,21 +1,43 @@
-// score.hip -- scoring-head importance (Eq. 5 restricted to the semantic retrieval heads).
+// score.hip -- scoring-head importance (Eq. 5 restricted to the semantic retrieval heads),
+// and the same sum over the pages of a page-statistics array (the page estimator).
 //
 // Several layers (the draft model's scoring layers) are scored in the same two launches:
 // their logits rows sit side by side and pass 2 sums every layer's pairs into one output.
-// Pass 1 (score_logits_kernel): one workgroup per (chunk of positions, KV head used by a
-//   scoring head, sequence and layer).  Each K row of that KV head is read once, with the same
-//   16-byte-per-lane MFMA A-operand loads as the attention kernel, and multiplied by
-//   every (scoring head of this KV head, query) pair at once (up to 16 pairs = one MFMA
-//   column tile).  The scaled logits (log2 domain) go to the workspace together with the
-//   chunk's running (max, sum of exp2) per pair.
+// Pass 1 (score_logits_kernel): one workgroup per (chunk of rows, column tile, sequence and
+//   layer).  A column tile is up to 16 (scoring head, query) pairs of one KV head; each K
+//   row of that KV head is read once per tile, with the same 16-byte-per-lane MFMA
+//   A-operand loads as the attention kernel, and multiplied by every pair of the tile at
+//   once.  The scaled logits (log2 domain) go to the workspace together with the chunk's
+//   running (max, sum of exp2) per pair.
+//   Page mode: a row is one page's [channel max | channel min] (length 2d) and the query
+//   operand is [q+ | q-] (q+ = max(q, 0), q- = min(q, 0)), so that the MFMA dot product is
+//   sum_c max(q_c max_c, q_c min_c), the largest q . k over keys inside the page's box.
 // Pass 2 (score_finish_kernel): per (chunk, output group, sequence): merge the chunk
 //   statistics of every pair into its softmax normaliser, then
 //   out[n] = init[n] + sum_pairs exp2(logit - M) / Z, pairs in (layer, head, query) order.
+//   Page mode (score_finish_pages_kernel): the same sum per page, written to every
+//   position of the page.
 #include "kernels.hpp"
 
 namespace dustin {
 
-template <int D, bool kPaged>
+// rows of sequence b scored: positions, or pages covering them
+__device__ __forceinline__ int score_rows(const ScoreArgs& a, int b) {
+  return (a.dims.len(b) + (1 << a.page_shift) - 1) >> a.page_shift;
+}
+
+// the non-negative (neg = false) or non-positive (neg = true) part of 8 bf16 values
+__device__ __forceinline__ u32x4 sign_part(u32x4 x, bool neg) {
+  u32x4 r;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint32_t m = ((x[i] >> 15) & 0x00010001u) * 0xFFFFu;  // 0xFFFF where the sign is set
+    r[i] = x[i] & (neg ? m : ~m);
+  }
+  return r;
+}
+
+template <int D, bool kPaged, bool kSign>
 __global__ __launch_bounds__(kScoreWaves * kWave) void score_logits_kernel(ScoreArgs a) {
   constexpr int KS = D / 32;
   // KV heads vary fastest: workgroups that run together read the same positions of every
@@ -25,10 +47,10 @@ __global__ __launch_bounds__(kScoreWaves * kWave) void score_logits_kernel(Score
   const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
   const int lr = lane & 15, lg = lane >> 4;
   const int g = a.used_kv[ug];
-  const int N = a.dims.len(b);
+  const int N = score_rows(a, b);
   const int nq = a.dims.nq(b);
-  const int p_begin = chunk * kScoreChunk;
-  const int p_end = min(N, p_begin + kScoreChunk);
+  const int p_begin = chunk * a.chunk;
+  const int p_end = min(N, p_begin + a.chunk);
 
   // pair lr of this KV head: (scoring head slot, query)
   const int npairs = a.pairs_per_kv[ug];
@@ -39,8 +61,17 @@ __global__ __launch_bounds__(kScoreWaves * kWave) void score_logits_kernel(Score
   if (pair_ok) {
     const uint16_t* qp = a.q_layers[layer] + (int64_t)b * a.q_sb + (int64_t)pair_q * a.q_sj +
                          (int64_t)a.heads[pair_slot] * a.q_sh + 8 * lg;
+    if constexpr (kSign) {  // [q+ | q-] from a query of length D / 2
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) qb[ks] = as_bf16x8(load16(qp + 32 * ks));
+      for (int ks = 0; ks < KS / 2; ++ks) {
+        const u32x4 x = load16(qp + 32 * ks);
+        qb[ks] = as_bf16x8(sign_part(x, false));
+        qb[ks + KS / 2] = as_bf16x8(sign_part(x, true));
+      }
+    } else {
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) qb[ks] = as_bf16x8(load16(qp + 32 * ks));
+    }
   } else {
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) qb[ks] = as_bf16x8(u32x4{0u, 0u, 0u, 0u});
@@ -137,32 +168,27 @@ __device__ __forceinline__ bool aligned16(const void* p) { return ((uintptr_t)p 
 constexpr int kFinishThreads = 256;
 constexpr int kFinishBatch = 8;  // logits rows loaded together per thread
 
-__global__ __launch_bounds__(kFinishThreads) void score_finish_kernel(ScoreArgs a) {
-  const int chunk = blockIdx.x, go = blockIdx.y, b = blockIdx.z;
+// The (layer, head slot, query) rows that output group go of sequence b sums, in that
+// order, with each row's softmax max M (log2 domain) and 1 / Z merged from the pass-1
+// chunk statistics.  Returns the number of rows.
+__device__ int finish_setup(const ScoreArgs& a, int b, int go, int nq, int n_rows, int* sm_row, float* sm_M,
+                            float* sm_iz, int* sm_slots, int* sm_ns) {
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
-  const int N = a.dims.len(b);
-  const int nq = a.dims.nq(b);
-  const int p_begin = chunk * kScoreFinishChunk;
-  if (p_begin >= N) return;
-
-  // the (head slot, query) pairs feeding output group go, in that order, with their
-  // logits row, softmax max M (log2 domain) and 1 / Z
-  __shared__ int sm_row[kScoreMaxPairs];
-  __shared__ float sm_M[kScoreMaxPairs], sm_iz[kScoreMaxPairs];
-  __shared__ int sm_np;
   if (tid == 0) {
-    int np = 0;
-    for (int l = 0; l < a.n_layers; ++l)
-      for (int slot = 0; slot < a.n_heads; ++slot) {
-        if (a.groups != 1 && a.heads[slot] / a.group_size != go) continue;
-        for (int j = 0; j < nq; ++j) sm_row[np++] = ((l * a.batch + b) * a.n_heads + slot) * a.nq_max + j;
-      }
-    sm_np = np;
+    int ns = 0;
+    for (int slot = 0; slot < a.n_heads; ++slot)
+      if (a.groups == 1 || a.heads[slot] / a.group_size == go) sm_slots[ns++] = slot;
+    *sm_ns = ns;
   }
   __syncthreads();
-  const int np = sm_np;
-  // each wave merges the per-chunk statistics of every fourth pair, one chunk per lane
-  const int nch = (N + kScoreChunk - 1) / kScoreChunk;
+  const int ns = *sm_ns, per_layer = ns * nq, np = a.n_layers * per_layer;
+  for (int i = tid; i < np; i += kFinishThreads) {
+    const int l = i / per_layer, r = i - l * per_layer, s = r / nq, j = r - s * nq;
+    sm_row[i] = ((l * a.batch + b) * a.n_heads + sm_slots[s]) * a.nq_max + j;
+  }
+  __syncthreads();
+  // each wave merges the per-chunk statistics of every fourth row, one chunk per lane
+  const int nch = (n_rows + a.chunk - 1) / a.chunk;
   for (int i = wave; i < np; i += kFinishThreads / kWave) {
     const float* st = a.stats + (int64_t)sm_row[i] * a.n_chunks * 2;
     float M = -INFINITY;
@@ -178,6 +204,22 @@ __global__ __launch_bounds__(kFinishThreads) void score_finish_kernel(ScoreArgs 
     }
   }
   __syncthreads();
+  return np;
+}
+
+__global__ __launch_bounds__(kFinishThreads) void score_finish_kernel(ScoreArgs a) {
+  const int chunk = blockIdx.x, go = blockIdx.y, b = blockIdx.z;
+  const int tid = threadIdx.x;
+  const int N = a.dims.len(b);
+  const int nq = a.dims.nq(b);
+  const int p_begin = chunk * kScoreFinishChunk;
+  if (p_begin >= N) return;
+
+  __shared__ int sm_row[kScoreMaxPairs];
+  __shared__ float sm_M[kScoreMaxPairs], sm_iz[kScoreMaxPairs];
+  __shared__ int sm_slots[kScoreMaxHeads];
+  __shared__ int sm_ns;
+  const int np = finish_setup(a, b, go, nq, N, sm_row, sm_M, sm_iz, sm_slots, &sm_ns);
 
   // four consecutive positions per thread (the logits rows are 64-element aligned, so
   // the vector load stays inside a row even past N)
@@ -212,21 +254,87 @@ __global__ __launch_bounds__(kFinishThreads) void score_finish_kernel(ScoreArgs 
   }
 }
 
-hipError_t launch_score(const ScoreArgs& a, int B, int n_used_kv, int head_dim, hipStream_t stream) {
+// Page mode: kScoreFinishPages pages per workgroup; wave w sums the rows i = w mod 4 of
+// lane's page, the four partial sums are added in wave order, and every position of the
+// page below N_b receives init + the page's sum.
+__global__ __launch_bounds__(kFinishThreads) void score_finish_pages_kernel(ScoreArgs a) {
+  const int chunk = blockIdx.x, go = blockIdx.y, b = blockIdx.z;
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+  const int N = a.dims.len(b);
+  const int P = score_rows(a, b);
+  const int nq = a.dims.nq(b);
+  const int p0 = chunk * kScoreFinishPages;
+  if (p0 >= P) return;
+
+  __shared__ int sm_row[kScoreMaxPairs];
+  __shared__ float sm_M[kScoreMaxPairs], sm_iz[kScoreMaxPairs];
+  __shared__ int sm_slots[kScoreMaxHeads];
+  __shared__ int sm_ns;
+  __shared__ float sm_acc[kFinishThreads / kWave][kScoreFinishPages];
+  const int np = finish_setup(a, b, go, nq, P, sm_row, sm_M, sm_iz, sm_slots, &sm_ns);
+
+  static_assert(kScoreFinishPages == kWave, "one page per lane");
+  const int p = p0 + lane;
+  const bool live = p < P;
+  float acc = 0.f;
+  constexpr int kWaves = kFinishThreads / kWave;
+  for (int i0 = wave; i0 < np; i0 += kWaves * kFinishBatch) {
+    float x[kFinishBatch];
+#pragma unroll
+    for (int u = 0; u < kFinishBatch; ++u) {
+      const int i = i0 + u * kWaves < np ? i0 + u * kWaves : i0;
+      x[u] = live ? a.logits[(int64_t)sm_row[i] * a.ld + p] : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < kFinishBatch; ++u) {
+      const int i = i0 + u * kWaves;
+      if (i < np) acc += fast_exp2(x[u] - sm_M[i]) * sm_iz[i];
+    }
+  }
+  sm_acc[wave][lane] = acc;
+  __syncthreads();
+
+  const float* init_row = a.init ? a.init + (int64_t)b * a.init_sb + (int64_t)go * a.init_sg : nullptr;
+  float* out_row = a.out + (int64_t)b * a.out_sb + (int64_t)go * a.out_sg;
+  const int n_end = min(N, (p0 + kScoreFinishPages) << a.page_shift);
+  for (int n = (p0 << a.page_shift) + tid; n < n_end; n += kFinishThreads) {
+    const int pp = (n >> a.page_shift) - p0;
+    float v = sm_acc[0][pp];
+#pragma unroll
+    for (int w = 1; w < kWaves; ++w) v += sm_acc[w][pp];
+    out_row[n] = (init_row ? init_row[n] : 0.f) + v;
+  }
+}
+
+hipError_t launch_score(const ScoreArgs& a, int B, int n_used_kv, int row_dim, hipStream_t stream) {
   dim3 grid1(n_used_kv, a.n_chunks, B * a.n_layers);
   const dim3 block(kScoreWaves * kWave);
   const bool paged = a.k.page_table != nullptr;
-  if (head_dim == 128) {
-    if (paged) hipLaunchKernelGGL((score_logits_kernel<128, true>), grid1, block, 0, stream, a);
-    else hipLaunchKernelGGL((score_logits_kernel<128, false>), grid1, block, 0, stream, a);
+  const bool pages = a.page_mode != 0;
+  if (pages) {
+    if (paged) return hipErrorInvalidValue;  // page statistics are a contiguous array
+    if (row_dim == 256) hipLaunchKernelGGL((score_logits_kernel<256, false, true>), grid1, block, 0, stream, a);
+    else if (row_dim == 128) hipLaunchKernelGGL((score_logits_kernel<128, false, true>), grid1, block, 0, stream, a);
+    else return hipErrorInvalidValue;
+  } else if (row_dim == 128) {
+    if (paged) hipLaunchKernelGGL((score_logits_kernel<128, true, false>), grid1, block, 0, stream, a);
+    else hipLaunchKernelGGL((score_logits_kernel<128, false, false>), grid1, block, 0, stream, a);
+  } else if (row_dim == 64) {
+    if (paged) hipLaunchKernelGGL((score_logits_kernel<64, true, false>), grid1, block, 0, stream, a);
+    else hipLaunchKernelGGL((score_logits_kernel<64, false, false>), grid1, block, 0, stream, a);
   } else {
-    if (paged) hipLaunchKernelGGL((score_logits_kernel<64, true>), grid1, block, 0, stream, a);
-    else hipLaunchKernelGGL((score_logits_kernel<64, false>), grid1, block, 0, stream, a);
+    return hipErrorInvalidValue;
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  dim3 grid2((a.dims.max_len + kScoreFinishChunk - 1) / kScoreFinishChunk, a.groups, B);
-  hipLaunchKernelGGL(score_finish_kernel, grid2, dim3(kFinishThreads), 0, stream, a);
+  if (pages) {
+    const int max_pages = (a.dims.max_len + (1 << a.page_shift) - 1) >> a.page_shift;
+    dim3 grid2((max_pages + kScoreFinishPages - 1) / kScoreFinishPages, a.groups, B);
+    hipLaunchKernelGGL(score_finish_pages_kernel, grid2, dim3(kFinishThreads), 0, stream, a);
+  } else {
+    dim3 grid2((a.dims.max_len + kScoreFinishChunk - 1) / kScoreFinishChunk, a.groups, B);
+    hipLaunchKernelGGL(score_finish_kernel, grid2, dim3(kFinishThreads), 0, stream, a);
+  }
   return hipGetLastError();
 }
 

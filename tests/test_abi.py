@@ -149,14 +149,12 @@ def test_score_rejects(L):
     assert _score(L, heads=(0, 8)) == D.ERR_INVALID_ARG               # head out of range
     assert _score(L, heads=(2, 2)) == D.ERR_INVALID_ARG               # duplicate head
     assert _score(L, heads=()) == D.ERR_UNSUPPORTED
-    assert _score(L, heads=tuple(range(17)), Hq=32) == D.ERR_UNSUPPORTED
+    assert _score(L, heads=tuple(range(65)), Hq=128) == D.ERR_UNSUPPORTED  # at most 64 heads
     assert _score(L, groups=3) == D.ERR_INVALID_ARG
     assert _score(L, q=None) == D.ERR_INVALID_ARG
     assert _score(L, out=None) == D.ERR_INVALID_ARG
     assert _score(L, kv=_kv(d=96)) == D.ERR_UNSUPPORTED
     assert _score(L, bt=_batch(nq=17)) == D.ERR_UNSUPPORTED
-    # 5 queries x 4 heads of one KV head exceed one 16-column MFMA tile
-    assert _score(L, heads=(0, 1, 2, 3), bt=_batch(nq=5)) == D.ERR_UNSUPPORTED
     assert _score(L, ws=None, ws_bytes=0) == D.ERR_WORKSPACE
     assert _score(L, ws=FAKE + 4) == D.ERR_WORKSPACE
     assert _score(L, ws_bytes=16) == D.ERR_WORKSPACE
@@ -171,3 +169,62 @@ def test_product_never_touches_the_oracle():
                 text = open(os.path.join(dirpath, f)).read()
                 assert not re.search(r"^\s*(import|from)\s+oracle", text, re.M), f
                 assert "liboracle" not in text, f
+
+
+def test_page_workspace_sizes(L):
+    s = L.dustin_page_score_workspace(16, 32768, 16, 5, 64)
+    assert s >= 16 * 64 * 5 * 2048 * 4 and s % 256 == 0
+    assert L.dustin_page_score_workspace(16, 32768, 12, 5, 64) == 0   # page size not 2^k
+    assert L.dustin_page_score_workspace(0, 32768, 16, 5, 64) == 0
+
+
+def _meta_call(L, kv=None, bt=None, frm=None, span=100, ps=16, meta=FAKE, sb=None, sp=None, pages=7):
+    kv = kv or _kv()
+    bt = bt or _batch()
+    d, Hkv = kv.head_dim, kv.num_kv_heads
+    sp = Hkv * 2 * d if sp is None else sp
+    sb = pages * sp if sb is None else sb
+    return L.dustin_page_meta(ctypes.byref(kv), ctypes.byref(bt), frm, span, ps, meta, sb, sp, pages, None)
+
+
+def test_page_meta_rejects(L):
+    assert _meta_call(L, ps=12) == D.ERR_INVALID_ARG                  # page size not 2^k
+    assert _meta_call(L, ps=0) == D.ERR_INVALID_ARG
+    assert _meta_call(L, ps=8192) == D.ERR_INVALID_ARG
+    assert _meta_call(L, kv=_kv(d=96)) == D.ERR_UNSUPPORTED
+    assert _meta_call(L, meta=None) == D.ERR_INVALID_ARG
+    assert _meta_call(L, meta=FAKE + 4) == D.ERR_INVALID_ARG
+    assert _meta_call(L, pages=6) == D.ERR_INVALID_ARG                # ceil(100 / 16) = 7 pages
+    assert _meta_call(L, sp=2 * 128) == D.ERR_INVALID_ARG             # rows of 2 KV heads overlap
+    assert _meta_call(L, span=101) == D.ERR_INVALID_ARG               # span > max_len
+    assert _meta_call(L, span=-1) == D.ERR_INVALID_ARG
+    assert _meta_call(L, frm=FAKE + 2) == D.ERR_INVALID_ARG
+    assert _meta_call(L, kv=_kv(cap=99)) == D.ERR_INVALID_ARG         # cache shorter than max_len
+    assert L.dustin_page_meta(None, ctypes.byref(_batch()), None, 10, 16, FAKE, 0, 512, 7,
+                              None) == D.ERR_INVALID_ARG
+
+
+def _pscore(L, heads=(0, 3), Hq=8, Hkv=2, d=128, ps=16, pages=7, bt=None, groups=1, q=FAKE, meta=FAKE,
+            out=FAKE, ws=FAKE, ws_bytes=1 << 30, sp=None):
+    bt = bt or _batch()
+    arr = (ctypes.c_int32 * max(1, len(heads)))(*heads)
+    sp = Hkv * 2 * d if sp is None else sp
+    return L.dustin_page_score(q, 800 * 8 * d, 8 * d, d, Hq, arr, len(heads), meta, pages * sp, sp, pages, Hkv,
+                               d, ps, ctypes.byref(bt), 0.1, groups, None, 0, 0, out, 0, 0, ws, ws_bytes, None)
+
+
+def test_page_score_rejects(L):
+    assert _pscore(L, heads=(0, 8)) == D.ERR_INVALID_ARG
+    assert _pscore(L, heads=(1, 1)) == D.ERR_INVALID_ARG
+    assert _pscore(L, heads=tuple(range(65)), Hq=128) == D.ERR_UNSUPPORTED
+    assert _pscore(L, ps=3) == D.ERR_INVALID_ARG
+    assert _pscore(L, d=96) == D.ERR_UNSUPPORTED
+    assert _pscore(L, Hq=7) == D.ERR_INVALID_ARG
+    assert _pscore(L, groups=3) == D.ERR_INVALID_ARG
+    assert _pscore(L, pages=6) == D.ERR_INVALID_ARG
+    assert _pscore(L, meta=None) == D.ERR_INVALID_ARG
+    assert _pscore(L, q=None) == D.ERR_INVALID_ARG
+    assert _pscore(L, out=None) == D.ERR_INVALID_ARG
+    assert _pscore(L, bt=_batch(nq=17)) == D.ERR_UNSUPPORTED
+    assert _pscore(L, ws=None, ws_bytes=0) == D.ERR_WORKSPACE
+    assert _pscore(L, ws_bytes=64) == D.ERR_WORKSPACE
