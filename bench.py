@@ -45,7 +45,7 @@ def parse():
     p.add_argument("--cpu-sample-seqs", type=int, default=16)
     p.add_argument("--copy-probe", action="store_true",
                    help="also run one plain 1 GiB device copy (counter calibration)")
-    p.add_argument("--only", choices=["all", "sparse", "dense", "estimate"], default="all",
+    p.add_argument("--only", choices=["all", "sparse", "dense", "estimate", "page"], default="all",
                    help="restrict the timed step (profiling runs)")
     return p.parse_args()
 
@@ -96,6 +96,21 @@ def topk_bytes(s):
     return sum(2 * 4 * n + 4 * min(k, n) for n, k in zip(s.seq_lens, s.budget))
 
 
+def page_bytes(s, ps):
+    """Page estimator: statistics rows (2d bf16 per page and KV head) built from K; page
+    scores read the rows of the KV heads their heads use and write S (4 B per position)."""
+    pages = [-(-n // ps) for n in s.seq_lens]
+    row = 2 * s.head_dim * 2
+    meta = sum(s.num_kv_heads * p * row for p in pages)
+    build = sum(s.num_kv_heads * n * s.head_dim * 2 for n in s.seq_lens) + meta
+    q_all = sum(t * s.num_q_heads * s.head_dim * 2 for t in s.n_query)
+    score_all = meta + q_all + sum(4 * n for n in s.seq_lens)
+    gs = s.num_q_heads // s.num_kv_heads
+    kvh = len({h // gs for h in s.target_heads})
+    score_srh = sum(kvh * p * row + 4 * n for p, n in zip(pages, s.seq_lens))
+    return {"build": build, "score_all_heads": score_all, "score_scoring_heads": score_srh}
+
+
 # ----------------------------------------------------------------------------- traffic
 
 def measured_traffic(workload, k):
@@ -112,6 +127,76 @@ def measured_traffic(workload, k):
     if rec.get("source_sha256") != kernel_sources_sha():
         return None
     return rec.get("bytes_per_launch")
+
+
+# ----------------------------------------------------------------------------- page estimator
+
+def page_estimator(s, layers, est, seq, nq, bud, steps, warmup, ps=16):
+    """The page estimator (Quest with 16-position pages) on the same layers: statistics
+    built once per layer (prefill) and refreshed for the newest T_b positions (per layer
+    and step), page scores of every query head of a layer (Quest-16) and of the target's
+    scoring heads only.  Each figure is the event time of `steps` launches cycling over
+    the stacked layers, divided by `steps`."""
+    import torch
+    import paper_2606_24957_amd as D
+    dev = seq.device
+    B, N = s.B, s.n_max
+    metas = [D.page_meta_empty(B, N, s.num_kv_heads, s.head_dim, ps, dev) for _ in layers]
+    build = [D.plan_page_meta(l.k, seq, ps, m, max_len=N, page_table=l.page_table)
+             for l, m in zip(layers, metas)]
+    newest = (seq - nq).clamp(min=0)  # the last T_b positions stand for the newest append
+    update = [D.plan_page_meta(l.k, seq, ps, m, from_=newest, max_span=s.t_max, max_len=N,
+                               page_table=l.page_table) for l, m in zip(layers, metas)]
+    s_q = torch.zeros((B, 1, N), dtype=torch.float32, device=dev)
+    s_h = torch.zeros((B, 1, N), dtype=torch.float32, device=dev)
+    quest = [D.plan_page_score(l.q, m, seq, list(range(s.num_q_heads)), ps, max_len=N, n_query=nq,
+                               out=s_q) for l, m in zip(layers, metas)]
+    srh = [D.plan_page_score(est.q_target, m, seq, s.target_heads, ps, max_len=N, out=s_h) for m in metas]
+    idx = torch.zeros((B, 1, s.k_max), dtype=torch.int32, device=dev)
+    cnt = torch.zeros((B, 1), dtype=torch.int32, device=dev)
+    sel = [D.plan_topk(None, s_q, seq, s.k_max, budget=bud, m_scalar=0, n_sink=s.n_sink,
+                       n_window=s.n_window, idx=idx, count=cnt)]
+
+    def timed(calls):
+        for i in range(warmup):
+            calls[i % len(calls)]()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for i in range(steps):
+            calls[i % len(calls)]()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / steps
+
+    t_build = timed(build)
+    t_update = timed(update)
+    t_quest = timed(quest)
+    t_srh = timed(srh)
+    t_sel = timed(sel)
+    nb = page_bytes(s, ps)
+
+    def gbps(b, us):
+        return round(b / (us * 1e-6) / 1e9, 1)
+
+    per_layer = t_update + t_quest + t_sel
+    rec = {
+        "page_size": ps,
+        "build_us_per_layer": round(t_build, 2), "build_GBps": gbps(nb["build"], t_build),
+        "update_us_per_layer": round(t_update, 2),
+        "score_all_heads_us_per_layer": round(t_quest, 2),
+        "score_all_heads_GBps": gbps(nb["score_all_heads"], t_quest),
+        "score_all_heads_frac": round(nb["score_all_heads"] / (t_quest * 1e-6) / 1e9 / PEAK_HBM_GBPS, 4),
+        "score_all_heads_bytes": nb["score_all_heads"],
+        "score_scoring_heads_us": round(t_srh, 2),
+        "score_scoring_heads_GBps": gbps(nb["score_scoring_heads"], t_srh),
+        "topk_us": round(t_sel, 2),
+        "quest16_estimation_us_per_step_L80": round(80 * per_layer, 1),
+    }
+    log(f"[bench] page estimator (page {ps}): build {t_build:.1f} us/layer, update {t_update:.1f}, "
+        f"all-heads score {t_quest:.1f} us/layer ({rec['score_all_heads_GBps']} GB/s), scoring-heads "
+        f"score {t_srh:.1f} us, top-k {t_sel:.1f} us; Quest-16 estimation at L=80 {80 * per_layer:.0f} us/step")
+    del metas
+    return rec
 
 
 # ----------------------------------------------------------------------------- CPU baseline
@@ -347,6 +432,13 @@ def main():
             vstep = {"error": str(exc)[:200]}
             log(f"[bench] verify step graph: {exc}")
 
+    page = None
+    if args.only in ("all", "page"):
+        page = page_estimator(s, layers, est, seq, nq, bud, args.steps, args.warmup)
+        if est_us == est_us:
+            page["dustin_estimation_us_per_step"] = round(est_us, 1)
+            page["quest16_over_dustin_L80"] = round(page["quest16_estimation_us_per_step_L80"] / est_us, 2)
+
     cpu = None
     if not args.no_cpu_baseline and args.only == "all":
         log("[bench] timing the oracle on the host cores ...")
@@ -395,6 +487,7 @@ def main():
             "per_step_L80": round(80 * dn_us / (est_us + 80 * sp_us), 3) if sp else None,
         },
         "verify_step": vstep,
+        "page_estimator": page,
         "cpu_baseline": cpu,
     }
     print(json.dumps(rec), flush=True)

@@ -263,32 +263,48 @@ int log2_exact(int x) {
   return s;
 }
 
-// The scoring heads and their pass-1 column tiles: every (head, query) pair, grouped by
-// the KV head it reads, at most 16 pairs per tile.
+// The scoring heads and their pass-1 column tiles: every (head, query) pair, KV head by
+// KV head, at most 16 pairs per tile; then the pass-1 workgroups, each up to
+// kScoreGroupTiles consecutive tiles of one KV head (its rows are read once for all).
 dustin_status score_pairs(ScoreArgs& a, const int32_t* heads_host, int32_t n_heads, int32_t num_q_heads,
-                          int32_t gs, int32_t nq_max, int* n_tiles) {
-  int nt = 0;
+                          int32_t gs, int32_t nq_max, int* n_groups, int* max_group) {
   for (int i = 0; i < n_heads; ++i) {
     const int h = heads_host[i];
     if (h < 0 || h >= num_q_heads) return DUSTIN_ERR_INVALID_ARG;
     for (int j = 0; j < i; ++j)
       if (heads_host[j] == h) return DUSTIN_ERR_INVALID_ARG;
     a.heads[i] = h;
-    const int g = h / gs;
-    for (int jq = 0; jq < nq_max; ++jq) {
-      int u = nt - 1;
-      while (u >= 0 && a.used_kv[u] != g) --u;
-      if (u < 0 || a.pairs_per_kv[u] >= 16) {
-        if (nt == kScoreMaxEntries) return DUSTIN_ERR_UNSUPPORTED;
-        u = nt++;
-        a.used_kv[u] = g;
+  }
+  int nt = 0;
+  for (int g = 0; g < num_q_heads / gs; ++g) {
+    int u = -1;  // the open tile of KV head g
+    for (int i = 0; i < n_heads; ++i) {
+      if (heads_host[i] / gs != g) continue;
+      for (int jq = 0; jq < nq_max; ++jq) {
+        if (u < 0 || a.pairs_per_kv[u] == 16) {
+          if (nt == kScoreMaxEntries) return DUSTIN_ERR_UNSUPPORTED;
+          u = nt++;
+          a.used_kv[u] = g;
+        }
+        a.pair_head[u * 16 + a.pairs_per_kv[u]] = (uint8_t)i;
+        a.pair_query[u * 16 + a.pairs_per_kv[u]] = (uint8_t)jq;
+        a.pairs_per_kv[u]++;
       }
-      a.pair_head[u * 16 + a.pairs_per_kv[u]] = (uint8_t)i;
-      a.pair_query[u * 16 + a.pairs_per_kv[u]] = (uint8_t)jq;
-      a.pairs_per_kv[u]++;
     }
   }
-  *n_tiles = nt;
+  int ng = 0, mg = 0;
+  for (int u = 0; u < nt; ++u) {
+    if (ng > 0 && a.used_kv[a.tile_first[ng - 1]] == a.used_kv[u] && a.tile_count[ng - 1] < kScoreGroupTiles) {
+      a.tile_count[ng - 1]++;
+    } else {
+      a.tile_first[ng] = (uint8_t)u;
+      a.tile_count[ng] = 1;
+      ++ng;
+    }
+    if (a.tile_count[ng - 1] > mg) mg = a.tile_count[ng - 1];
+  }
+  *n_groups = ng;
+  *max_group = mg;
   return DUSTIN_OK;
 }
 
@@ -300,7 +316,7 @@ bool score_io_ok(const float* init, int64_t init_sb, int64_t init_sg, const floa
 
 // Fills the output, size and workspace fields of a (heads, layers, k view, dims already
 // set) and launches both passes over `cols` rows per sequence at most.
-dustin_status score_launch(ScoreArgs& a, int n_tiles, int row_dim, int B, int32_t nq_max, int64_t cols,
+dustin_status score_launch(ScoreArgs& a, int n_groups, int max_group, int row_dim, int B, int32_t nq_max, int64_t cols,
                            float scale, int32_t groups, const float* init, int64_t init_sb, int64_t init_sg,
                            float* out, int64_t out_sb, int64_t out_sg, void* workspace, size_t workspace_bytes,
                            void* stream) {
@@ -322,7 +338,7 @@ dustin_status score_launch(ScoreArgs& a, int n_tiles, int row_dim, int B, int32_
   a.logits = static_cast<float*>(workspace);
   a.stats = reinterpret_cast<float*>(static_cast<char*>(workspace) +
                                      round_up(rows * a.ld * sizeof(float), kAlign));
-  const hipError_t e = launch_score(a, B, n_tiles, row_dim, static_cast<hipStream_t>(stream));
+  const hipError_t e = launch_score(a, B, n_groups, max_group, row_dim, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? DUSTIN_OK : DUSTIN_ERR_LAUNCH;
 }
 
@@ -360,8 +376,9 @@ dustin_status run_score(int32_t n_layers, const void* const* q_layers, int64_t q
   memset(&a, 0, sizeof a);
   a.n_heads = n_heads;
   a.group_size = num_q_heads / Hkv;
-  int n_tiles = 0;
-  dustin_status st = score_pairs(a, heads_host, n_heads, num_q_heads, a.group_size, bt->nq_max, &n_tiles);
+  int n_groups = 0, max_group = 0;
+  dustin_status st =
+      score_pairs(a, heads_host, n_heads, num_q_heads, a.group_size, bt->nq_max, &n_groups, &max_group);
   if (st != DUSTIN_OK) return st;
   KvView kv;
   st = kv_of(k, k->head_dim, bt->max_len, &kv);
@@ -380,7 +397,7 @@ dustin_status run_score(int32_t n_layers, const void* const* q_layers, int64_t q
   a.k = kv;
   a.dims = dims_of(bt);
   a.chunk = kScoreChunk;
-  return score_launch(a, n_tiles, k->head_dim, B, bt->nq_max, bt->max_len, scale, groups, init, init_sb,
+  return score_launch(a, n_groups, max_group, k->head_dim, B, bt->nq_max, bt->max_len, scale, groups, init, init_sb,
                       init_sg, out, out_sb, out_sg, workspace, workspace_bytes, stream);
 }
 
@@ -506,8 +523,8 @@ dustin_status dustin_page_score(const void* q, int64_t q_sb, int64_t q_sj, int64
   if (st != DUSTIN_OK) return st;
   a.n_heads = n_heads;
   a.group_size = num_q_heads / num_kv_heads;
-  int n_tiles = 0;
-  st = score_pairs(a, heads_host, n_heads, num_q_heads, a.group_size, bt->nq_max, &n_tiles);
+  int n_groups = 0, max_group = 0;
+  st = score_pairs(a, heads_host, n_heads, num_q_heads, a.group_size, bt->nq_max, &n_groups, &max_group);
   if (st != DUSTIN_OK) return st;
   const int B = bt->batch;
   if (B > 65535) return DUSTIN_ERR_UNSUPPORTED;
@@ -522,7 +539,7 @@ dustin_status dustin_page_score(const void* q, int64_t q_sb, int64_t q_sj, int64
   a.page_mode = 1;
   a.page_shift = log2_exact(page_size);
   a.chunk = kScorePageChunk;
-  return score_launch(a, n_tiles, 2 * head_dim, B, bt->nq_max, P, scale, groups, init, init_sb, init_sg, out,
+  return score_launch(a, n_groups, max_group, 2 * head_dim, B, bt->nq_max, P, scale, groups, init, init_sb, init_sg, out,
                       out_sb, out_sg, workspace, workspace_bytes, stream);
 }
 

@@ -45,6 +45,7 @@ constexpr int kScoreFinishChunk = 1024;  // positions per pass-2 workgroup (4 pe
 constexpr int kScoreFinishPages = 64;    // pages per pass-2 workgroup in page mode
 constexpr int kScoreMaxHeads = 64;
 constexpr int kScoreMaxEntries = 64;     // pass-1 column tiles: (KV head, up to 16 pairs)
+constexpr int kScoreGroupTiles = 3;      // column tiles of one KV head per pass-1 workgroup
 constexpr int kScoreMaxLayers = 8;
 constexpr int kScoreMaxPairs = 1024;     // (layer, head, query) rows one output sums
 
@@ -64,6 +65,8 @@ struct ScoreArgs {
   int32_t n_heads;
   int32_t used_kv[kScoreMaxEntries];       // KV head of each pass-1 column tile
   int32_t pairs_per_kv[kScoreMaxEntries];  // (head, query) pairs of that tile
+  uint8_t tile_first[kScoreMaxEntries];    // pass-1 workgroup x: its first tile
+  uint8_t tile_count[kScoreMaxEntries];    // and its tile count (same KV head)
   uint8_t pair_head[kScoreMaxEntries * 16];   // head slot of pair i of tile u
   uint8_t pair_query[kScoreMaxEntries * 16];  // query of that pair
   int32_t group_size, groups;
@@ -79,8 +82,9 @@ struct ScoreArgs {
 };
 static_assert(sizeof(ScoreArgs) <= 4096, "kernel arguments stay within 4 KiB");
 
-// row_dim: length of a K row (head_dim, or 2 * head_dim for page statistics)
-hipError_t launch_score(const ScoreArgs& a, int B, int n_used_kv, int row_dim, hipStream_t stream);
+// n_groups pass-1 workgroups along x (tile_first / tile_count), max_group the largest
+// tile count; row_dim: length of a K row (head_dim, or 2 * head_dim for page statistics)
+hipError_t launch_score(const ScoreArgs& a, int B, int n_groups, int max_group, int row_dim, hipStream_t stream);
 
 // ---- page statistics for the page estimator (page.hip) ----
 constexpr int kMaxPageSize = 4096;

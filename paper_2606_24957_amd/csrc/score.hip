@@ -37,52 +37,68 @@ __device__ __forceinline__ u32x4 sign_part(u32x4 x, bool neg) {
   return r;
 }
 
-template <int D, bool kPaged, bool kSign>
+template <int D, bool kPaged, bool kSign, int NT>
 __global__ __launch_bounds__(kScoreWaves * kWave) void score_logits_kernel(ScoreArgs a) {
   constexpr int KS = D / 32;
+  // 16-row tiles per iteration (loads issued together); fewer when the query operands of
+  // several column tiles take the registers
+  constexpr int U = NT == 1 ? 4 : 2;
   // KV heads vary fastest: workgroups that run together read the same positions of every
-  // used KV head (neighbouring 256-byte pieces of the same cache rows)
-  const int ug = blockIdx.x, chunk = blockIdx.y;
+  // used KV head (neighbouring pieces of the same cache rows)
+  const int grp = blockIdx.x, chunk = blockIdx.y;
   const int layer = blockIdx.z / a.batch, b = blockIdx.z - layer * a.batch;
   const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
   const int lr = lane & 15, lg = lane >> 4;
-  const int g = a.used_kv[ug];
+  const int u0 = a.tile_first[grp];
+  const int nt = NT == 1 ? 1 : a.tile_count[grp];  // column tiles of this group, one KV head
+  const int g = a.used_kv[u0];
   const int N = score_rows(a, b);
   const int nq = a.dims.nq(b);
   const int p_begin = chunk * a.chunk;
   const int p_end = min(N, p_begin + a.chunk);
+  const int64_t rb = (int64_t)layer * a.batch + b;  // (layer, sequence) row block
 
-  // pair lr of this KV head: (scoring head slot, query)
-  const int npairs = a.pairs_per_kv[ug];
-  const int pair_slot = lr < npairs ? a.pair_head[ug * 16 + lr] : 0;
-  const int pair_q = lr < npairs ? a.pair_query[ug * 16 + lr] : 0;
-  const bool pair_ok = lr < npairs && pair_q < nq;
-  bf16x8 qb[KS];
-  if (pair_ok) {
-    const uint16_t* qp = a.q_layers[layer] + (int64_t)b * a.q_sb + (int64_t)pair_q * a.q_sj +
-                         (int64_t)a.heads[pair_slot] * a.q_sh + 8 * lg;
-    if constexpr (kSign) {  // [q+ | q-] from a query of length D / 2
+  // column lr of tile t: (scoring head slot, query)
+  bf16x8 qb[NT][KS];
+  int pair_slot[NT], pair_q[NT];
+  bool pair_ok[NT];
+  float* lrow[NT];
 #pragma unroll
-      for (int ks = 0; ks < KS / 2; ++ks) {
-        const u32x4 x = load16(qp + 32 * ks);
-        qb[ks] = as_bf16x8(sign_part(x, false));
-        qb[ks + KS / 2] = as_bf16x8(sign_part(x, true));
+  for (int t = 0; t < NT; ++t) {
+    const int u = u0 + (t < nt ? t : 0);
+    const int npairs = t < nt ? a.pairs_per_kv[u] : 0;
+    pair_slot[t] = lr < npairs ? a.pair_head[u * 16 + lr] : 0;
+    pair_q[t] = lr < npairs ? a.pair_query[u * 16 + lr] : 0;
+    pair_ok[t] = lr < npairs && pair_q[t] < nq;
+    lrow[t] = a.logits + ((rb * a.n_heads + pair_slot[t]) * a.nq_max + pair_q[t]) * a.ld;
+    if (pair_ok[t]) {
+      const uint16_t* qp = a.q_layers[layer] + (int64_t)b * a.q_sb + (int64_t)pair_q[t] * a.q_sj +
+                           (int64_t)a.heads[pair_slot[t]] * a.q_sh + 8 * lg;
+      if constexpr (kSign) {  // [q+ | q-] from a query of length D / 2
+#pragma unroll
+        for (int ks = 0; ks < KS / 2; ++ks) {
+          const u32x4 x = load16(qp + 32 * ks);
+          qb[t][ks] = as_bf16x8(sign_part(x, false));
+          qb[t][ks + KS / 2] = as_bf16x8(sign_part(x, true));
+        }
+      } else {
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) qb[t][ks] = as_bf16x8(load16(qp + 32 * ks));
       }
     } else {
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) qb[ks] = as_bf16x8(load16(qp + 32 * ks));
+      for (int ks = 0; ks < KS; ++ks) qb[t][ks] = as_bf16x8(u32x4{0u, 0u, 0u, 0u});
     }
-  } else {
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) qb[ks] = as_bf16x8(u32x4{0u, 0u, 0u, 0u});
   }
   KvView kv = a.k;
   kv.data = a.k_layers[layer];
-  const int64_t rb = (int64_t)layer * a.batch + b;  // (layer, sequence) row block
-  float* lrow = a.logits + ((rb * a.n_heads + pair_slot) * a.nq_max + pair_q) * a.ld;
 
-  float m_run = -INFINITY, s_run = 0.f;
-  constexpr int U = 4;  // 16-position tiles per iteration (loads issued together)
+  float m_run[NT], s_run[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    m_run[t] = -INFINITY;
+    s_run[t] = 0.f;
+  }
   for (int p0 = p_begin + wave * 16 * U; p0 < p_end; p0 += kScoreWaves * 16 * U) {
     u32x4 kr[U][KS];
 #pragma unroll
@@ -94,60 +110,70 @@ __global__ __launch_bounds__(kScoreWaves * kWave) void score_logits_kernel(Score
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      f32x4 c = {0.f, 0.f, 0.f, 0.f};
+      const int pb = p0 + 16 * u + 4 * lg;  // this lane's 4 rows, column lr
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) c = mfma16x16x32(as_bf16x8(kr[u][ks]), qb[ks], c);
-      const int pb = p0 + 16 * u + 4 * lg;  // this lane's 4 positions, pair lr
-      float x[4];
-      float mx = -INFINITY;
+      for (int t = 0; t < NT; ++t) {
+        if (t >= nt) break;  // uniform over the workgroup
+        f32x4 c = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        x[e] = (pb + e < p_end) ? c[e] * a.scale_log2 : -INFINITY;
-        mx = fmaxf(mx, x[e]);
-      }
-      const float m_new = fmaxf(m_run, mx);
-      const float m_use = m_new == -INFINITY ? 0.f : m_new;
-      float add = 0.f;
+        for (int ks = 0; ks < KS; ++ks) c = mfma16x16x32(as_bf16x8(kr[u][ks]), qb[t][ks], c);
+        float x[4];
+        float mx = -INFINITY;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) add += fast_exp2(x[e] - m_use);
-      s_run = s_run * fast_exp2(m_run - m_use) + add;
-      m_run = m_new;
-      if (pair_ok) {
-        if (pb + 3 < p_end) {
-          *reinterpret_cast<f32x4*>(lrow + pb) = f32x4{x[0], x[1], x[2], x[3]};
-        } else {
+        for (int e = 0; e < 4; ++e) {
+          x[e] = (pb + e < p_end) ? c[e] * a.scale_log2 : -INFINITY;
+          mx = fmaxf(mx, x[e]);
+        }
+        const float m_new = fmaxf(m_run[t], mx);
+        const float m_use = m_new == -INFINITY ? 0.f : m_new;
+        float add = 0.f;
 #pragma unroll
-          for (int e = 0; e < 4; ++e)
-            if (pb + e < p_end) lrow[pb + e] = x[e];
+        for (int e = 0; e < 4; ++e) add += fast_exp2(x[e] - m_use);
+        s_run[t] = s_run[t] * fast_exp2(m_run[t] - m_use) + add;
+        m_run[t] = m_new;
+        if (pair_ok[t]) {
+          if (pb + 3 < p_end) {
+            *reinterpret_cast<f32x4*>(lrow[t] + pb) = f32x4{x[0], x[1], x[2], x[3]};
+          } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              if (pb + e < p_end) lrow[t][pb + e] = x[e];
+          }
         }
       }
     }
   }
 
   // reduce (max, sum) over lane groups, then over waves (fixed order)
+  __shared__ float sm[NT][kScoreWaves][16][2];
 #pragma unroll
-  for (int off = 16; off <= 32; off <<= 1) {
-    const float mo = __shfl_xor(m_run, off), so = __shfl_xor(s_run, off);
-    const float mn = fmaxf(m_run, mo);
-    const float mu = mn == -INFINITY ? 0.f : mn;
-    s_run = s_run * fast_exp2(m_run - mu) + so * fast_exp2(mo - mu);
-    m_run = mn;
-  }
-  __shared__ float sm[kScoreWaves][16][2];
-  if (lg == 0) {
-    sm[wave][lr][0] = m_run;
-    sm[wave][lr][1] = s_run;
+  for (int t = 0; t < NT; ++t) {
+#pragma unroll
+    for (int off = 16; off <= 32; off <<= 1) {
+      const float mo = __shfl_xor(m_run[t], off), so = __shfl_xor(s_run[t], off);
+      const float mn = fmaxf(m_run[t], mo);
+      const float mu = mn == -INFINITY ? 0.f : mn;
+      s_run[t] = s_run[t] * fast_exp2(m_run[t] - mu) + so * fast_exp2(mo - mu);
+      m_run[t] = mn;
+    }
+    if (lg == 0) {
+      sm[t][wave][lr][0] = m_run[t];
+      sm[t][wave][lr][1] = s_run[t];
+    }
   }
   __syncthreads();
-  if (threadIdx.x < 16 && pair_ok) {
-    float M = -INFINITY;
-    for (int w = 0; w < kScoreWaves; ++w) M = fmaxf(M, sm[w][lr][0]);
-    const float mu = M == -INFINITY ? 0.f : M;
-    float S = 0.f;
-    for (int w = 0; w < kScoreWaves; ++w) S += sm[w][lr][1] * fast_exp2(sm[w][lr][0] - mu);
-    float* st = a.stats + (((rb * a.n_heads + pair_slot) * a.nq_max + pair_q) * a.n_chunks + chunk) * 2;
-    st[0] = M;
-    st[1] = S;
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    if (threadIdx.x < 16 && t < nt && pair_ok[t]) {
+      float M = -INFINITY;
+      for (int w = 0; w < kScoreWaves; ++w) M = fmaxf(M, sm[t][w][lr][0]);
+      const float mu = M == -INFINITY ? 0.f : M;
+      float S = 0.f;
+      for (int w = 0; w < kScoreWaves; ++w) S += sm[t][w][lr][1] * fast_exp2(sm[t][w][lr][0] - mu);
+      float* st = a.stats + (((rb * a.n_heads + pair_slot[t]) * a.nq_max + pair_q[t]) * a.n_chunks + chunk) * 2;
+      st[0] = M;
+      st[1] = S;
+    }
   }
 }
 
@@ -187,19 +213,42 @@ __device__ int finish_setup(const ScoreArgs& a, int b, int go, int nq, int n_row
     sm_row[i] = ((l * a.batch + b) * a.n_heads + sm_slots[s]) * a.nq_max + j;
   }
   __syncthreads();
-  // each wave merges the per-chunk statistics of every fourth row, one chunk per lane
   const int nch = (n_rows + a.chunk - 1) / a.chunk;
-  for (int i = wave; i < np; i += kFinishThreads / kWave) {
-    const float* st = a.stats + (int64_t)sm_row[i] * a.n_chunks * 2;
-    float M = -INFINITY;
-    for (int c = lane; c < nch; c += kWave) M = fmaxf(M, st[2 * c]);
-    M = wave_max(M);
-    const float mu = M == -INFINITY ? 0.f : M;
-    float Z = 0.f;
-    for (int c = lane; c < nch; c += kWave) Z += st[2 * c + 1] * fast_exp2(st[2 * c] - mu);
-    Z = wave_sum(Z);
-    if (lane == 0) {
-      sm_M[i] = mu;
+  if (np <= kFinishThreads / kWave * 4) {
+    // few rows: each wave merges every fourth row, one chunk per lane (one round trip)
+    for (int i = wave; i < np; i += kFinishThreads / kWave) {
+      const float* st = a.stats + (int64_t)sm_row[i] * a.n_chunks * 2;
+      float M = -INFINITY;
+      for (int c = lane; c < nch; c += kWave) M = fmaxf(M, st[2 * c]);
+      M = wave_max(M);
+      const float mu = M == -INFINITY ? 0.f : M;
+      float Z = 0.f;
+      for (int c = lane; c < nch; c += kWave) Z += st[2 * c + 1] * fast_exp2(st[2 * c] - mu);
+      Z = wave_sum(Z);
+      if (lane == 0) {
+        sm_M[i] = mu;
+        sm_iz[i] = Z > 0.f ? 1.f / Z : 0.f;
+      }
+    }
+  } else {
+    // many rows: one row per thread, its chunks' (max, sum) loaded kFinishBatch at a time
+    // and merged in chunk order
+    for (int i = tid; i < np; i += kFinishThreads) {
+      const float2* st = reinterpret_cast<const float2*>(a.stats + (int64_t)sm_row[i] * a.n_chunks * 2);
+      float M = -INFINITY, Z = 0.f;
+      for (int c0 = 0; c0 < nch; c0 += kFinishBatch) {
+        float2 v[kFinishBatch];
+#pragma unroll
+        for (int u = 0; u < kFinishBatch; ++u) v[u] = c0 + u < nch ? st[c0 + u] : make_float2(-INFINITY, 0.f);
+#pragma unroll
+        for (int u = 0; u < kFinishBatch; ++u) {
+          const float mn = fmaxf(M, v[u].x);
+          const float mu = mn == -INFINITY ? 0.f : mn;
+          Z = Z * fast_exp2(M - mu) + v[u].y * fast_exp2(v[u].x - mu);
+          M = mn;
+        }
+      }
+      sm_M[i] = M == -INFINITY ? 0.f : M;
       sm_iz[i] = Z > 0.f ? 1.f / Z : 0.f;
     }
   }
@@ -278,15 +327,16 @@ __global__ __launch_bounds__(kFinishThreads) void score_finish_pages_kernel(Scor
   const bool live = p < P;
   float acc = 0.f;
   constexpr int kWaves = kFinishThreads / kWave;
-  for (int i0 = wave; i0 < np; i0 += kWaves * kFinishBatch) {
-    float x[kFinishBatch];
+  constexpr int kBatch = 2 * kFinishBatch;  // rows loaded together per lane
+  for (int i0 = wave; i0 < np; i0 += kWaves * kBatch) {
+    float x[kBatch];
 #pragma unroll
-    for (int u = 0; u < kFinishBatch; ++u) {
+    for (int u = 0; u < kBatch; ++u) {
       const int i = i0 + u * kWaves < np ? i0 + u * kWaves : i0;
       x[u] = live ? a.logits[(int64_t)sm_row[i] * a.ld + p] : 0.f;
     }
 #pragma unroll
-    for (int u = 0; u < kFinishBatch; ++u) {
+    for (int u = 0; u < kBatch; ++u) {
       const int i = i0 + u * kWaves;
       if (i < np) acc += fast_exp2(x[u] - sm_M[i]) * sm_iz[i];
     }
@@ -306,26 +356,32 @@ __global__ __launch_bounds__(kFinishThreads) void score_finish_pages_kernel(Scor
   }
 }
 
-hipError_t launch_score(const ScoreArgs& a, int B, int n_used_kv, int row_dim, hipStream_t stream) {
-  dim3 grid1(n_used_kv, a.n_chunks, B * a.n_layers);
+template <int NT>
+hipError_t launch_logits(const ScoreArgs& a, dim3 grid, int row_dim, bool paged, bool pages, hipStream_t stream) {
   const dim3 block(kScoreWaves * kWave);
-  const bool paged = a.k.page_table != nullptr;
-  const bool pages = a.page_mode != 0;
   if (pages) {
     if (paged) return hipErrorInvalidValue;  // page statistics are a contiguous array
-    if (row_dim == 256) hipLaunchKernelGGL((score_logits_kernel<256, false, true>), grid1, block, 0, stream, a);
-    else if (row_dim == 128) hipLaunchKernelGGL((score_logits_kernel<128, false, true>), grid1, block, 0, stream, a);
+    if (row_dim == 256) hipLaunchKernelGGL((score_logits_kernel<256, false, true, NT>), grid, block, 0, stream, a);
+    else if (row_dim == 128) hipLaunchKernelGGL((score_logits_kernel<128, false, true, NT>), grid, block, 0, stream, a);
     else return hipErrorInvalidValue;
   } else if (row_dim == 128) {
-    if (paged) hipLaunchKernelGGL((score_logits_kernel<128, true, false>), grid1, block, 0, stream, a);
-    else hipLaunchKernelGGL((score_logits_kernel<128, false, false>), grid1, block, 0, stream, a);
+    if (paged) hipLaunchKernelGGL((score_logits_kernel<128, true, false, NT>), grid, block, 0, stream, a);
+    else hipLaunchKernelGGL((score_logits_kernel<128, false, false, NT>), grid, block, 0, stream, a);
   } else if (row_dim == 64) {
-    if (paged) hipLaunchKernelGGL((score_logits_kernel<64, true, false>), grid1, block, 0, stream, a);
-    else hipLaunchKernelGGL((score_logits_kernel<64, false, false>), grid1, block, 0, stream, a);
+    if (paged) hipLaunchKernelGGL((score_logits_kernel<64, true, false, NT>), grid, block, 0, stream, a);
+    else hipLaunchKernelGGL((score_logits_kernel<64, false, false, NT>), grid, block, 0, stream, a);
   } else {
     return hipErrorInvalidValue;
   }
-  hipError_t e = hipGetLastError();
+  return hipGetLastError();
+}
+
+hipError_t launch_score(const ScoreArgs& a, int B, int n_groups, int max_group, int row_dim, hipStream_t stream) {
+  const dim3 grid1(n_groups, a.n_chunks, B * a.n_layers);
+  const bool paged = a.k.page_table != nullptr;
+  const bool pages = a.page_mode != 0;
+  hipError_t e = max_group > 1 ? launch_logits<kScoreGroupTiles>(a, grid1, row_dim, paged, pages, stream)
+                               : launch_logits<1>(a, grid1, row_dim, paged, pages, stream);
   if (e != hipSuccess) return e;
   if (pages) {
     const int max_pages = (a.dims.max_len + (1 << a.page_shift) - 1) >> a.page_shift;

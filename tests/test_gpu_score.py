@@ -142,3 +142,16 @@ def test_score_layers_one_layer_is_dustin_score():
     b = D.score_layers([q], [k], seq, heads, init=init, max_len=N)
     torch.cuda.synchronize()
     assert torch.equal(a[:, :, :1000], b[:, :, :1000]) and torch.equal(a[0], b[0])
+
+
+def test_score_twelve_draft_heads_share_a_workgroup():
+    """Dustin-D's 12 draft heads: 24 (head, query) pairs per KV head span two column tiles,
+    which one pass-1 workgroup computes from a single read of each K row."""
+    _case(3, 0, 4, 14, 2, 64, list(range(12)), n_list=[3000, 1025, 40], with_init=True, seed=5)
+    _case(2, 0, 4, 14, 2, 64, list(range(12)), groups=2, n_list=[2100, 700], seed=6)
+
+
+def test_score_all_target_heads():
+    """Every head of a Qwen2.5-72B-shaped layer (the naive estimator's per-layer work):
+    64 heads, 2 queries, 16 pairs per KV head."""
+    _case(2, 0, 2, 64, 8, 128, list(range(64)), n_list=[2000, 555], seed=7)
