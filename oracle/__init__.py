@@ -56,6 +56,10 @@ def _load():
         lib.oracle_page_score.argtypes = [_ptr, _i64, _i64, _i64, _ptr, _i64, _i64, _i64, _i32,
                                           _ptr, _ptr, _i32, _i32, _i32, _i32, _ptr, _i32, _i32,
                                           ctypes.c_double, _ptr, _i64, _i64, _ptr, _i64, _i64]
+        lib.oracle_arr.restype = _i32
+        lib.oracle_arr.argtypes = [_ptr, _i64, _i64, _i64, _ptr, _i64, _i64, _i64, _i32, _ptr, _ptr,
+                                   _i32, _i32, _i32, _i32, ctypes.c_double, _ptr, _i64, _i64, _ptr,
+                                   _ptr, _ptr, _i64, _i64]
         lib.oracle_max_threads.restype = _i32
         lib.oracle_set_threads.argtypes = [_i32]
         _lib = lib
@@ -250,6 +254,39 @@ def arr_window(A, sel):
     A = np.ascontiguousarray(A, dtype=np.float64)
     s = _i32arr(sel)
     return float(_load().oracle_arr_window(_p(A), A.shape[0], A.shape[1], _p(s), len(s)))
+
+
+def arr(q, k, seq_lens, window, scale, groups=1, idx=None, count=None, num_kv_heads=None,
+        with_abar=False, length=None):
+    """Windowed attention recovery rate of the verification window (Eqs. 1-4), averaged over
+    the heads each index set serves.  q: uint16 [B, w_max, Hq, d] (the w_b = window[b] queries);
+    k: uint16 [B, N, Hkv, d]; idx int32 [B, G, >= count], count int32 [B, G] (None: the empty
+    set).  Returns arr float64 [B, G], and with with_abar also A-bar float64 [B, G, length]."""
+    lib = _load()
+    B, _, Hq, d = q.shape
+    Hkv = k.shape[2] if num_kv_heads is None else num_kv_heads
+    _check_inner(q, "q")
+    _check_inner(k, "k")
+    seq = _i32arr(seq_lens, B)
+    wa = _i32arr(window, B)
+    out = np.zeros((B, groups), dtype=np.float64)
+    ab = None
+    if with_abar:
+        n_out = length if length is not None else max(int(seq.max(initial=0)), 1)
+        ab = np.zeros((B, groups, n_out), dtype=np.float64)
+    ix = cn = None
+    if idx is not None:
+        ix = np.ascontiguousarray(idx, dtype=np.int32)
+        cn = np.ascontiguousarray(count, dtype=np.int32)
+    qs, ks = _st(q), _st(k)
+    abs_ = _st(ab) if ab is not None else [0, 0, 0]
+    ixs = _st(ix) if ix is not None else [0, 0, 0]
+    rc = lib.oracle_arr(_p(q), qs[0], qs[1], qs[2], _p(k), ks[0], ks[1], ks[2], B, _p(seq), _p(wa),
+                        Hq, Hkv, d, groups, float(scale), _p(ix), ixs[0], ixs[1], _p(cn), _p(out),
+                        _p(ab), abs_[0], abs_[1])
+    if rc:
+        raise ValueError(f"oracle_arr rejected its arguments ({rc})")
+    return (out, ab) if with_abar else out
 
 
 def overhead_ratio(hd_sel, ld_sel, gamma, ht_sel, lt_sel, hd, ld, ht, lt):

@@ -493,3 +493,97 @@ int oracle_page_score(const uint16_t* q, int64_t q_sb, int64_t q_sj, int64_t q_s
   }
   return rc;
 }
+
+/* -------------------------------------------------------------------------------
+ * Attention recovery rate of the verification window (Eqs. 1-4, the evaluation
+ * framework), with these readings: the valid positions of a verification query are the
+ * committed positions [0, N_b) (the window's own tokens are attended whatever the policy);
+ * the window is the w_b = n_query[b] verification queries; a shared index set is judged
+ * by the mean over the heads it serves (every head when groups == 1, else the heads of KV
+ * head go).  Per (b, go):
+ *   A_{t,h}[n] = softmax_{n < N_b}(scale * q[b, t, h] . K[b, n, g(h)])        (Eq. 1's A)
+ *   ARR_t      = sum_{n in I} A_{t,h}[n]                                        (Eq. 1)
+ *   arr[b, go] = mean over h of (1 / w_b) sum_{t < w_b} ARR_t                   (Eq. 2)
+ *   abar[b, go, n] = mean over h of (1 / w_b) sum_t A_{t,h}[n]                  (Eq. 3's A-bar)
+ * so that the SD oracle's set is TopK_k(abar) and its windowed ARR is the sum of abar over
+ * that set (Eq. 4).  I is idx[b, go, 0 .. count[b, go]); duplicate positions count once.
+ *   arr  : fp64 [B, groups]                      (row-major)
+ *   abar : fp64 [B, groups, >= N_b] or NULL       strides abar_sb, abar_sg
+ * ------------------------------------------------------------------------------- */
+int oracle_arr(const uint16_t* q, int64_t q_sb, int64_t q_sj, int64_t q_sh,
+               const uint16_t* k, int64_t k_sb, int64_t k_sn, int64_t k_sh,
+               int B, const int32_t* seq_lens, const int32_t* n_query,
+               int num_q_heads, int num_kv_heads, int head_dim, int groups, double scale,
+               const int32_t* idx, int64_t idx_sb, int64_t idx_sg, const int32_t* count,
+               double* arr, double* abar, int64_t abar_sb, int64_t abar_sg) {
+  if (!q || !k || !seq_lens || !n_query || !arr || (idx == NULL) != (count == NULL)) return -1;
+  if (B < 0 || num_q_heads <= 0 || num_kv_heads <= 0 || head_dim <= 0) return -1;
+  if (num_q_heads % num_kv_heads) return -2;
+  if (groups != 1 && groups != num_kv_heads) return -3;
+  const int group_size = num_q_heads / num_kv_heads;
+  int rc = 0;
+#pragma omp parallel for collapse(2) schedule(dynamic)
+  for (int b = 0; b < B; ++b) {
+    for (int go = 0; go < groups; ++go) {
+      const int N = seq_lens[b];
+      const int w = n_query[b];
+      arr[b * groups + go] = 0.0;
+      if (N <= 0 || w <= 0) continue;
+      double* a = (double*)malloc((size_t)N * sizeof(double));
+      double* acc = (double*)calloc((size_t)N, sizeof(double));
+      unsigned char* in_set = (unsigned char*)calloc((size_t)N, 1);
+      if (!a || !acc || !in_set) {
+        free(a);
+        free(acc);
+        free(in_set);
+#pragma omp atomic write
+        rc = -9;
+        continue;
+      }
+      if (idx) {
+        const int c = count[b * groups + go];
+        for (int i = 0; i < c; ++i) {
+          const int n = idx[b * idx_sb + go * idx_sg + i];
+          if (n >= 0 && n < N) in_set[n] = 1;
+        }
+      }
+      int nh = 0;
+      double arr_sum = 0.0;
+      for (int h = 0; h < num_q_heads; ++h) {
+        const int g = h / group_size;
+        if (groups != 1 && g != go) continue;
+        ++nh;
+        for (int t = 0; t < w; ++t) {
+          const uint16_t* qv = q + b * q_sb + t * q_sj + h * q_sh;
+          double mx = -INFINITY;
+          for (int n = 0; n < N; ++n) {
+            const uint16_t* kv = k + b * k_sb + (int64_t)n * k_sn + g * k_sh;
+            double dot = 0.0;
+            for (int c = 0; c < head_dim; ++c)
+              dot += oracle_bf16_to_double(qv[c]) * oracle_bf16_to_double(kv[c]);
+            a[n] = scale * dot;
+            if (a[n] > mx) mx = a[n];
+          }
+          double z = 0.0;
+          for (int n = 0; n < N; ++n) z += exp(a[n] - mx);
+          double arr_t = 0.0;
+          for (int n = 0; n < N; ++n) {
+            a[n] = exp(a[n] - mx) / z;
+            acc[n] += a[n];
+            if (in_set[n]) arr_t += a[n];
+          }
+          arr_sum += arr_t;
+        }
+      }
+      arr[b * groups + go] = nh ? arr_sum / ((double)w * nh) : 0.0;
+      if (abar) {
+        double* o = abar + b * abar_sb + go * abar_sg;
+        for (int n = 0; n < N; ++n) o[n] = nh ? acc[n] / ((double)w * nh) : 0.0;
+      }
+      free(a);
+      free(acc);
+      free(in_set);
+    }
+  }
+  return rc;
+}

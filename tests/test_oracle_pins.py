@@ -542,6 +542,79 @@ def test_arr_full_set_is_one_and_oracle_policy_is_upper_bound():
         assert O.arr_window(A, rng.choice(n, k, replace=False)) <= best + 1e-15
 
 
+def _softmax_rows(logits):
+    z = torch.softmax(torch.from_numpy(logits), dim=-1)  # library softmax, fp64
+    return z.numpy()
+
+
+def test_arr_of_qk_matches_library_softmax_and_arr_window():
+    """oracle_arr against the attention rows built with torch.softmax in fp64 and the
+    separately pinned arr_window, per head, then the mean over the heads of each group."""
+    rng = np.random.default_rng(44)
+    B, w, Hq, Hkv, d, N = 2, 3, 4, 2, 8, 40
+    q = rand_bits(rng, (B, w, Hq, d))
+    k = rand_bits(rng, (B, N, Hkv, d))
+    seq, win = [40, 23], [3, 2]
+    idx = np.zeros((B, Hkv, 10), dtype=np.int32)
+    cnt = np.zeros((B, Hkv), dtype=np.int32)
+    for b in range(B):
+        for g in range(Hkv):
+            sel = np.sort(rng.choice(seq[b], 7, replace=False))
+            idx[b, g, :7], cnt[b, g] = sel, 7
+    got, abar = O.arr(q, k, seq, win, 0.3, groups=Hkv, idx=idx, count=cnt, with_abar=True, length=N)
+    qv, kv = val(q), val(k)
+    for b in range(B):
+        n, t = seq[b], win[b]
+        for g in range(Hkv):
+            heads = [h for h in range(Hq) if h // (Hq // Hkv) == g]
+            per_head, mean_rows = [], np.zeros(n)
+            for h in heads:
+                A = _softmax_rows(0.3 * qv[b, :t, h] @ kv[b, :n, g].T)
+                per_head.append(O.arr_window(A, idx[b, g, :cnt[b, g]]))
+                mean_rows += A.mean(0) / len(heads)
+            assert got[b, g] == pytest.approx(np.mean(per_head), abs=1e-12)
+            np.testing.assert_allclose(abar[b, g, :n], mean_rows, atol=1e-14)
+
+
+def test_arr_closed_forms_and_oracle_bound():
+    """The full set recovers everything; the empty set nothing; A-bar sums to one; windowed
+    ARR is linear in the set (sum of A-bar over it); and no set of size k beats TopK_k of
+    A-bar (Eq. 4), checked over every subset of a tiny row."""
+    rng = np.random.default_rng(45)
+    B, w, Hq, Hkv, d, N, k = 1, 4, 2, 1, 8, 9, 3
+    q = rand_bits(rng, (B, w, Hq, d), 2.0)
+    kk = rand_bits(rng, (B, N, Hkv, d))
+    full = np.arange(N, dtype=np.int32).reshape(1, 1, N)
+    one, abar = O.arr(q, kk, [N], [w], 0.5, idx=full, count=[[N]], with_abar=True)
+    assert one[0, 0] == pytest.approx(1.0, abs=1e-12)
+    assert abar[0, 0].sum() == pytest.approx(1.0, abs=1e-12)
+    assert O.arr(q, kk, [N], [w], 0.5)[0, 0] == 0.0
+    best = -1.0
+    for sub in itertools.combinations(range(N), k):
+        ix = np.array(sub, dtype=np.int32).reshape(1, 1, k)
+        v = O.arr(q, kk, [N], [w], 0.5, idx=ix, count=[[k]])[0, 0]
+        assert v == pytest.approx(abar[0, 0, list(sub)].sum(), abs=1e-12)
+        best = max(best, v)
+    top = np.argsort(-abar[0, 0], kind="stable")[:k]
+    assert best == pytest.approx(abar[0, 0, top].sum(), abs=1e-12)
+
+
+def test_arr_dominant_key():
+    """A key aligned with every window query takes nearly all mass: ARR is about 1 with it
+    and about 0 without it."""
+    rng = np.random.default_rng(46)
+    w, d, N = 2, 16, 30
+    qf = rng.standard_normal((1, w, 1, d))
+    kf = rng.standard_normal((1, N, 1, d)) * 0.1
+    kf[0, 11, 0] = 8.0 * qf[0].mean(0)[0]
+    q, kk = bits(qf), bits(kf)
+    with_key = O.arr(q, kk, [N], [w], 1.0, idx=np.array([[[11]]], dtype=np.int32), count=[[1]])[0, 0]
+    others = np.array([[list(range(11)) + list(range(12, N))]], dtype=np.int32)
+    without = O.arr(q, kk, [N], [w], 1.0, idx=others, count=[[N - 1]])[0, 0]
+    assert with_key > 0.999 and without < 1e-3
+    assert with_key + without == pytest.approx(1.0, abs=1e-12)
+
+
 # ----------------------------------------------------------------------------- KV append / commit
 
 def _kv_case(rng, B=3, cap=40, H=2, d=16, T=5):
