@@ -17,7 +17,8 @@
  * dustin_page_meta and dustin_page_score are the page estimator the paper compares its
  * scoring heads with (page-level key minima and maxima; Quest-16 in the estimation
  * overhead analysis): they produce an importance array that step 3 takes in place of,
- * or on top of, S_T.
+ * or on top of, S_T.  dustin_arr measures how much of the window's attention an index set
+ * keeps (attention recovery rate), the paper's fidelity measure of a selection.
  *
  * Conventions shared by every entry point
  *   - All tensor pointers are DEVICE pointers unless a name ends in _host.  The caller
@@ -215,6 +216,28 @@ dustin_status dustin_page_score(const void* q, int64_t q_sb, int64_t q_sj, int64
                                 int32_t page_size, const dustin_batch* bt, float scale, int32_t groups,
                                 const float* init, int64_t init_sb, int64_t init_sg, float* out, int64_t out_sb,
                                 int64_t out_sg, void* workspace, size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------------
+ * dustin_arr -- windowed attention recovery rate of index sets (the evaluation framework,
+ * Eqs. 1-4), averaged over the heads a set serves:
+ *   arr[b, go] = (1 / (w_b * heads_per_group)) * sum_{i < count[b, go]} s[b, go, idx[b, go, i]]
+ * where s is dustin_score's output over every head the set serves (all query heads when
+ * groups == 1, the heads of KV head go otherwise: heads_per_group of them) and the w_b =
+ * n_query[b] queries of the verification window, with init = NULL.  Then
+ * s / (w_b * heads_per_group) is the window- and head-averaged attention A-bar (Eq. 3) over
+ * the committed positions, and, ARR being linear in the weights, arr is the windowed ARR
+ * (Eq. 2) averaged over those heads.  The SD oracle (Eq. 4) is dustin_topk on s with
+ * n_sink = n_window = 0 and m = 0, followed by this call on its set.
+ *   s          fp32 [B, >= groups or 1, >= max_len], strides s_sb, s_sg (0 = one row per b)
+ *   idx, count int32 as dustin_topk writes them: distinct positions; count clamped to
+ *              [0, k_max]; positions outside [0, N_b) are skipped
+ *   bt         seq_lens (N_b), n_query (w_b; NULL = nq_max), k_max
+ *   arr        fp64 [B, groups] (device, row-major, 8-byte aligned)
+ * The sum is taken in fp64 in a fixed order: repeated calls give identical bits.
+ * --------------------------------------------------------------------------------- */
+dustin_status dustin_arr(const float* s, int64_t s_sb, int64_t s_sg, const int32_t* idx, int64_t idx_sb,
+                         int64_t idx_sg, const int32_t* count, const dustin_batch* bt, int32_t groups,
+                         int32_t heads_per_group, double* arr, void* stream);
 
 /* ---------------------------------------------------------------------------------
  * dustin_topk -- tiered hybrid selection, Eq. 6 (hybrid_selection), with the protected

@@ -29,7 +29,7 @@ EXPORTED = ("dustin_status_string", "dustin_version", "dustin_score_workspace", 
             "dustin_topk_workspace", "dustin_topk", "dustin_attn_workspace",
             "dustin_sparse_verify_attn", "dense_verify_attn", "dustin_kv_append", "dustin_kv_commit",
             "dustin_score_layers", "dustin_page_meta", "dustin_page_score_workspace",
-            "dustin_page_score")
+            "dustin_page_score", "dustin_arr")
 
 
 class DustinError(RuntimeError):
@@ -106,6 +106,8 @@ def lib():
         L.dustin_page_score.argtypes = [_vp, _i64, _i64, _i64, _i32, _vp, _i32, _vp, _i64, _i64, _i32,
                                         _i32, _i32, _i32, P_BT, ctypes.c_float, _i32, _vp, _i64, _i64,
                                         _vp, _i64, _i64, _vp, _sz, _vp]
+        L.dustin_arr.restype = ctypes.c_int
+        L.dustin_arr.argtypes = [_vp, _i64, _i64, _vp, _i64, _i64, _vp, P_BT, _i32, _i32, _vp, _vp]
         L.dustin_kv_commit.restype = ctypes.c_int
         L.dustin_kv_commit.argtypes = [_vp, _vp, _vp, _i32, _i32, _vp]
         _lib = L
@@ -373,6 +375,43 @@ def plan_page_score(q: torch.Tensor, meta: torch.Tensor, seq_lens, heads: Sequen
 def page_score(q, meta, seq_lens, heads, page_size, **kw):
     """Page-estimator importance; returns out (positions >= N_b untouched)."""
     return plan_page_score(q, meta, seq_lens, heads, page_size, **kw)()
+
+
+# ----------------------------------------------------------------------------- attention recovery rate
+
+def plan_arr(s: torch.Tensor, idx: torch.Tensor, count: torch.Tensor, seq_lens, heads_per_group: int,
+             *, window=None, max_len: Optional[int] = None, out: Optional[torch.Tensor] = None,
+             stream=None) -> Call:
+    """Prepared dustin_arr: windowed ARR (Eqs. 1-2) of the sets (idx, count) from s, the Eq. 5
+    score over every served head and the window's queries.  Returns fp64 [B, groups]."""
+    _on_gpu(s, idx, count, out)
+    if s.dtype != torch.float32 or s.dim() != 3 or s.stride(2) != 1:
+        raise ValueError("s must be fp32 [B, G or 1, N] with contiguous positions")
+    if idx.dtype != torch.int32 or count.dtype != torch.int32 or idx.stride(2) != 1:
+        raise ValueError("idx / count must be int32 (idx [B, G, k_max] contiguous in k)")
+    B, G, k_max = idx.shape
+    dev = s.device
+    seq = _i32_dev(seq_lens, dev)
+    if window is None:
+        raise ValueError("window: the verification queries per sequence (an int or one per sequence)")
+    if isinstance(window, int):
+        win, w_max = None, int(window)
+    else:
+        win, w_max = _i32_dev(window, dev), 1 << 16
+    count = count.contiguous()
+    max_len = s.shape[2] if max_len is None else int(max_len)
+    if out is None:
+        out = torch.empty((B, G), dtype=torch.float64, device=dev)
+    bt = _batch(B, max_len, w_max, k_max, seq, win)
+    s_sg = s.stride(1) if s.shape[1] > 1 else 0
+    args = (_ptr(s), s.stride(0), s_sg, _ptr(idx), idx.stride(0), idx.stride(1), _ptr(count),
+            ctypes.byref(bt), G, int(heads_per_group), _ptr(out), _stream(stream))
+    return Call(lib().dustin_arr, args, "dustin_arr", (s, idx, count, bt), out)
+
+
+def arr(s, idx, count, seq_lens, heads_per_group, **kw):
+    """Windowed ARR of index sets; returns fp64 [B, groups]."""
+    return plan_arr(s, idx, count, seq_lens, heads_per_group, **kw)()
 
 
 # ----------------------------------------------------------------------------- top-k

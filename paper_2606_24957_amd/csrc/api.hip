@@ -543,6 +543,35 @@ dustin_status dustin_page_score(const void* q, int64_t q_sb, int64_t q_sj, int64
                       out_sb, out_sg, workspace, workspace_bytes, stream);
 }
 
+// ------------------------------------------------------------------ attention recovery rate
+
+dustin_status dustin_arr(const float* s, int64_t s_sb, int64_t s_sg, const int32_t* idx, int64_t idx_sb,
+                         int64_t idx_sg, const int32_t* count, const dustin_batch* bt, int32_t groups,
+                         int32_t heads_per_group, double* arr, void* stream) {
+  if (!batch_ok(bt) || !s || !idx || !count || !arr) return DUSTIN_ERR_INVALID_ARG;
+  if (groups < 1 || groups > 65535 || heads_per_group < 1) return DUSTIN_ERR_INVALID_ARG;
+  if (!aligned(s, 4) || !aligned(idx, 4) || !aligned(count, 4) || !aligned(arr, 8)) return DUSTIN_ERR_INVALID_ARG;
+  if (s_sb < 0 || s_sg < 0 || idx_sb < 0 || idx_sg < 0) return DUSTIN_ERR_INVALID_ARG;
+  const int B = bt->batch;
+  if (B > 65535) return DUSTIN_ERR_UNSUPPORTED;
+  if (B == 0) return DUSTIN_OK;
+  ArrArgs a;
+  memset(&a, 0, sizeof a);
+  a.s = s;
+  a.s_sb = s_sb;
+  a.s_sg = s_sg;
+  a.idx = idx;
+  a.idx_sb = idx_sb;
+  a.idx_sg = idx_sg;
+  a.count = count;
+  a.dims = dims_of(bt);
+  a.groups = groups;
+  a.heads_per_group = heads_per_group;
+  a.arr = arr;
+  const hipError_t e = launch_arr(a, B, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? DUSTIN_OK : DUSTIN_ERR_LAUNCH;
+}
+
 // ------------------------------------------------------------------ top-k
 
 size_t dustin_topk_workspace(int32_t batch, int32_t groups, int32_t max_len) {

@@ -86,6 +86,20 @@ static_assert(sizeof(ScoreArgs) <= 4096, "kernel arguments stay within 4 KiB");
 // tile count; row_dim: length of a K row (head_dim, or 2 * head_dim for page statistics)
 hipError_t launch_score(const ScoreArgs& a, int B, int n_groups, int max_group, int row_dim, hipStream_t stream);
 
+// ---- attention recovery rate (arr.hip) ----
+struct ArrArgs {
+  const float* s;  // Eq. 5 score over the served heads and the window's queries
+  int64_t s_sb, s_sg;
+  const int32_t* idx;
+  int64_t idx_sb, idx_sg;
+  const int32_t* count;
+  SeqDims dims;    // seq_lens (N_b), n_query (w_b), k_max
+  int32_t groups, heads_per_group;
+  double* arr;     // [B, groups]
+};
+
+hipError_t launch_arr(const ArrArgs& a, int B, hipStream_t stream);
+
 // ---- page statistics for the page estimator (page.hip) ----
 constexpr int kMaxPageSize = 4096;
 struct PageMetaArgs {

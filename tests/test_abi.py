@@ -228,3 +228,20 @@ def test_page_score_rejects(L):
     assert _pscore(L, bt=_batch(nq=17)) == D.ERR_UNSUPPORTED
     assert _pscore(L, ws=None, ws_bytes=0) == D.ERR_WORKSPACE
     assert _pscore(L, ws_bytes=64) == D.ERR_WORKSPACE
+
+
+def test_arr_rejects(L):
+    bt = _batch()
+
+    def call(s=FAKE, idx=FAKE, cnt=FAKE, groups=1, hpg=8, out=FAKE, sb=100, b=bt):
+        return L.dustin_arr(s, sb, 0, idx, 40, 40, cnt, ctypes.byref(b) if b else None, groups, hpg, out, None)
+
+    assert call(s=None) == D.ERR_INVALID_ARG
+    assert call(idx=None) == D.ERR_INVALID_ARG
+    assert call(cnt=None) == D.ERR_INVALID_ARG
+    assert call(out=None) == D.ERR_INVALID_ARG
+    assert call(out=FAKE + 4) == D.ERR_INVALID_ARG                    # fp64 output
+    assert call(groups=0) == D.ERR_INVALID_ARG
+    assert call(hpg=0) == D.ERR_INVALID_ARG
+    assert call(sb=-1) == D.ERR_INVALID_ARG
+    assert call(b=None) == D.ERR_INVALID_ARG
