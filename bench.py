@@ -199,6 +199,45 @@ def page_estimator(s, layers, est, seq, nq, bud, steps, warmup, ps=16):
     return rec
 
 
+# ----------------------------------------------------------------------------- selection fidelity
+
+def arr_eval(s, layer, s_t, s_d, idx, cnt, seq, nq, bud, mm):
+    """Windowed attention recovery rate (Eqs. 1-4) of the step's selection and of its
+    variants on the first layer: A-bar from every query head over the 5 verification queries
+    (dustin_score), then dustin_arr per set, averaged over the batch.  Also the event time
+    of one evaluation (A-bar plus the oracle's selection and both ARRs)."""
+    import torch
+    import paper_2606_24957_amd as D
+    N, k, P = s.n_max, s.k_max, s.n_sink + s.n_window
+    heads = list(range(s.num_q_heads))
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    abar = D.score(layer.q, layer.k, seq, heads, n_query=nq, max_len=N, page_table=layer.page_table)
+    oidx, ocnt = D.topk(None, abar, seq, k, budget=bud, n_sink=0, n_window=0, m_scalar=0)
+    orc = D.arr(abar, oidx, ocnt, seq, s.num_q_heads, window=nq)
+    hyb = D.arr(abar, idx, cnt, seq, s.num_q_heads, window=nq)
+    e1.record()
+    torch.cuda.synchronize()
+    eval_us = e0.elapsed_time(e1) * 1e3
+    res = {"sd_oracle": orc, "dustin": hyb}
+    ti, tc = D.topk(None, s_t, seq, k, budget=bud, m_scalar=0, n_sink=s.n_sink, n_window=s.n_window)
+    res["dustin_t"] = D.arr(abar, ti, tc, seq, s.num_q_heads, window=nq)
+    di, dc = D.topk(s_d, None, seq, k, budget=bud, n_sink=s.n_sink, n_window=s.n_window)
+    res["dustin_d"] = D.arr(abar, di, dc, seq, s.num_q_heads, window=nq)
+    if len(set(s.budget)) == 1:  # StreamingLLM-like: the whole budget on sinks and the recent window
+        si, sc = D.topk(None, s_t, seq, k, budget=bud, m_scalar=0, n_sink=s.n_sink, n_window=k - s.n_sink)
+        res["sinks_and_recent"] = D.arr(abar, si, sc, seq, s.num_q_heads, window=nq)
+    torch.cuda.synchronize()
+    rec = {name: round(float(v.mean()), 5) for name, v in res.items()}
+    rec["eval_us"] = round(eval_us, 1)
+    rec["budget_k"] = k
+    log(f"[bench] windowed ARR at k={k} (mean over the batch): " +
+        ", ".join(f"{n} {v:.4f}" for n, v in rec.items() if n not in ("eval_us", "budget_k")) +
+        f"; evaluation {eval_us:.0f} us")
+    del abar
+    return rec
+
+
 # ----------------------------------------------------------------------------- CPU baseline
 
 def cpu_baseline(s, layer0, est, n_seq):
@@ -432,6 +471,10 @@ def main():
             vstep = {"error": str(exc)[:200]}
             log(f"[bench] verify step graph: {exc}")
 
+    fidelity = None
+    if args.only == "all":
+        fidelity = arr_eval(s, layers[0], s_t, s_d, idx, cnt, seq, nq, bud, mm)
+
     page = None
     if args.only in ("all", "page"):
         page = page_estimator(s, layers, est, seq, nq, bud, args.steps, args.warmup)
@@ -488,6 +531,7 @@ def main():
         },
         "verify_step": vstep,
         "page_estimator": page,
+        "selection_arr": fidelity,
         "cpu_baseline": cpu,
     }
     print(json.dumps(rec), flush=True)
