@@ -238,6 +238,50 @@ def arr_eval(s, layer, s_t, s_d, idx, cnt, seq, nq, bud, mm):
     return rec
 
 
+# ----------------------------------------------------------------------------- SpecAttn-style step
+
+def per_layer_selection(s, layers, dev, steps, warmup, sparse_us, dense_us, dustin_est_us, draft_layers=24):
+    """The per-layer, all-draft-head selection of the paper's SpecAttn comparison: relevance
+    from all 14 heads of each of the draft model's 24 layers (synthetic, planted like the
+    draft scoring layers), one index set per draft layer, target layers matched by depth.
+    Its estimation (the per-layer scores and the top-k) is timed with events; per-step
+    speedups use the sparse and dense per-layer times measured above."""
+    import torch
+    from paper_2606_24957_amd import step as S
+    from paper_2606_24957_amd import workloads as W
+    s24 = s.replace(draft=W.DraftShape(layers=draft_layers))
+    est24 = W.make_estimation(s24, layers[0], dev)
+    st = S.PerLayerSelectionStep(s24, layers, est24, dev, n_target=80)
+    for _ in range(warmup):
+        st.run()
+    torch.cuda.synchronize()
+    e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+    e0.record()
+    for _ in range(steps):
+        st.ops[0]()
+        st.ops[1]()
+    e1.record()
+    for _ in range(steps):
+        st.run()
+    e2.record()
+    torch.cuda.synchronize()
+    est_us = e0.elapsed_time(e1) * 1e3 / steps
+    step_us = e1.elapsed_time(e2) * 1e3 / steps
+    rec = {
+        "draft_layers": draft_layers, "draft_heads": s.draft.num_q_heads,
+        "estimation_us_per_step": round(est_us, 1),
+        f"step_us_L{len(layers)}": round(step_us, 1),
+        "per_step_speedup_L80": round(80 * dense_us / (est_us + 80 * sparse_us), 3),
+        "dustin_per_step_speedup_L80": round(80 * dense_us / (dustin_est_us + 80 * sparse_us), 3),
+    }
+    log(f"[bench] per-layer all-draft-head selection ({draft_layers} draft layers x "
+        f"{s.draft.num_q_heads} heads): estimation {est_us:.0f} us/step, step over {len(layers)} layers "
+        f"{step_us:.0f} us; per-step speedup at L=80 {rec['per_step_speedup_L80']}x vs Dustin "
+        f"{rec['dustin_per_step_speedup_L80']}x")
+    del st, est24
+    return rec
+
+
 # ----------------------------------------------------------------------------- CPU baseline
 
 def cpu_baseline(s, layer0, est, n_seq):
@@ -471,6 +515,14 @@ def main():
             vstep = {"error": str(exc)[:200]}
             log(f"[bench] verify step graph: {exc}")
 
+    per_layer = None
+    if args.only == "all" and s.draft is not None:
+        try:
+            per_layer = per_layer_selection(s, layers, dev, args.steps, args.warmup, sp_us, dn_us, est_us)
+        except Exception as exc:  # reported, not fatal
+            per_layer = {"error": str(exc)[:200]}
+            log(f"[bench] per-layer selection: {exc}")
+
     fidelity = None
     if args.only == "all":
         fidelity = arr_eval(s, layers[0], s_t, s_d, idx, cnt, seq, nq, bud, mm)
@@ -532,6 +584,7 @@ def main():
         "verify_step": vstep,
         "page_estimator": page,
         "selection_arr": fidelity,
+        "per_layer_selection": per_layer,
         "cpu_baseline": cpu,
     }
     print(json.dumps(rec), flush=True)

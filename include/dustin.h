@@ -146,7 +146,7 @@ dustin_status dustin_score(const void* q, int64_t q_sb, int64_t q_sj, int64_t q_
  * in two launches whatever n_layers is.  The layers share every shape and stride:
  *   q_layers_host  host array of n_layers device pointers, each laid out as q above
  *   k_layers_host  host array of n_layers dustin_kv that differ only in `data`
- *   1 <= n_layers <= 8; n_layers * n_heads * nq_max <= 1024; batch * n_layers <= 65535
+ *   1 <= n_layers <= 32; n_layers * n_heads * nq_max <= 1024; batch * n_layers <= 65535
  *   workspace  dustin_score_workspace(batch, max_len, nq_max, n_heads * n_layers) bytes
  * Every other argument is as for dustin_score.  The sum over layers is accumulated in
  * fp32 together with the heads' and queries' terms and rounded once at the end.
@@ -158,6 +158,25 @@ dustin_status dustin_score_layers(int32_t n_layers, const void* const* q_layers_
                                   int32_t groups, const float* init, int64_t init_sb, int64_t init_sg,
                                   float* out, int64_t out_sb, int64_t out_sg, void* workspace,
                                   size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------------
+ * dustin_score_per_layer -- Eq. 5 for n_layers layers in two launches, each layer into
+ * its own output: the per-layer, per-head relevance of the SpecAttn-style selection the
+ * paper compares with (appendix on SpecAttn: every draft layer and head scores tokens for
+ * its own target layers, with no aggregation across layers).
+ *   out[l, b, go, n] = sum_{h in heads of go} sum_{j < nq_b} softmax_{n' < N_b}(scale * q_l[b, j, h] . K_l[b, n', g(h)])[n]
+ * for n < N_b, written at out + l * out_sl + b * out_sb + go * out_sg (fp32, elements).
+ * There is no init.  1 <= n_layers <= 32; n_heads * nq_max <= 1024; batch * n_layers <=
+ * 65535; groups * n_layers <= 65535; workspace as for dustin_score_layers.  Every other
+ * argument is as for dustin_score_layers.  Each layer's output has the same bits as a
+ * dustin_score call on that layer alone.
+ * --------------------------------------------------------------------------------- */
+dustin_status dustin_score_per_layer(int32_t n_layers, const void* const* q_layers_host, int64_t q_sb,
+                                     int64_t q_sj, int64_t q_sh, int32_t num_q_heads,
+                                     const int32_t* heads_host, int32_t n_heads,
+                                     const dustin_kv* k_layers_host, const dustin_batch* bt, float scale,
+                                     int32_t groups, float* out, int64_t out_sl, int64_t out_sb,
+                                     int64_t out_sg, void* workspace, size_t workspace_bytes, void* stream);
 
 /* ---------------------------------------------------------------------------------
  * dustin_page_meta -- page statistics of the page estimator.  The paper describes it

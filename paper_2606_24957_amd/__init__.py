@@ -29,7 +29,7 @@ EXPORTED = ("dustin_status_string", "dustin_version", "dustin_score_workspace", 
             "dustin_topk_workspace", "dustin_topk", "dustin_attn_workspace",
             "dustin_sparse_verify_attn", "dense_verify_attn", "dustin_kv_append", "dustin_kv_commit",
             "dustin_score_layers", "dustin_page_meta", "dustin_page_score_workspace",
-            "dustin_page_score", "dustin_arr")
+            "dustin_page_score", "dustin_arr", "dustin_score_per_layer")
 
 
 class DustinError(RuntimeError):
@@ -106,6 +106,9 @@ def lib():
         L.dustin_page_score.argtypes = [_vp, _i64, _i64, _i64, _i32, _vp, _i32, _vp, _i64, _i64, _i32,
                                         _i32, _i32, _i32, P_BT, ctypes.c_float, _i32, _vp, _i64, _i64,
                                         _vp, _i64, _i64, _vp, _sz, _vp]
+        L.dustin_score_per_layer.restype = ctypes.c_int
+        L.dustin_score_per_layer.argtypes = [_i32, _vp, _i64, _i64, _i64, _i32, _vp, _i32, P_KV, P_BT,
+                                             ctypes.c_float, _i32, _vp, _i64, _i64, _i64, _vp, _sz, _vp]
         L.dustin_arr.restype = ctypes.c_int
         L.dustin_arr.argtypes = [_vp, _i64, _i64, _vp, _i64, _i64, _vp, P_BT, _i32, _i32, _vp, _vp]
         L.dustin_kv_commit.restype = ctypes.c_int
@@ -298,6 +301,48 @@ def plan_score_layers(qs: Sequence[torch.Tensor], ks: Sequence[torch.Tensor], se
 def score_layers(qs, ks, seq_lens, heads, **kw):
     """Eq. 5 summed over layers; returns out (positions >= N_b untouched)."""
     return plan_score_layers(qs, ks, seq_lens, heads, **kw)()
+
+
+def plan_score_per_layer(qs: Sequence[torch.Tensor], ks: Sequence[torch.Tensor], seq_lens,
+                         heads: Sequence[int], *, n_query=None, scale: Optional[float] = None,
+                         groups: int = 1, out: Optional[torch.Tensor] = None,
+                         max_len: Optional[int] = None, page_table: Optional[torch.Tensor] = None,
+                         stream=None) -> Call:
+    """Prepared dustin_score_per_layer: Eq. 5 of each layer (qs[l], ks[l]) into out[l]
+    (fp32 [L, B, groups, max_len]), in two launches."""
+    if len(qs) != len(ks) or not qs:
+        raise ValueError("one query tensor per cache, at least one layer")
+    _on_gpu(*qs, *ks, out, page_table)
+    q0 = qs[0]
+    B, nq_max, Hq, d = q0.shape
+    for q in qs:
+        if q.shape != q0.shape or q.stride() != q0.stride() or q.dtype != q0.dtype:
+            raise ValueError("the layers' queries must share shape and strides")
+    dev = q0.device
+    seq = _i32_dev(seq_lens, dev)
+    nqa = _i32_dev(n_query, dev)
+    kvs = (DustinKV * len(ks))()
+    for i, k in enumerate(ks):
+        kvs[i] = kv_view(k, page_table)
+    max_len = _capacity(kvs[0]) if max_len is None else int(max_len)
+    if out is None:
+        out = torch.empty((len(qs), B, groups, max_len), dtype=torch.float32, device=dev)
+    heads_host = (ctypes.c_int32 * len(heads))(*[int(h) for h in heads])
+    q_host = (ctypes.c_void_p * len(qs))(*[q.data_ptr() for q in qs])
+    bt = _batch(B, max_len, nq_max, 0, seq, nqa)
+    nbytes = lib().dustin_score_workspace(B, max_len, nq_max, len(heads) * len(qs))
+    ws = workspace(nbytes, dev, "score")
+    scale = 1.0 / math.sqrt(d) if scale is None else scale
+    args = (len(qs), q_host, q0.stride(0), q0.stride(1), q0.stride(2), Hq, heads_host, len(heads),
+            kvs, ctypes.byref(bt), float(scale), int(groups), _ptr(out), out.stride(0), out.stride(1),
+            out.stride(2), _ptr(ws), nbytes, _stream(stream))
+    return Call(lib().dustin_score_per_layer, args, "dustin_score_per_layer",
+                (tuple(qs), tuple(ks), kvs, bt, ws, heads_host, q_host), out)
+
+
+def score_per_layer(qs, ks, seq_lens, heads, **kw):
+    """Eq. 5 of each layer into its own output; returns out [L, B, groups, max_len]."""
+    return plan_score_per_layer(qs, ks, seq_lens, heads, **kw)()
 
 
 # ----------------------------------------------------------------------------- page estimator

@@ -347,7 +347,8 @@ dustin_status run_score(int32_t n_layers, const void* const* q_layers, int64_t q
                         int64_t q_sh, int32_t num_q_heads, const int32_t* heads_host, int32_t n_heads,
                         const dustin_kv* k_layers, const dustin_batch* bt, float scale, int32_t groups,
                         const float* init, int64_t init_sb, int64_t init_sg, float* out, int64_t out_sb,
-                        int64_t out_sg, void* workspace, size_t workspace_bytes, void* stream) {
+                        int64_t out_sg, void* workspace, size_t workspace_bytes, void* stream,
+                        bool per_layer = false, int64_t out_sl = 0) {
   if (!batch_ok(bt) || !q_layers || !k_layers || !out || !heads_host) return DUSTIN_ERR_INVALID_ARG;
   if (n_layers < 1 || n_layers > kScoreMaxLayers) return DUSTIN_ERR_UNSUPPORTED;
   if (!isfinite(scale)) return DUSTIN_ERR_INVALID_ARG;
@@ -358,7 +359,8 @@ dustin_status run_score(int32_t n_layers, const void* const* q_layers, int64_t q
   if (k->head_dim != 64 && k->head_dim != 128) return DUSTIN_ERR_UNSUPPORTED;
   if (groups != 1 && groups != Hkv) return DUSTIN_ERR_INVALID_ARG;
   if (bt->nq_max < 1 || bt->nq_max > 16) return DUSTIN_ERR_UNSUPPORTED;
-  if ((int64_t)n_layers * n_heads * bt->nq_max > kScoreMaxPairs) return DUSTIN_ERR_UNSUPPORTED;
+  if ((int64_t)(per_layer ? 1 : n_layers) * n_heads * bt->nq_max > kScoreMaxPairs) return DUSTIN_ERR_UNSUPPORTED;
+  if (per_layer && (init || out_sl < 0)) return DUSTIN_ERR_INVALID_ARG;
   for (int l = 0; l < n_layers; ++l) {
     if (!q_layers[l] || !rows_aligned(q_layers[l], q_sb, q_sj, q_sh)) return DUSTIN_ERR_INVALID_ARG;
     const dustin_kv* kl = &k_layers[l];
@@ -397,6 +399,9 @@ dustin_status run_score(int32_t n_layers, const void* const* q_layers, int64_t q
   a.k = kv;
   a.dims = dims_of(bt);
   a.chunk = kScoreChunk;
+  a.per_layer = per_layer ? 1 : 0;
+  a.out_sl = out_sl;
+  if ((int64_t)groups * (per_layer ? n_layers : 1) > 65535) return DUSTIN_ERR_UNSUPPORTED;
   return score_launch(a, n_groups, max_group, k->head_dim, B, bt->nq_max, bt->max_len, scale, groups, init, init_sb,
                       init_sg, out, out_sb, out_sg, workspace, workspace_bytes, stream);
 }
@@ -430,6 +435,17 @@ dustin_status dustin_score_layers(int32_t n_layers, const void* const* q_layers_
   return run_score(n_layers, q_layers_host, q_sb, q_sj, q_sh, num_q_heads, heads_host, n_heads, k_layers_host,
                    bt, scale, groups, init, init_sb, init_sg, out, out_sb, out_sg, workspace, workspace_bytes,
                    stream);
+}
+
+dustin_status dustin_score_per_layer(int32_t n_layers, const void* const* q_layers_host, int64_t q_sb,
+                                     int64_t q_sj, int64_t q_sh, int32_t num_q_heads,
+                                     const int32_t* heads_host, int32_t n_heads,
+                                     const dustin_kv* k_layers_host, const dustin_batch* bt, float scale,
+                                     int32_t groups, float* out, int64_t out_sl, int64_t out_sb,
+                                     int64_t out_sg, void* workspace, size_t workspace_bytes, void* stream) {
+  return run_score(n_layers, q_layers_host, q_sb, q_sj, q_sh, num_q_heads, heads_host, n_heads, k_layers_host,
+                   bt, scale, groups, nullptr, 0, 0, out, out_sb, out_sg, workspace, workspace_bytes, stream,
+                   true, out_sl);
 }
 
 // ------------------------------------------------------------------ page estimator

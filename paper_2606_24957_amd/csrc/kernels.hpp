@@ -46,7 +46,7 @@ constexpr int kScoreFinishPages = 64;    // pages per pass-2 workgroup in page m
 constexpr int kScoreMaxHeads = 64;
 constexpr int kScoreMaxEntries = 64;     // pass-1 column tiles: (KV head, up to 16 pairs)
 constexpr int kScoreGroupTiles = 3;      // column tiles of one KV head per pass-1 workgroup
-constexpr int kScoreMaxLayers = 8;
+constexpr int kScoreMaxLayers = 32;
 constexpr int kScoreMaxPairs = 1024;     // (layer, head, query) rows one output sums
 
 // Eq. 5 over the positions of a cache, or (page mode) over the pages of a page-statistics
@@ -75,6 +75,8 @@ struct ScoreArgs {
   int64_t init_sb, init_sg;
   float* out;
   int64_t out_sb, out_sg;
+  int32_t per_layer;  // 1: layer l writes out + l * out_sl (no init); 0: layers summed
+  int64_t out_sl;
   float* logits;  // [n_layers, B, n_heads, nq_max, ld]  scaled logits, log2 domain
   float* stats;   // [n_layers, B, n_heads, nq_max, n_chunks, 2]  (max, sum of exp2) per chunk
   int64_t ld;

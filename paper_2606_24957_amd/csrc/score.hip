@@ -15,6 +15,7 @@
 // Pass 2 (score_finish_kernel): per (chunk, output group, sequence): merge the chunk
 //   statistics of every pair into its softmax normaliser, then
 //   out[n] = init[n] + sum_pairs exp2(logit - M) / Z, pairs in (layer, head, query) order.
+//   With per-layer outputs each layer's pairs go to that layer's own output row instead.
 //   Page mode (score_finish_pages_kernel): the same sum per page, written to every
 //   position of the page.
 #include "kernels.hpp"
@@ -195,10 +196,11 @@ constexpr int kFinishThreads = 256;
 constexpr int kFinishBatch = 8;  // logits rows loaded together per thread
 
 // The (layer, head slot, query) rows that output group go of sequence b sums, in that
-// order, with each row's softmax max M (log2 domain) and 1 / Z merged from the pass-1
-// chunk statistics.  Returns the number of rows.
-__device__ int finish_setup(const ScoreArgs& a, int b, int go, int nq, int n_rows, int* sm_row, float* sm_M,
-                            float* sm_iz, int* sm_slots, int* sm_ns) {
+// order (every layer, or layer lo alone when each layer has its own output), with each
+// row's softmax max M (log2 domain) and 1 / Z merged from the pass-1 chunk statistics.
+// Returns the number of rows.
+__device__ int finish_setup(const ScoreArgs& a, int b, int go, int lo, int nq, int n_rows, int* sm_row,
+                            float* sm_M, float* sm_iz, int* sm_slots, int* sm_ns) {
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
   if (tid == 0) {
     int ns = 0;
@@ -207,9 +209,10 @@ __device__ int finish_setup(const ScoreArgs& a, int b, int go, int nq, int n_row
     *sm_ns = ns;
   }
   __syncthreads();
-  const int ns = *sm_ns, per_layer = ns * nq, np = a.n_layers * per_layer;
+  const int ns = *sm_ns, per_layer = ns * nq;
+  const int l0 = a.per_layer ? lo : 0, np = (a.per_layer ? 1 : a.n_layers) * per_layer;
   for (int i = tid; i < np; i += kFinishThreads) {
-    const int l = i / per_layer, r = i - l * per_layer, s = r / nq, j = r - s * nq;
+    const int l = l0 + i / per_layer, r = i % per_layer, s = r / nq, j = r - s * nq;
     sm_row[i] = ((l * a.batch + b) * a.n_heads + sm_slots[s]) * a.nq_max + j;
   }
   __syncthreads();
@@ -257,7 +260,7 @@ __device__ int finish_setup(const ScoreArgs& a, int b, int go, int nq, int n_row
 }
 
 __global__ __launch_bounds__(kFinishThreads) void score_finish_kernel(ScoreArgs a) {
-  const int chunk = blockIdx.x, go = blockIdx.y, b = blockIdx.z;
+  const int chunk = blockIdx.x, go = blockIdx.y % a.groups, lo = blockIdx.y / a.groups, b = blockIdx.z;
   const int tid = threadIdx.x;
   const int N = a.dims.len(b);
   const int nq = a.dims.nq(b);
@@ -268,7 +271,7 @@ __global__ __launch_bounds__(kFinishThreads) void score_finish_kernel(ScoreArgs 
   __shared__ float sm_M[kScoreMaxPairs], sm_iz[kScoreMaxPairs];
   __shared__ int sm_slots[kScoreMaxHeads];
   __shared__ int sm_ns;
-  const int np = finish_setup(a, b, go, nq, N, sm_row, sm_M, sm_iz, sm_slots, &sm_ns);
+  const int np = finish_setup(a, b, go, lo, nq, N, sm_row, sm_M, sm_iz, sm_slots, &sm_ns);
 
   // four consecutive positions per thread (the logits rows are 64-element aligned, so
   // the vector load stays inside a row even past N)
@@ -292,7 +295,7 @@ __global__ __launch_bounds__(kFinishThreads) void score_finish_kernel(ScoreArgs 
     }
   }
   const float* init_row = a.init ? a.init + (int64_t)b * a.init_sb + (int64_t)go * a.init_sg : nullptr;
-  float* out_row = a.out + (int64_t)b * a.out_sb + (int64_t)go * a.out_sg;
+  float* out_row = a.out + (int64_t)b * a.out_sb + (int64_t)go * a.out_sg + (int64_t)lo * a.out_sl;
   if (n0 + 3 < N && aligned16(out_row + n0) && (!init_row || aligned16(init_row + n0))) {
     const f32x4 in = init_row ? *reinterpret_cast<const f32x4*>(init_row + n0) : f32x4{0.f, 0.f, 0.f, 0.f};
     *reinterpret_cast<f32x4*>(out_row + n0) = in + acc;
@@ -307,7 +310,7 @@ __global__ __launch_bounds__(kFinishThreads) void score_finish_kernel(ScoreArgs 
 // lane's page, the four partial sums are added in wave order, and every position of the
 // page below N_b receives init + the page's sum.
 __global__ __launch_bounds__(kFinishThreads) void score_finish_pages_kernel(ScoreArgs a) {
-  const int chunk = blockIdx.x, go = blockIdx.y, b = blockIdx.z;
+  const int chunk = blockIdx.x, go = blockIdx.y % a.groups, lo = blockIdx.y / a.groups, b = blockIdx.z;
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
   const int N = a.dims.len(b);
   const int P = score_rows(a, b);
@@ -320,7 +323,7 @@ __global__ __launch_bounds__(kFinishThreads) void score_finish_pages_kernel(Scor
   __shared__ int sm_slots[kScoreMaxHeads];
   __shared__ int sm_ns;
   __shared__ float sm_acc[kFinishThreads / kWave][kScoreFinishPages];
-  const int np = finish_setup(a, b, go, nq, P, sm_row, sm_M, sm_iz, sm_slots, &sm_ns);
+  const int np = finish_setup(a, b, go, lo, nq, P, sm_row, sm_M, sm_iz, sm_slots, &sm_ns);
 
   static_assert(kScoreFinishPages == kWave, "one page per lane");
   const int p = p0 + lane;
@@ -345,7 +348,7 @@ __global__ __launch_bounds__(kFinishThreads) void score_finish_pages_kernel(Scor
   __syncthreads();
 
   const float* init_row = a.init ? a.init + (int64_t)b * a.init_sb + (int64_t)go * a.init_sg : nullptr;
-  float* out_row = a.out + (int64_t)b * a.out_sb + (int64_t)go * a.out_sg;
+  float* out_row = a.out + (int64_t)b * a.out_sb + (int64_t)go * a.out_sg + (int64_t)lo * a.out_sl;
   const int n_end = min(N, (p0 + kScoreFinishPages) << a.page_shift);
   for (int n = (p0 << a.page_shift) + tid; n < n_end; n += kFinishThreads) {
     const int pp = (n >> a.page_shift) - p0;
@@ -383,12 +386,13 @@ hipError_t launch_score(const ScoreArgs& a, int B, int n_groups, int max_group, 
   hipError_t e = max_group > 1 ? launch_logits<kScoreGroupTiles>(a, grid1, row_dim, paged, pages, stream)
                                : launch_logits<1>(a, grid1, row_dim, paged, pages, stream);
   if (e != hipSuccess) return e;
+  const int outs = a.per_layer ? a.n_layers : 1;  // outputs per (group, sequence)
   if (pages) {
     const int max_pages = (a.dims.max_len + (1 << a.page_shift) - 1) >> a.page_shift;
-    dim3 grid2((max_pages + kScoreFinishPages - 1) / kScoreFinishPages, a.groups, B);
+    dim3 grid2((max_pages + kScoreFinishPages - 1) / kScoreFinishPages, a.groups * outs, B);
     hipLaunchKernelGGL(score_finish_pages_kernel, grid2, dim3(kFinishThreads), 0, stream, a);
   } else {
-    dim3 grid2((a.dims.max_len + kScoreFinishChunk - 1) / kScoreFinishChunk, a.groups, B);
+    dim3 grid2((a.dims.max_len + kScoreFinishChunk - 1) / kScoreFinishChunk, a.groups * outs, B);
     hipLaunchKernelGGL(score_finish_kernel, grid2, dim3(kFinishThreads), 0, stream, a);
   }
   return hipGetLastError();

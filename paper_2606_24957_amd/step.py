@@ -9,7 +9,7 @@ from typing import List, Optional
 
 import torch
 
-from . import (plan_kv_append, plan_kv_commit, plan_score, plan_score_layers,
+from . import (plan_kv_append, plan_kv_commit, plan_score, plan_score_layers, plan_score_per_layer,
                plan_sparse_verify_attn, plan_topk)
 
 
@@ -93,3 +93,54 @@ class VerifyStep:
     def commit(self, accepted: torch.Tensor):
         """After verification: N_b += accepted_b (clamped to [0, T_b])."""
         plan_kv_commit(self.seq, accepted, n_query=self.nq, nq_max=self.s.t_max)()
+
+
+def draft_layer_of(layer: int, n_target: int, n_draft: int) -> int:
+    """The draft layer whose relevance selects the tokens of target layer `layer`: layers
+    matched by depth, target layer l to draft layer floor(l * n_draft / n_target)."""
+    return min(n_draft - 1, layer * n_draft // n_target)
+
+
+class PerLayerSelectionStep:
+    """The SpecAttn-style step the paper compares with (appendix on SpecAttn): token relevance
+    from every head of every draft layer, one index set per draft layer (no aggregation
+    across layers), each target layer attending with the set of its depth-matched draft
+    layer.  Launches: the per-layer draft scores (two), one top-k over (draft layer, sequence)
+    rows, then per target layer the sparse attention.  est holds the draft model's layers
+    (draft_q, draft_k); n_target is the target model's depth for the layer matching."""
+
+    def __init__(self, s, layers, est, device, n_target: Optional[int] = None):
+        self.s, self.layers, self.est = s, layers, est
+        i32 = lambda x: torch.tensor(list(x), dtype=torch.int32, device=device)
+        self.seq, self.nq, self.gam = i32(s.seq_lens), i32(s.n_query), i32(s.draft_gamma)
+        self.bud = i32(s.budget)
+        Ld, B, N = len(est.draft_q), s.B, s.n_max
+        self.n_draft = Ld
+        self.n_target = len(layers) if n_target is None else n_target
+        # selection rows are (draft layer, sequence), layer-major: layer j's sets and counts
+        # are the contiguous rows [j B, (j + 1) B)
+        self.seq_rows, self.bud_rows = self.seq.repeat(Ld), self.bud.repeat(Ld)
+        self.rel = torch.zeros((Ld, B, 1, N), dtype=torch.float32, device=device)
+        self.idx = torch.zeros((Ld * B, 1, s.k_max), dtype=torch.int32, device=device)
+        self.cnt = torch.zeros((Ld * B, 1), dtype=torch.int32, device=device)
+        self.outs = [torch.empty_like(l.q) for l in layers]
+        self.ops = self._plan()
+
+    def _plan(self) -> List:
+        s, est, N, B = self.s, self.est, self.s.n_max, self.s.B
+        heads = list(range(s.draft.num_q_heads))
+        ops = [plan_score_per_layer(est.draft_q, est.draft_k, self.seq, heads, n_query=self.gam,
+                                    out=self.rel, max_len=N)]
+        ops.append(plan_topk(self.rel.view(self.n_draft * B, 1, N), None, self.seq_rows, s.k_max,
+                             budget=self.bud_rows, n_sink=s.n_sink, n_window=s.n_window,
+                             idx=self.idx, count=self.cnt))
+        for i, (L, o) in enumerate(zip(self.layers, self.outs)):
+            j = draft_layer_of(i, self.n_target, self.n_draft)
+            ops.append(plan_sparse_verify_attn(L.q, L.k, L.v, self.idx[j * B:(j + 1) * B],
+                                               self.cnt[j * B:(j + 1) * B], self.seq, n_query=self.nq,
+                                               page_table=L.page_table, out=o))
+        return ops
+
+    def run(self):
+        for op in self.ops:
+            op()

@@ -97,3 +97,39 @@ def test_graph_replays_match_the_eager_step(preset):
         for o, oref in zip(st.outs, ref[0]):
             for b, t in enumerate(s.n_query):
                 assert torch.equal(o[b, :t].view(torch.int16), oref[b, :t].view(torch.int16)), f"replay {r}"
+
+
+def test_per_layer_selection_step():
+    """The SpecAttn-style step: draft layer j's relevance is dustin_score over all 14 draft
+    heads of that layer (bit-identical), its index set is the oracle's Eq. 6 selection on that
+    relevance with the draft tier only (bit-exact), and target layer i attends with the set of
+    draft layer floor(i * L_d / L_t)."""
+    s = W.config("qwen7b").replace(layers=4, draft=W.DraftShape(layers=6))
+    layers = [W.make_layer(s, l, DEV) for l in range(s.layers)]
+    est = W.make_estimation(s, layers[0], DEV)
+    st = S.PerLayerSelectionStep(s, layers, est, DEV, n_target=12)
+    st.run()
+    torch.cuda.synchronize()
+    B, N = s.B, s.n_max
+    seq = torch.tensor(s.seq_lens, dtype=torch.int32, device=DEV)
+    gam = torch.tensor(s.draft_gamma, dtype=torch.int32, device=DEV)
+    nq = torch.tensor(s.n_query, dtype=torch.int32, device=DEV)
+    for j in range(6):
+        one = D.score(est.draft_q[j], est.draft_k[j], seq, list(range(14)), n_query=gam, max_len=N)
+        torch.cuda.synchronize()
+        for b, n in enumerate(s.seq_lens):
+            assert torch.equal(st.rel[j, b, 0, :n], one[b, 0, :n]), f"layer {j} b={b}"
+        rel = st.rel[j].cpu().numpy()
+        ri, rc = O.select(rel, None, s.seq_lens, s.k_max, budget=s.budget, m_scalar=s.k_max - 20)
+        for b in range(B):
+            c = int(st.cnt[j * B + b, 0])
+            assert c == int(rc[b, 0]), f"layer {j} b={b}"
+            np.testing.assert_array_equal(st.idx[j * B + b, 0, :c].cpu().numpy(), ri[b, 0, :c])
+    for i, L in enumerate(layers):
+        j = S.draft_layer_of(i, 12, 6)
+        assert j == i * 6 // 12
+        ref = D.sparse_verify_attn(L.q, L.k, L.v, st.idx[j * B:(j + 1) * B], st.cnt[j * B:(j + 1) * B], seq,
+                                   n_query=nq)
+        torch.cuda.synchronize()
+        for b, t in enumerate(s.n_query):
+            assert torch.equal(st.outs[i][b, :t].view(torch.int16), ref[b, :t].view(torch.int16)), f"layer {i}"

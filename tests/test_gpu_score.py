@@ -155,3 +155,26 @@ def test_score_all_target_heads():
     """Every head of a Qwen2.5-72B-shaped layer (the naive estimator's per-layer work):
     64 heads, 2 queries, 16 pairs per KV head."""
     _case(2, 0, 2, 64, 8, 128, list(range(64)), n_list=[2000, 555], seed=7)
+
+
+@pytest.mark.parametrize("groups", [1, 2])
+def test_score_per_layer_outputs_equal_single_layer_calls(groups):
+    """dustin_score_per_layer: every layer into its own row, bit-identical to dustin_score
+    on that layer alone (all 14 draft heads x 4 queries: two column tiles per KV head); one
+    layer also against the oracle."""
+    B, N, nq, Hq, Hkv, d = 2, 2500, 4, 14, 2, 64
+    heads = list(range(Hq))
+    g = torch.Generator(device=DEV).manual_seed(13)
+    seq = torch.tensor([N, 1700], dtype=torch.int32, device=DEV)
+    nqt = torch.tensor([4, 3], dtype=torch.int32, device=DEV)
+    qs = [torch.randn((B, nq, Hq, d), generator=g, device=DEV).to(torch.bfloat16) for _ in range(5)]
+    ks = [torch.randn((B, N, Hkv, d), generator=g, device=DEV).to(torch.bfloat16) for _ in range(5)]
+    out = D.score_per_layer(qs, ks, seq, heads, n_query=nqt, groups=groups, max_len=N)
+    singles = [D.score(q, k, seq, heads, n_query=nqt, groups=groups, max_len=N).clone() for q, k in zip(qs, ks)]
+    torch.cuda.synchronize()
+    for l, one in enumerate(singles):
+        assert torch.equal(out[l, 0, :, :N], one[0, :, :N]) and torch.equal(out[l, 1, :, :1700], one[1, :, :1700])
+    ref = O.score(bits(qs[3]), bits(ks[3]), [N, 1700], [4, 3], heads, scale_of(d), num_kv_heads=Hkv, groups=groups)
+    for b, n in enumerate([N, 1700]):
+        for go in range(groups):
+            check_score(host(out[3])[b, go, :n], ref[b, go, :n], n, f"layer 3 b={b} go={go}")
