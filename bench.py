@@ -41,6 +41,8 @@ def parse():
                    choices=["tiny", "qwen7b", "qwen72b", "ragged", "long131k"])
     p.add_argument("--k", type=int, default=None, help="override the budget k (e.g. 512)")
     p.add_argument("--layers", type=int, default=None, help="override the stacked layer count")
+    p.add_argument("--groups", choices=["1", "hkv"], default="1",
+                   help="index sets per sequence: one (the paper's global set) or one per KV head")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-sample-seqs", type=int, default=16)
     p.add_argument("--copy-probe", action="store_true",
@@ -208,25 +210,27 @@ def arr_eval(s, layer, s_t, s_d, idx, cnt, seq, nq, bud, mm):
     of one evaluation (A-bar plus the oracle's selection and both ARRs)."""
     import torch
     import paper_2606_24957_amd as D
-    N, k, P = s.n_max, s.k_max, s.n_sink + s.n_window
+    N, k, P, G = s.n_max, s.k_max, s.n_sink + s.n_window, s.groups
     heads = list(range(s.num_q_heads))
+    hpg = s.num_q_heads // G
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
-    abar = D.score(layer.q, layer.k, seq, heads, n_query=nq, max_len=N, page_table=layer.page_table)
-    oidx, ocnt = D.topk(None, abar, seq, k, budget=bud, n_sink=0, n_window=0, m_scalar=0)
-    orc = D.arr(abar, oidx, ocnt, seq, s.num_q_heads, window=nq)
-    hyb = D.arr(abar, idx, cnt, seq, s.num_q_heads, window=nq)
+    abar = D.score(layer.q, layer.k, seq, heads, n_query=nq, groups=G, max_len=N, page_table=layer.page_table)
+    oidx, ocnt = D.topk(None, abar, seq, k, budget=bud, n_sink=0, n_window=0, m_scalar=0, groups=G)
+    orc = D.arr(abar, oidx, ocnt, seq, hpg, window=nq)
+    hyb = D.arr(abar, idx, cnt, seq, hpg, window=nq)
     e1.record()
     torch.cuda.synchronize()
     eval_us = e0.elapsed_time(e1) * 1e3
     res = {"sd_oracle": orc, "dustin": hyb}
-    ti, tc = D.topk(None, s_t, seq, k, budget=bud, m_scalar=0, n_sink=s.n_sink, n_window=s.n_window)
-    res["dustin_t"] = D.arr(abar, ti, tc, seq, s.num_q_heads, window=nq)
-    di, dc = D.topk(s_d, None, seq, k, budget=bud, n_sink=s.n_sink, n_window=s.n_window)
-    res["dustin_d"] = D.arr(abar, di, dc, seq, s.num_q_heads, window=nq)
+    ti, tc = D.topk(None, s_t, seq, k, budget=bud, m_scalar=0, n_sink=s.n_sink, n_window=s.n_window, groups=G)
+    res["dustin_t"] = D.arr(abar, ti, tc, seq, hpg, window=nq)
+    di, dc = D.topk(s_d, None, seq, k, budget=bud, n_sink=s.n_sink, n_window=s.n_window, groups=G)
+    res["dustin_d"] = D.arr(abar, di, dc, seq, hpg, window=nq)
     if len(set(s.budget)) == 1:  # StreamingLLM-like: the whole budget on sinks and the recent window
-        si, sc = D.topk(None, s_t, seq, k, budget=bud, m_scalar=0, n_sink=s.n_sink, n_window=k - s.n_sink)
-        res["sinks_and_recent"] = D.arr(abar, si, sc, seq, s.num_q_heads, window=nq)
+        si, sc = D.topk(None, s_t, seq, k, budget=bud, m_scalar=0, n_sink=s.n_sink, n_window=k - s.n_sink,
+                        groups=G)
+        res["sinks_and_recent"] = D.arr(abar, si, sc, seq, hpg, window=nq)
     torch.cuda.synchronize()
     rec = {name: round(float(v.mean()), 5) for name, v in res.items()}
     rec["eval_us"] = round(eval_us, 1)
@@ -303,8 +307,10 @@ def cpu_baseline(s, layer0, est, n_seq):
     v = bf16_bits(vv[sl])
     times = {}
     t0 = time.perf_counter()
-    init = None if est.init_target is None else est.init_target[sl].cpu().numpy()
-    st = O.score(bf16_bits(est.q_target[sl]), k, seq, [1] * nb, s.target_heads, scale, init=init)
+    init = None if est.init_target is None else np.ascontiguousarray(
+        np.broadcast_to(est.init_target[sl].cpu().numpy(), (nb, s.groups, s.n_max)))
+    st = O.score(bf16_bits(est.q_target[sl]), k, seq, [1] * nb, s.target_heads, scale,
+                 num_kv_heads=s.num_kv_heads, groups=s.groups, init=init)
     times["score_target"] = time.perf_counter() - t0
     t0 = time.perf_counter()
     if est.s_draft_given is not None:
@@ -317,7 +323,7 @@ def cpu_baseline(s, layer0, est, n_seq):
                          [t - 1 for t in nq], s.draft.heads, dscale, init=sd)
     times["score_draft"] = time.perf_counter() - t0
     t0 = time.perf_counter()
-    idx, cnt = O.select(sd, st, seq, s.k_max, budget=s.budget[:nb], m=s.m[:nb])
+    idx, cnt = O.select(sd, st, seq, s.k_max, budget=s.budget[:nb], m=s.m[:nb], groups=s.groups)
     times["select"] = time.perf_counter() - t0
     rows = O.all_rows(nb, nq, s.num_q_heads)
     t0 = time.perf_counter()
@@ -364,6 +370,8 @@ def main():
         s = s.replace(budget=(args.k,) * s.B, m=((args.k - s.n_sink - s.n_window) // 2,) * s.B)
     if args.layers is not None:
         s = s.replace(layers=args.layers)
+    if args.groups == "hkv":
+        s = W.per_kv_head(s)
     L = s.layers
     log(f"[bench] workload {s.name}: B={s.B} N={s.n_max} Hq={s.num_q_heads} Hkv={s.num_kv_heads} "
         f"T={s.t_max} k={s.k_max} layers={L} paged={bool(s.page_size)}")
@@ -379,7 +387,8 @@ def main():
     gam = torch.tensor(s.draft_gamma, dtype=torch.int32, device=dev)
     bud = torch.tensor(s.budget, dtype=torch.int32, device=dev)
     mm = torch.tensor(s.m, dtype=torch.int32, device=dev)
-    s_t = torch.zeros((B, 1, N), dtype=torch.float32, device=dev)
+    G = s.groups
+    s_t = torch.zeros((B, G, N), dtype=torch.float32, device=dev)
     s_d = torch.zeros((B, 1, N), dtype=torch.float32, device=dev)
     idx = torch.zeros((B, s.groups, s.k_max), dtype=torch.int32, device=dev)
     cnt = torch.zeros((B, s.groups), dtype=torch.int32, device=dev)
@@ -387,7 +396,10 @@ def main():
     outs_d = [torch.empty_like(l.q) for l in layers]
 
     # prepared launches (arguments marshalled once)
-    score_t = D.plan_score(est.q_target, layers[0].k, seq, s.target_heads, init=est.init_target,
+    init_t = est.init_target
+    if init_t is not None and G > 1:  # one historical row, the same for every group
+        init_t = init_t.expand(B, G, N)
+    score_t = D.plan_score(est.q_target, layers[0].k, seq, s.target_heads, groups=G, init=init_t,
                            out=s_t, max_len=N, page_table=layers[0].page_table)
     score_d = []
     if est.s_draft_given is not None:
@@ -516,7 +528,7 @@ def main():
             log(f"[bench] verify step graph: {exc}")
 
     per_layer = None
-    if args.only == "all" and s.draft is not None:
+    if args.only == "all" and s.draft is not None and s.groups == 1:
         try:
             per_layer = per_layer_selection(s, layers, dev, args.steps, args.warmup, sp_us, dn_us, est_us)
         except Exception as exc:  # reported, not fatal

@@ -37,7 +37,7 @@ class VerifyStep:
         self.seq, self.nq, self.gam = i32(s.seq_lens), i32(s.n_query), i32(s.draft_gamma)
         self.bud, self.mm = i32(s.budget), i32(s.m)
         N = s.n_max
-        self.s_t = torch.zeros((s.B, 1, N), dtype=torch.float32, device=device)
+        self.s_t = torch.zeros((s.B, s.groups, N), dtype=torch.float32, device=device)
         self.s_d = torch.zeros((s.B, 1, N), dtype=torch.float32, device=device)
         self.idx = torch.zeros((s.B, s.groups, s.k_max), dtype=torch.int32, device=device)
         self.cnt = torch.zeros((s.B, s.groups), dtype=torch.int32, device=device)
@@ -49,9 +49,11 @@ class VerifyStep:
     def _plan(self) -> List:
         """The step's operations, bound to the current stream."""
         s, est, N = self.s, self.est, self.s.n_max
-        ops = [plan_score(est.q_target, self.layers[0].k, self.seq, s.target_heads,
-                          init=est.init_target, out=self.s_t, max_len=N,
-                          page_table=self.layers[0].page_table)]
+        init = est.init_target
+        if init is not None and s.groups > 1:  # one historical row, the same for every group
+            init = init.expand(s.B, s.groups, N)
+        ops = [plan_score(est.q_target, self.layers[0].k, self.seq, s.target_heads, groups=s.groups,
+                          init=init, out=self.s_t, max_len=N, page_table=self.layers[0].page_table)]
         if est.s_draft_given is not None:
             given = est.s_draft_given
             ops.append(lambda: self.s_d.copy_(given))

@@ -139,6 +139,15 @@ def config(name: str, **overrides) -> Shape:
     return s
 
 
+def per_kv_head(s: Shape) -> Shape:
+    """The same workload with one index set per KV head (groups = Hkv): each KV head then
+    needs target scoring heads of its own, so the preset takes one per KV head (head
+    g * G + g mod G of group g, G = Hq / Hkv), in place of heads spread over half the groups."""
+    gs = s.num_q_heads // s.num_kv_heads
+    heads = tuple(g * gs + g % gs for g in range(s.num_kv_heads))
+    return s.replace(name=s.name + "_per_kv_head", groups=s.num_kv_heads, target_heads=heads)
+
+
 def shrink(s: Shape, B: int = None, n: int = None, k: int = None, layers: int = None,
            t: int = None, name: str = None) -> Shape:
     """A smaller copy of a preset with uniform per-sequence values, for oracle-sized tests."""

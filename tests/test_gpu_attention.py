@@ -13,7 +13,7 @@ import torch
 import oracle as O
 import paper_2606_24957_amd as D
 from paper_2606_24957_amd import workloads as W
-from tests.gpu_util import bits, check_attention, gpu_rows, scale_of
+from tests.gpu_util import bits, check_attention, check_score, gpu_rows, scale_of
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
@@ -218,3 +218,37 @@ def test_full_size_ragged_paged_layer():
 @pytest.mark.skipif(os.environ.get("DUSTIN_SKIP_131K") == "1", reason="131k layer skipped by request")
 def test_full_size_131k_layer():
     _full_size_sampled(W.config("long131k").replace(layers=1), n_rows=24)
+
+
+def test_full_size_per_kv_head_step():
+    """One index set per KV head at the headline shape (groups = 8, one target scoring head
+    per KV head): the step's per-group target score against the oracle, its per-group sets
+    bit-exact against the oracle's Eq. 6 on the same scores, and sampled attention rows with
+    those sets against the oracle."""
+    from paper_2606_24957_amd import step as S
+    s = W.per_kv_head(W.config("qwen72b").replace(layers=1))
+    L = W.make_layer(s, 0, DEV)
+    est = W.make_estimation(s, L, DEV)
+    st = S.VerifyStep(s, [L], est, DEV, append=False)
+    st.run()
+    torch.cuda.synchronize()
+    s_t, s_d = st.s_t.cpu().numpy(), st.s_d.cpu().numpy()
+    idx_np, cnt_np = st.idx.cpu().numpy(), st.cnt.cpu().numpy()
+    kk, vv = L.contiguous_kv(s)
+    rows = _sample_rows(s, 32, 5)
+    for b in (0, 6, 15):
+        n = s.seq_lens[b]
+        ref_t = O.score(bits(est.q_target[b:b + 1]), bits(kk[b:b + 1, :n]), [n], [1], s.target_heads,
+                        scale_of(128), num_kv_heads=8, groups=8)
+        for g in range(8):
+            check_score(s_t[b, g, :n], ref_t[0, g, :n], n, f"S_T b={b} g={g}")
+        ri, rc = O.select(s_d[b:b + 1], s_t[b:b + 1], [n], s.k_max, budget=[s.budget[b]], m=[s.m[b]], groups=8)
+        np.testing.assert_array_equal(cnt_np[b], rc[0])
+        for g in range(8):
+            np.testing.assert_array_equal(idx_np[b, g, :rc[0, g]], ri[0, g, :rc[0, g]], err_msg=f"b={b} g={g}")
+    for b in sorted(set(rows[:, 0].tolist())):
+        sel = rows[rows[:, 0] == b].copy()
+        sel[:, 0] = 0
+        ref = O.attention(bits(L.q[b:b + 1]), bits(kk[b:b + 1]), bits(vv[b:b + 1]), [s.seq_lens[b]],
+                          scale_of(128), sel, idx=idx_np[b:b + 1], count=cnt_np[b:b + 1])
+        check_attention(gpu_rows(st.outs[0], rows[rows[:, 0] == b]), ref, f"per-kv-head b={b}")
