@@ -430,14 +430,16 @@ def main():
             if rec: marks.append(ev())
             sel()
             if rec: marks.append(ev())
+        # the layers run back to back, events only around each block of L layers (an event
+        # between launches adds its own end-of-pipe wait, which a forward pass does not have)
         if args.only in ("all", "sparse"):
             for c in sparse:
                 c()
-                if rec: marks.append(ev())
+            if rec: marks.append(ev())
         if args.only in ("all", "dense"):
             for c in dense:
                 c()
-                if rec: marks.append(ev())
+            if rec: marks.append(ev())
         return marks
 
     for _ in range(args.warmup):
@@ -468,10 +470,10 @@ def main():
             est_k.append(m[2].elapsed_time(m[3]))
             i = 3
         if args.only in ("all", "sparse"):
-            sp += [m[i + j].elapsed_time(m[i + j + 1]) for j in range(L)]
-            i += L
+            sp.append(m[i].elapsed_time(m[i + 1]) / L)
+            i += 1
         if args.only in ("all", "dense"):
-            dn += [m[i + j].elapsed_time(m[i + j + 1]) for j in range(L)]
+            dn.append(m[i].elapsed_time(m[i + 1]) / L)
 
     def med(x):
         x = sorted(x)
@@ -480,13 +482,24 @@ def main():
     def mean(x):
         return sum(x) / len(x) if x else float("nan")
 
+    # the same sparse launches with an event between each (for comparison only)
+    sp_ev = []
+    if args.only in ("all", "sparse"):
+        for _ in range(max(1, args.steps // 3)):
+            es = [ev()]
+            for c in sparse:
+                c()
+                es.append(ev())
+            torch.cuda.synchronize()
+            sp_ev += [es[j].elapsed_time(es[j + 1]) for j in range(L)]
     sp_us, dn_us = mean(sp) * 1e3, mean(dn) * 1e3
     est_us = (mean(est_t) + mean(est_d) + mean(est_k)) * 1e3
     sb, db = sparse_bytes(s), dense_bytes(s)
     eb = score_bytes(s, True) + (0 if est.s_draft_given is not None else score_bytes(s, False)) + topk_bytes(s)
     achieved = sb / (sp_us * 1e-6) / 1e9 if sp else float("nan")
     dense_gbps = db / (dn_us * 1e-6) / 1e9 if dn else float("nan")
-    log(f"[bench] sparse {sp_us:.2f} us/layer (median {med(sp) * 1e3:.2f}) = {achieved:.0f} GB/s on "
+    log(f"[bench] sparse {sp_us:.2f} us/layer (median {med(sp) * 1e3:.2f}; with an event between launches "
+        f"{mean(sp_ev) * 1e3:.2f}) = {achieved:.0f} GB/s on "
         f"{sb / 1e6:.1f} MB; dense {dn_us:.1f} us/layer = {dense_gbps:.0f} GB/s; estimation "
         f"{est_us:.1f} us/step (target {mean(est_t) * 1e3:.1f}, draft {mean(est_d) * 1e3:.1f}, "
         f"topk {mean(est_k) * 1e3:.1f}); {ms_per_step:.3f} ms/step wall")
@@ -582,6 +595,8 @@ def main():
             "frac": round(achieved / PEAK_HBM_GBPS, 4), "traffic": traffic,
             "kernel": SPARSE_KERNEL + " (sparse)", "bytes_per_launch": sb,
             "avg_launch_us": round(sp_us, 3),
+            "timing": f"events around {L} back-to-back launches per step, divided by {L}",
+            "avg_launch_us_with_event_between_launches": round(mean(sp_ev) * 1e3, 3) if sp_ev else None,
         },
         "dense": {"us_per_layer": round(dn_us, 3), "GBps": round(dense_gbps, 1), "bytes_per_launch": db,
                   "frac": round(dense_gbps / PEAK_HBM_GBPS, 4)},
