@@ -91,3 +91,22 @@ def test_arr_full_size_qwen72b():
     np.testing.assert_allclose(got[sel], ref, atol=ARR_ABS)
     ref_o = O.arr(qb, kb, lens, wins, scale_of(128), idx=host(oidx)[sel], count=host(ocnt)[sel])
     np.testing.assert_allclose(got_orc[sel], ref_o, atol=ARR_ABS)
+
+
+def test_arr_degenerate_lengths():
+    """ARR of an empty sequence is 0, of a one-position sequence with that position is 1."""
+    B, Hq, Hkv, d = 3, 4, 1, 128
+    seq = [0, 1, 300]
+    g = torch.Generator(device=DEV).manual_seed(10)
+    q = torch.randn((B, 3, Hq, d), generator=g, device=DEV).to(torch.bfloat16)
+    k = torch.randn((B, 320, Hkv, d), generator=g, device=DEV).to(torch.bfloat16)
+    seq_t = torch.tensor(seq, dtype=torch.int32, device=DEV)
+    s = D.score(q, k, seq_t, list(range(Hq)), n_query=torch.tensor([3, 3, 3], dtype=torch.int32, device=DEV),
+                max_len=320)
+    s[0].fill_(7.0)                                                # never read: N_0 = 0
+    idx, cnt = D.topk(None, s, seq_t, 64, n_sink=0, n_window=0, m_scalar=0)
+    a = host(D.arr(s, idx, cnt, seq_t, Hq, window=3))
+    torch.cuda.synchronize()
+    assert a[0, 0] == 0.0 and abs(a[1, 0] - 1.0) < 2e-4 and 0.0 < a[2, 0] < 1.0
+    ref = O.arr(bits(q), bits(k[:, :300]), seq, [3, 3, 3], scale_of(d), idx=host(idx), count=host(cnt))
+    np.testing.assert_allclose(a, ref, atol=2e-4)

@@ -178,3 +178,35 @@ def test_page_score_full_size_qwen72b():
         pages, per = np.unique(inner // ps, return_counts=True)
         full = [p for p, c_ in zip(pages, per) if c_ == min(ps, n - s.n_window - p * ps) or p * ps < s.n_sink]
         assert len(pages) - len(full) <= 1
+
+
+def test_page_estimator_degenerate_lengths():
+    """Empty sequences get no page and no output; a sequence shorter than one page has one
+    page whose score is the whole softmax (1 per (head, query)); a page size above every
+    length gives one page per sequence."""
+    B, Hq, Hkv, d, ps = 3, 8, 2, 128, 16
+    seq = [0, 5, 40]
+    N = 48
+    k = _k(B, N, Hkv, d, 9)
+    g = torch.Generator(device=DEV).manual_seed(9)
+    q = torch.randn((B, 2, Hq, d), generator=g, device=DEV).to(torch.bfloat16)
+    meta = torch.full((B, 3, Hkv, 2 * d), -3.0, dtype=torch.bfloat16, device=DEV)
+    D.page_meta(k, seq, ps, meta=meta, max_len=N)
+    out = torch.full((B, 1, N), -5.0, device=DEV)
+    D.page_score(q, meta, seq, [0, 5], ps, max_len=N, n_query=torch.tensor([2, 2, 1], dtype=torch.int32,
+                                                                           device=DEV), out=out)
+    big = D.page_meta(k, seq, 64, max_len=N)
+    out64 = D.page_score(q, big, seq, [0, 5], 64, max_len=N)
+    torch.cuda.synchronize()
+    m = meta.float().cpu()
+    assert torch.all(m[0] == -3.0)                                 # N_b = 0: no page written
+    assert torch.all(m[1, 1:] == -3.0) and torch.all(m[2, 3:] == -3.0)
+    o = host(out)
+    assert np.all(o[0] == -5.0)                                    # no output for N_b = 0
+    np.testing.assert_allclose(o[1, 0, :5], 2 * 2, rtol=1e-6)       # one page: 2 heads x 2 queries
+    assert np.all(o[1, 0, 5:] == -5.0)
+    ref = O.page_score(bits(q), bits(meta), seq, [2, 2, 1], [0, 5], scale_of(d), ps, length=N)
+    check_score(o[2, 0, :40], ref[2, 0, :40], 3, "b=2")
+    o64 = host(out64)
+    np.testing.assert_allclose(o64[2, 0, :40], 2 * 2, rtol=1e-6)    # one page of 64 holds all 40
+
