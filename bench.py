@@ -565,6 +565,22 @@ def main():
         cpu = cpu_baseline(s, layers[0], est, args.cpu_sample_seqs)
         log(f"[bench] oracle: {cpu}")
 
+    # context for the roofline: what a plain 1 GiB device copy reaches on this machine
+    copy_gbps = None
+    if args.only == "all":
+        src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        c0.record()
+        for _ in range(5):
+            dst.copy_(src)
+        c1.record()
+        torch.cuda.synchronize()
+        copy_gbps = round(2 * (1 << 30) * 5 / (c0.elapsed_time(c1) * 1e-3) / 1e9, 1)
+        del src, dst
+        log(f"[bench] 1 GiB device copy: {copy_gbps} GB/s (read + write)")
+
     traffic = measured_traffic(s.name, s.k_max)
     rec = {
         "metric": "sparse verify-attention us/layer + achieved HBM GB/s, B=16 ctx=32k 72B-shape",
@@ -597,6 +613,8 @@ def main():
             "avg_launch_us": round(sp_us, 3),
             "timing": f"events around {L} back-to-back launches per step, divided by {L}",
             "avg_launch_us_with_event_between_launches": round(mean(sp_ev) * 1e3, 3) if sp_ev else None,
+            "measured_copy_GBps": copy_gbps,
+            "frac_of_measured_copy": round(achieved / copy_gbps, 4) if copy_gbps else None,
         },
         "dense": {"us_per_layer": round(dn_us, 3), "GBps": round(dense_gbps, 1), "bytes_per_launch": db,
                   "frac": round(dense_gbps / PEAK_HBM_GBPS, 4)},
