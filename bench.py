@@ -353,8 +353,8 @@ def cpu_baseline(s, layer0, est, n_seq):
 def main():
     args = parse()
     if args.gpus != 1:
-        log(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the data-parallel "
-            "path shards by sequence or KV head with no exchange inside a layer, see DESIGN.md")
+        log(f"bench.py measures one GPU only (asked for --gpus {args.gpus}): the path would shard by "
+            "sequence or by KV head, with no exchange inside a layer, and that is not built here")
         sys.exit(2)
     import torch
     import paper_2606_24957_amd as D

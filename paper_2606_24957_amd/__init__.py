@@ -208,6 +208,15 @@ def kv_view(cache: torch.Tensor, page_table: Optional[torch.Tensor] = None) -> D
     return kv
 
 
+def _check_scores(t: torch.Tensor, B: int, groups: int, max_len: int, name: str):
+    """An fp32 [>= B, >= groups (or 1 with stride 0), >= max_len] score array with
+    contiguous positions."""
+    if t.dtype != torch.float32 or t.dim() != 3 or t.stride(2) != 1:
+        raise ValueError(f"{name} must be fp32 [B, G, N] with contiguous positions")
+    if t.shape[0] < B or t.shape[2] < max_len or not (t.shape[1] >= groups or t.stride(1) == 0):
+        raise ValueError(f"{name} {tuple(t.shape)} does not hold [{B}, {groups}, {max_len}]")
+
+
 def _capacity(kv: DustinKV) -> int:
     return kv.max_pages * kv.page_size if kv.page_table else kv.capacity
 
@@ -243,6 +252,9 @@ def plan_score(q: torch.Tensor, k: torch.Tensor, seq_lens, heads: Sequence[int],
     max_len = _capacity(kv) if max_len is None else int(max_len)
     if out is None:
         out = torch.empty((B, groups, max_len), dtype=torch.float32, device=dev)
+    _check_scores(out, B, groups, max_len, "out")
+    if init is not None:
+        _check_scores(init, B, groups, max_len, "init")
     heads_host = (ctypes.c_int32 * len(heads))(*[int(h) for h in heads])
     bt = _batch(B, max_len, nq_max, 0, seq, nqa)
     nbytes = lib().dustin_score_workspace(B, max_len, nq_max, len(heads))
@@ -284,6 +296,9 @@ def plan_score_layers(qs: Sequence[torch.Tensor], ks: Sequence[torch.Tensor], se
     max_len = _capacity(kvs[0]) if max_len is None else int(max_len)
     if out is None:
         out = torch.empty((B, groups, max_len), dtype=torch.float32, device=dev)
+    _check_scores(out, B, groups, max_len, "out")
+    if init is not None:
+        _check_scores(init, B, groups, max_len, "init")
     heads_host = (ctypes.c_int32 * len(heads))(*[int(h) for h in heads])
     q_host = (ctypes.c_void_p * len(qs))(*[q.data_ptr() for q in qs])
     bt = _batch(B, max_len, nq_max, 0, seq, nqa)
@@ -327,6 +342,9 @@ def plan_score_per_layer(qs: Sequence[torch.Tensor], ks: Sequence[torch.Tensor],
     max_len = _capacity(kvs[0]) if max_len is None else int(max_len)
     if out is None:
         out = torch.empty((len(qs), B, groups, max_len), dtype=torch.float32, device=dev)
+    if (out.dtype != torch.float32 or out.dim() != 4 or out.shape[0] < len(qs) or out.shape[1] < B
+            or out.shape[2] < groups or out.shape[3] < max_len or out.stride(3) != 1):
+        raise ValueError(f"out must be fp32 [>= {len(qs)}, >= {B}, >= {groups}, >= {max_len}] with contiguous positions")
     heads_host = (ctypes.c_int32 * len(heads))(*[int(h) for h in heads])
     q_host = (ctypes.c_void_p * len(qs))(*[q.data_ptr() for q in qs])
     bt = _batch(B, max_len, nq_max, 0, seq, nqa)
@@ -370,7 +388,12 @@ def plan_page_meta(k: torch.Tensor, seq_lens, page_size: int, meta: torch.Tensor
     max_span = max_len if max_span is None else int(max_span)
     if meta.dtype != torch.bfloat16 or meta.dim() != 4 or meta.stride(3) != 1 or meta.stride(2) != meta.shape[3]:
         raise ValueError("meta must be bf16 [B, pages, Hkv, 2d] with contiguous (Hkv, 2d) rows")
-    bt = _batch(seq.shape[0], max_len, 0, 0, seq)
+    B = seq.shape[0]
+    pages = (max_len + int(page_size) - 1) // int(page_size)
+    if (meta.shape[0] < B or meta.shape[1] < pages or meta.shape[2] != k.shape[2]
+            or meta.shape[3] != 2 * k.shape[3]):
+        raise ValueError(f"meta {tuple(meta.shape)} does not hold [{B}, {pages}, {k.shape[2]}, {2 * k.shape[3]}]")
+    bt = _batch(B, max_len, 0, 0, seq)
     args = (ctypes.byref(kv), ctypes.byref(bt), _ptr(frm), max_span, int(page_size), _ptr(meta),
             meta.stride(0), meta.stride(1), meta.shape[1], _stream(stream))
     return Call(lib().dustin_page_meta, args, "dustin_page_meta", (k, meta, kv, bt, frm), meta)
@@ -402,8 +425,14 @@ def plan_page_score(q: torch.Tensor, meta: torch.Tensor, seq_lens, heads: Sequen
     seq = _i32_dev(seq_lens, dev)
     nqa = _i32_dev(n_query, dev)
     max_len = int(max_len)
+    pages = (max_len + int(page_size) - 1) // int(page_size)
+    if meta.shape[0] < B or meta.shape[1] < pages:
+        raise ValueError(f"meta {tuple(meta.shape)} holds fewer than {B} sequences or {pages} pages")
     if out is None:
         out = torch.empty((B, groups, max_len), dtype=torch.float32, device=dev)
+    _check_scores(out, B, groups, max_len, "out")
+    if init is not None:
+        _check_scores(init, B, groups, max_len, "init")
     heads_host = (ctypes.c_int32 * len(heads))(*[int(h) for h in heads])
     bt = _batch(B, max_len, nq_max, 0, seq, nqa)
     nbytes = lib().dustin_page_score_workspace(B, max_len, int(page_size), nq_max, len(heads))
@@ -435,6 +464,8 @@ def plan_arr(s: torch.Tensor, idx: torch.Tensor, count: torch.Tensor, seq_lens, 
     if idx.dtype != torch.int32 or count.dtype != torch.int32 or idx.stride(2) != 1:
         raise ValueError("idx / count must be int32 (idx [B, G, k_max] contiguous in k)")
     B, G, k_max = idx.shape
+    if count.shape != (B, G) or s.shape[0] < B or s.shape[1] not in (1, G):
+        raise ValueError("count must be [B, G] and s [B, G or 1, N] for idx [B, G, k_max]")
     dev = s.device
     seq = _i32_dev(seq_lens, dev)
     if window is None:
@@ -447,6 +478,10 @@ def plan_arr(s: torch.Tensor, idx: torch.Tensor, count: torch.Tensor, seq_lens, 
     max_len = s.shape[2] if max_len is None else int(max_len)
     if out is None:
         out = torch.empty((B, G), dtype=torch.float64, device=dev)
+    if out.dtype != torch.float64 or out.shape != (B, G) or not out.is_contiguous():
+        raise ValueError("out must be a contiguous fp64 [B, G] tensor")
+    if max_len > s.shape[2]:
+        raise ValueError("max_len exceeds the score rows")
     bt = _batch(B, max_len, w_max, k_max, seq, win)
     s_sg = s.stride(1) if s.shape[1] > 1 else 0
     args = (_ptr(s), s.stride(0), s_sg, _ptr(idx), idx.stride(0), idx.stride(1), _ptr(count),
