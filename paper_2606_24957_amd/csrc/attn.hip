@@ -183,7 +183,7 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
   int n_raw = 0, t_raw = 0, c_raw = 0;
   const int rows_mem = a.dims.nq_max * a.group_size;  // query rows present in memory
   auto q_row_ptr = [&](int r) {
-    const int t = r / a.group_size, hh = r - t * a.group_size;
+    const int t = small_div(r, a.group_size), hh = r - t * a.group_size;
     return a.q + (int64_t)b * a.q_sb + (int64_t)t * a.q_st + (int64_t)(g * a.group_size + hh) * a.q_sh;
   };
   // Q^T as B operands: lane holds Q[row rt*16+lr][32 ks + 8 lg + e] (row r = t G + hh),
@@ -218,21 +218,23 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
                            : a.dims.seq_lens + b;
       own_sizes = *src;
     }
+    // Every query load is unconditional: a row past those in memory reads the last one,
+    // and is zeroed with the rows of absent verification tokens once the sizes are known.
+    // (Conditional loads made the compiler recompute the row address, a division and
+    // 64-bit products, inside every load's branch.)
     if constexpr (kQReg) {
 #pragma unroll
       for (int rt = 0; rt < RT; ++rt) {
-        const int r = rt * 16 + lr;
+        const uint16_t* qp = q_row_ptr(min(rt * 16 + lr, rows_mem - 1)) + 8 * lg;
 #pragma unroll
-        for (int ks = 0; ks < 4; ++ks)
-          qreg[rt][ks] = r < rows_mem ? as_bf16x8(load16(q_row_ptr(r) + 8 * lg + 32 * ks))
-                                      : as_bf16x8(u32x4{0u, 0u, 0u, 0u});
+        for (int ks = 0; ks < 4; ++ks) qreg[rt][ks] = as_bf16x8(load16(qp + 32 * ks));
       }
     } else {
 #pragma unroll
       for (int j = 0; j < kQPer; ++j) {
-        const int e = threadIdx.x + j * kW * kWave;
+        const int e = min((int)threadIdx.x + j * kW * kWave, kQChunks - 1);
         const int r = e / (kD / 8), c0 = (e % (kD / 8)) * 8;
-        qx[j] = (e < kQChunks && r < rows_mem) ? load16(q_row_ptr(r) + c0) : u32x4{0u, 0u, 0u, 0u};
+        qx[j] = load16(q_row_ptr(min(r, rows_mem - 1)) + c0);
       }
     }
     if constexpr (kStage) load_selection(s_begin);
@@ -244,16 +246,17 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
   };
   prologue_loads();
   // sizes of pairs 4 lane .. 4 lane + 3 (wave 0; issued with the prologue loads)
+  // (unconditional loads: a lane past the last pair reads the last pair's sizes, which
+  // count for nothing, see steps_of's callers)
   int pn[4], pt[4], pc[4];
   if (balance && wave == 0) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const int p = 4 * lane + j;
-      const bool ok = p < a.pairs;
-      const int pb = ok ? small_div(p, a.num_kv_heads) : 0, pg = ok ? p - pb * a.num_kv_heads : 0;
-      pn[j] = ok ? a.dims.seq_lens[pb] : 0;
-      pt[j] = ok ? (a.dims.n_query ? a.dims.n_query[pb] : a.dims.nq_max) : 0;
-      pc[j] = ok && kSparse ? a.count[pb * a.groups + (a.groups == 1 ? 0 : pg)] : 0;
+      const int p = min(4 * lane + j, a.pairs - 1);
+      const int pb = small_div(p, a.num_kv_heads), pg = p - pb * a.num_kv_heads;
+      pn[j] = a.dims.seq_lens[pb];
+      pt[j] = a.dims.n_query ? a.dims.n_query[pb] : a.dims.nq_max;
+      pc[j] = kSparse ? a.count[pb * a.groups + (a.groups == 1 ? 0 : pg)] : 0;
     }
   }
 
@@ -272,7 +275,7 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
     if (wave == 0) {
       int st[4];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) st[j] = steps_of(pn[j], pt[j], pc[j]);
+      for (int j = 0; j < 4; ++j) st[j] = 4 * lane + j < a.pairs ? steps_of(pn[j], pt[j], pc[j]) : 0;
       // ceil(x / s) splits of size ceil(x / k), and with that size no empty trailing split
       auto splits_for = [](int x, int s, int& size) {
         const int k0 = x ? small_div(x + s - 1, s) : 0;
@@ -424,7 +427,7 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
 #pragma unroll
   for (int rt = 0; rt < RT; ++rt) {
     const int r = rt * 16 + lr;
-    limit[rt] = wstart + (r < rows ? r / a.group_size : T - 1);
+    limit[rt] = wstart + (r < rows ? small_div(r, a.group_size) : T - 1);
   }
   if constexpr (kQReg) {
 #pragma unroll
