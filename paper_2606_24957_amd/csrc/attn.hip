@@ -120,7 +120,7 @@ template <int RT, bool kSparse, bool kPaged, bool kQReg>
 __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
   constexpr bool kStage = kSparse || kPaged;  // rows resolved through an LDS table
   constexpr int NDT = kD / 16;     // output 16-column tiles
-  constexpr int kQPitch = kD + 8;  // LDS row pitch (bf16) of staged queries (kQReg false)
+  constexpr int kQPitch = kD + 8;  // LDS row pitch (bf16) of staged queries
   constexpr int kPitch = kD + 4;   // LDS row pitch (fp32) of the merged accumulator
   constexpr int kTilesBytes = kW * 2 * kTile;                    // K and V tiles of every wave
   constexpr int kStageBytes = kStage ? kStageSteps * kStep * 4 : 0;
@@ -130,10 +130,12 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
   constexpr int kFinalBytes = kNB * kBufFloats * 4;
   __shared__ __attribute__((aligned(1024))) char smem[kLoopBytes > kFinalBytes ? kLoopBytes : kFinalBytes];
   uint32_t* const sm_phys = reinterpret_cast<uint32_t*>(smem + kTilesBytes);
-  // staged queries live in an LDS object of their own: the compiler can then see that
-  // the direct-to-LDS row loads in flight never write them, and reads them without
-  // waiting for those loads
-  __shared__ __attribute__((aligned(16))) uint16_t sm_q[kQReg ? 8 : RT * 16 * kQPitch];
+  // The queries are loaded once per workgroup (each thread a few 16-byte chunks) and
+  // staged in LDS; with up to three row tiles every wave then copies them to registers
+  // after the staging barrier, else they are read from LDS at every step.  They live in an
+  // LDS object of their own: the compiler can then see that the direct-to-LDS row loads in
+  // flight never write them, and reads them without waiting for those loads.
+  __shared__ __attribute__((aligned(16))) uint16_t sm_q[RT * 16 * kQPitch];
 
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);  // wave-uniform
@@ -187,10 +189,10 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
     return a.q + (int64_t)b * a.q_sb + (int64_t)t * a.q_st + (int64_t)(g * a.group_size + hh) * a.q_sh;
   };
   // Q^T as B operands: lane holds Q[row rt*16+lr][32 ks + 8 lg + e] (row r = t G + hh),
-  // in registers for up to 3 row tiles, else staged in LDS and read per step.
+  // in registers for up to 3 row tiles, else read from the LDS staging at every step.
   bf16x8 qreg[kQReg ? RT : 1][4];
   constexpr int kQChunks = RT * 16 * (kD / 8), kQPer = (kQChunks + kW * kWave - 1) / (kW * kWave);
-  u32x4 qx[kQReg ? 1 : kQPer];
+  u32x4 qx[kQPer];
   int32_t sel[kStageBatch];  // selected positions of this thread's tokens in a chunk
   auto load_selection = [&](int cs) {
 #pragma unroll
@@ -219,23 +221,14 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
       own_sizes = *src;
     }
     // Every query load is unconditional: a row past those in memory reads the last one,
-    // and is zeroed with the rows of absent verification tokens once the sizes are known.
+    // and is zeroed with the rows of absent verification tokens when it is staged.
     // (Conditional loads made the compiler recompute the row address, a division and
     // 64-bit products, inside every load's branch.)
-    if constexpr (kQReg) {
 #pragma unroll
-      for (int rt = 0; rt < RT; ++rt) {
-        const uint16_t* qp = q_row_ptr(min(rt * 16 + lr, rows_mem - 1)) + 8 * lg;
-#pragma unroll
-        for (int ks = 0; ks < 4; ++ks) qreg[rt][ks] = as_bf16x8(load16(qp + 32 * ks));
-      }
-    } else {
-#pragma unroll
-      for (int j = 0; j < kQPer; ++j) {
-        const int e = min((int)threadIdx.x + j * kW * kWave, kQChunks - 1);
-        const int r = e / (kD / 8), c0 = (e % (kD / 8)) * 8;
-        qx[j] = load16(q_row_ptr(min(r, rows_mem - 1)) + c0);
-      }
+    for (int j = 0; j < kQPer; ++j) {
+      const int e = min((int)threadIdx.x + j * kW * kWave, kQChunks - 1);
+      const int r = e / (kD / 8), c0 = (e % (kD / 8)) * 8;
+      qx[j] = load16(q_row_ptr(min(r, rows_mem - 1)) + c0);
     }
     if constexpr (kStage) load_selection(s_begin);
     first_v0 = (s_begin + wave) * kStep + 8 * lg;
@@ -429,19 +422,12 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
     const int r = rt * 16 + lr;
     limit[rt] = wstart + (r < rows ? small_div(r, a.group_size) : T - 1);
   }
-  if constexpr (kQReg) {
+  // rows of absent verification tokens act as zero queries
 #pragma unroll
-    for (int rt = 0; rt < RT; ++rt)
-      if (rt * 16 + lr >= rows)  // rows of absent verification tokens act as zero queries
-#pragma unroll
-        for (int ks = 0; ks < 4; ++ks) qreg[rt][ks] = as_bf16x8(u32x4{0u, 0u, 0u, 0u});
-  } else {
-#pragma unroll
-    for (int j = 0; j < kQPer; ++j) {
-      const int e = threadIdx.x + j * kW * kWave;
-      const int r = e / (kD / 8), c0 = (e % (kD / 8)) * 8;
-      if (e < kQChunks) *reinterpret_cast<u32x4*>(sm_q + r * kQPitch + c0) = r < rows ? qx[j] : u32x4{0u, 0u, 0u, 0u};
-    }
+  for (int j = 0; j < kQPer; ++j) {
+    const int e = threadIdx.x + j * kW * kWave;
+    const int r = e / (kD / 8), c0 = (e % (kD / 8)) * 8;
+    if (e < kQChunks) *reinterpret_cast<u32x4*>(sm_q + r * kQPitch + c0) = r < rows ? qx[j] : u32x4{0u, 0u, 0u, 0u};
   }
   auto q_operand = [&](int rt, int ks) -> bf16x8 {
     if constexpr (kQReg)
@@ -646,6 +632,15 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
       }
     }
     lds_barrier();  // staged rows (and staged queries) are visible
+    if constexpr (kQReg) {
+      if (cs == s_begin) {
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+          for (int ks = 0; ks < 4; ++ks)
+            qreg[rt][ks] = as_bf16x8(*reinterpret_cast<const u32x4*>(sm_q + (rt * 16 + lr) * kQPitch + 8 * lg + 32 * ks));
+      }
+    }
     // this wave's steps: cs + wave + i kW
     int st = cs + wave;
     if (st >= ce) continue;
