@@ -165,8 +165,8 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
     unit = (xcd * A + 7) / 8 + xslot;
     return unit < ((xcd + 1) * A + 7) / 8;
   };
-  // With one split per pair, unit = pair.  With several, wave 0 sizes the splits from the
-  // actual per-pair token counts below.  Meanwhile the prologue loads of the uniform guess
+  // With one split per pair, unit = pair.  With several, every wave sizes the splits from
+  // the actual per-pair token counts below.  Meanwhile the prologue loads of the uniform guess
   // (every pair `splits` splits of split_steps steps, exact when the lengths are equal) are
   // already in flight; they are issued again only if the guess was wrong.
   const bool balance = a.splits > 1;  // kernel-uniform
@@ -238,11 +238,11 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
     }
   };
   prologue_loads();
-  // sizes of pairs 4 lane .. 4 lane + 3 (wave 0; issued with the prologue loads)
+  // sizes of pairs 4 lane .. 4 lane + 3 (every wave; issued with the prologue loads)
   // (unconditional loads: a lane past the last pair reads the last pair's sizes, which
   // count for nothing, see steps_of's callers)
   int pn[4], pt[4], pc[4];
-  if (balance && wave == 0) {
+  if (balance) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int p = min(4 * lane + j, a.pairs - 1);
@@ -263,107 +263,96 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
     // The smallest split size s (at least min_split_steps) whose splits fit the U slots:
     // pair p takes ceil(steps_p / s) splits of equal size.  s = ceil(W / U) (W = total steps)
     // fits when the lengths are equal; otherwise a binary search up to ceil(W / (U - pairs)),
-    // which always fits (sum ceil(steps_p / s) <= W / s + pairs).
-    __shared__ int sm_sched[8];
-    if (wave == 0) {
-      int st[4];
+    // which always fits (sum ceil(steps_p / s) <= W / s + pairs).  Every wave plans the same
+    // schedule from the same sizes, so no wave waits for another here.
+    int st[4];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) st[j] = 4 * lane + j < a.pairs ? steps_of(pn[j], pt[j], pc[j]) : 0;
-      // ceil(x / s) splits of size ceil(x / k), and with that size no empty trailing split
-      auto splits_for = [](int x, int s, int& size) {
-        const int k0 = x ? small_div(x + s - 1, s) : 0;
-        size = k0 ? small_div(x + k0 - 1, k0) : 0;
-        return k0 ? small_div(x + size - 1, size) : 0;
-      };
-      const int st0 = __builtin_amdgcn_readfirstlane(st[0]);
-      bool differs = false;
+    for (int j = 0; j < 4; ++j) st[j] = 4 * lane + j < a.pairs ? steps_of(pn[j], pt[j], pc[j]) : 0;
+    // ceil(x / s) splits of size ceil(x / k), and with that size no empty trailing split
+    auto splits_for = [](int x, int s, int& size) {
+      const int k0 = x ? small_div(x + s - 1, s) : 0;
+      size = k0 ? small_div(x + k0 - 1, k0) : 0;
+      return k0 ? small_div(x + size - 1, size) : 0;
+    };
+    const int st0 = __builtin_amdgcn_readfirstlane(st[0]);
+    bool differs = false;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) differs |= 4 * lane + j < a.pairs && st[j] != st0;
-      if (!__any(differs)) {
-        // equal lengths (the common case): every pair takes the same splits, no scan
-        int sz0;
-        const int k = splits_for(st0, max(small_div(st0 + a.splits - 1, a.splits), a.min_split_steps), sz0);
-        if (lane == 0) {
-          int my = 0;
-          sm_sched[0] = -1;
-          if (k && unit_of(a.pairs * k, my)) {
-            const int p = small_div(my, k);
-            sm_sched[0] = p;
-            sm_sched[1] = my - p * k;
-            sm_sched[2] = k;
-            sm_sched[3] = sz0;
-            sm_sched[4] = p * k;
-          }
-        }
-      } else {
-        int kk[4], sz[4], start[4];
-        int loc = 0;
+    for (int j = 0; j < 4; ++j) differs |= 4 * lane + j < a.pairs && st[j] != st0;
+    int p_new = -1, split_new = 0;
+    if (!__any(differs)) {
+      // equal lengths (the common case): every pair takes the same splits, no scan
+      int sz0;
+      const int k = splits_for(st0, max(small_div(st0 + a.splits - 1, a.splits), a.min_split_steps), sz0);
+      int my = 0;
+      if (k && unit_of(a.pairs * k, my)) {
+        p_new = small_div(my, k);
+        split_new = my - p_new * k;
+        nsplit = k;
+        split_steps = sz0;
+        slot0 = p_new * k;
+      }
+    } else {
+      int kk[4], sz[4], start[4];
+      int loc = 0;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) loc += st[j];
-        const int W = __builtin_amdgcn_readlane(wave_inclusive_sum(loc), 63);
-        // splits per pair for split size s, each pair's first unit, and the total
-        auto plan = [&](int s) {
-          int tot = 0;
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            kk[j] = splits_for(st[j], s, sz[j]);
-            start[j] = tot;
-            tot += kk[j];
-          }
-          const int incl = wave_inclusive_sum(tot);
-#pragma unroll
-          for (int j = 0; j < 4; ++j) start[j] += incl - tot;
-          return __builtin_amdgcn_readlane(incl, 63);
-        };
-        int s = max((W + U - 1) / U, a.min_split_steps);
-        int A = plan(s);
-        if (A > U) {
-          int lo = s + 1, hi = max(lo, (W + (U - a.pairs) - 1) / (U - a.pairs));
-          while (lo < hi) {
-            const int mid = (lo + hi) >> 1;
-            if (plan(mid) <= U) hi = mid;
-            else lo = mid + 1;
-          }
-          A = plan(lo);
-        }
-        int my = 0;
-        const bool ok = A <= U && unit_of(A, my);
-        if (lane == 0) sm_sched[0] = -1;  // no unit here (overwritten below by its owner)
+      for (int j = 0; j < 4; ++j) loc += st[j];
+      const int W = __builtin_amdgcn_readlane(wave_inclusive_sum(loc), 63);
+      // splits per pair for split size s, each pair's first unit, and the total
+      auto plan = [&](int s) {
+        int tot = 0;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          if (ok && kk[j] && my >= start[j] && my < start[j] + kk[j]) {
-            sm_sched[0] = 4 * lane + j;
-            sm_sched[1] = my - start[j];
-            sm_sched[2] = kk[j];
-            sm_sched[3] = sz[j];
-            sm_sched[4] = start[j];
-          }
+          kk[j] = splits_for(st[j], s, sz[j]);
+          start[j] = tot;
+          tot += kk[j];
         }
+        const int incl = wave_inclusive_sum(tot);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) start[j] += incl - tot;
+        return __builtin_amdgcn_readlane(incl, 63);
+      };
+      int s = max((W + U - 1) / U, a.min_split_steps);
+      int A = plan(s);
+      if (A > U) {
+        int lo = s + 1, hi = max(lo, (W + (U - a.pairs) - 1) / (U - a.pairs));
+        while (lo < hi) {
+          const int mid = (lo + hi) >> 1;
+          if (plan(mid) <= U) hi = mid;
+          else lo = mid + 1;
+        }
+        A = plan(lo);
       }
-      // the owner pair's sizes, from the lane that loaded them (the pair index is read
-      // back by the same wave: its own LDS write precedes the read)
-      wait_lds_all();
-      const int p = __builtin_amdgcn_readfirstlane(sm_sched[0]);
+      int my = 0;
+      const bool ok = A <= U && unit_of(A, my);
+      // the pair whose units contain this unit: one lane and slot holds it
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        if (p >= 0 && 4 * lane + j == p) {
-          sm_sched[5] = pn[j];
-          sm_sched[6] = pt[j];
-          sm_sched[7] = pc[j];
+        const uint64_t m = __ballot(ok && kk[j] && my >= start[j] && my < start[j] + kk[j]);
+        if (m) {
+          const int l = __builtin_ctzll(m);
+          p_new = 4 * l + j;
+          slot0 = __builtin_amdgcn_readlane(start[j], l);
+          nsplit = __builtin_amdgcn_readlane(kk[j], l);
+          split_steps = __builtin_amdgcn_readlane(sz[j], l);
+          split_new = my - slot0;
         }
       }
     }
-    lds_barrier();
-    // (read back as wave-uniform values, so that everything derived stays scalar)
-    const int p_new = __builtin_amdgcn_readfirstlane(sm_sched[0]);
-    const int split_new = __builtin_amdgcn_readfirstlane(sm_sched[1]);
-    nsplit = __builtin_amdgcn_readfirstlane(sm_sched[2]);
-    split_steps = __builtin_amdgcn_readfirstlane(sm_sched[3]);
-    slot0 = __builtin_amdgcn_readfirstlane(sm_sched[4]);
+    // (wave-uniform values, so that everything derived stays scalar)
+    p_new = __builtin_amdgcn_readfirstlane(p_new);
+    split_new = __builtin_amdgcn_readfirstlane(split_new);
+    nsplit = __builtin_amdgcn_readfirstlane(nsplit);
+    split_steps = __builtin_amdgcn_readfirstlane(split_steps);
+    slot0 = __builtin_amdgcn_readfirstlane(slot0);
     if (p_new < 0 || p_new >= a.pairs || slot0 < 0 || nsplit < 1 || slot0 + nsplit > U) return;
-    n_raw = __builtin_amdgcn_readfirstlane(sm_sched[5]);
-    t_raw = __builtin_amdgcn_readfirstlane(sm_sched[6]);
-    c_raw = __builtin_amdgcn_readfirstlane(sm_sched[7]);
+    // the pair's sizes, from the lane and slot that loaded them
+    const int ol = p_new >> 2, oj = p_new & 3;
+    auto owner = [&](const int (&v)[4]) {
+      return __builtin_amdgcn_readlane(oj == 0 ? v[0] : oj == 1 ? v[1] : oj == 2 ? v[2] : v[3], ol);
+    };
+    n_raw = owner(pn);
+    t_raw = owner(pt);
+    c_raw = owner(pc);
     if (p_new != pair || split_new * split_steps != s_begin) {  // the guess was wrong
       pair = p_new;
       s_begin = split_new * split_steps;
