@@ -153,6 +153,7 @@ dustin_status run_attention(bool sparse, const void* q, int64_t q_sb, int64_t q_
   if (num_q_heads <= 0 || Hkv <= 0 || num_q_heads % Hkv || v->num_kv_heads != Hkv)
     return DUSTIN_ERR_INVALID_ARG;
   if (k->head_dim != 128 || v->head_dim != 128) return DUSTIN_ERR_UNSUPPORTED;
+  if (bt->max_len > INT32_MAX - 64) return DUSTIN_ERR_UNSUPPORTED;  // positions N_b + t are int32
   if (k->page_table != v->page_table) return DUSTIN_ERR_INVALID_ARG;  // one table for K and V
   if (k->page_table && (k->page_size != v->page_size || k->max_pages != v->max_pages ||
                         k->num_pages != v->num_pages))

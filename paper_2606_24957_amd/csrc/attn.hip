@@ -387,18 +387,18 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
 
   // Position of virtual token v (clamped into the cache; past-the-end -> 0) and its
   // physical row.
-  auto pos_of = [&](int v, int32_t selected) -> int64_t {
-    int64_t pos;
-    if (v < wstart) pos = kSparse ? (int64_t)selected : (int64_t)v;
-    else if (v < total) pos = (int64_t)N + (v - wstart);
-    else pos = 0;
-    return pos < 0 ? 0 : (pos >= a.k.capacity ? a.k.capacity - 1 : pos);
+  // positions are 32-bit: N_b + T_b and the selected positions are int32 (a capacity
+  // beyond that bound leaves every int32 position inside it)
+  const int cap_m1 = (int)(a.k.capacity - 1 < INT32_MAX ? a.k.capacity - 1 : INT32_MAX - 1);
+  auto pos_of = [&](int v, int32_t selected) -> int {
+    const int pos = v < wstart ? (kSparse ? selected : v) : (v < total ? N + (v - wstart) : 0);
+    return clampi(pos, 0, cap_m1);
   };
-  auto page_of = [&](int64_t pos) -> int {
+  auto page_of = [&](int pos) -> int {
     return clampi(a.k.page_table[(int64_t)b * a.k.max_pages + (pos >> a.k.page_shift)], 0,
                   a.k.num_pages - 1);
   };
-  auto phys_at = [&](int64_t pos, int page) -> uint32_t {
+  auto phys_at = [&](int pos, int page) -> uint32_t {
     if constexpr (kPaged)
       return ((uint32_t)page << a.k.page_shift) | (uint32_t)(pos & ((1 << a.k.page_shift) - 1));
     else
@@ -569,7 +569,7 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
   // Physical rows of this thread's tokens in chunk cs (reads sel, and the page table).
   uint32_t staged[kStageBatch];
   auto stage_rows = [&](int cs) {
-    int64_t pos[kStageBatch];
+    int pos[kStageBatch];
     int page[kStageBatch];
 #pragma unroll
     for (int j = 0; j < kStageBatch; ++j) pos[j] = pos_of(cs * kStep + (int)threadIdx.x + j * kW * kWave, sel[j]);
