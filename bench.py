@@ -334,6 +334,22 @@ def cpu_baseline(s, layer0, est, n_seq):
     times["dense_layer"] = time.perf_counter() - t0
     f = s.B / nb
     us = {key: val * f * 1e6 for key, val in times.items()}
+    # one thread, one sequence: the sparse layer and the scores of sequence 0
+    threads = O.max_threads()
+    O.set_threads(1)
+    try:
+        s0 = slice(0, 1)
+        t0 = time.perf_counter()
+        O.attention(q[s0], k[s0], v[s0], seq[:1], scale, O.all_rows(1, nq[:1], s.num_q_heads),
+                    idx=idx[s0], count=cnt[s0])
+        one_sparse = (time.perf_counter() - t0) * s.B * 1e6
+        t0 = time.perf_counter()
+        O.score(bf16_bits(est.q_target[s0]), k[s0], seq[:1], [1], s.target_heads, scale,
+                num_kv_heads=s.num_kv_heads, groups=s.groups,
+                init=None if init is None else init[s0])
+        one_score = (time.perf_counter() - t0) * s.B * 1e6
+    finally:
+        O.set_threads(threads)
     return {
         "value": round(us["sparse_layer"], 1),
         "unit": "us/layer",
@@ -344,6 +360,8 @@ def cpu_baseline(s, layer0, est, n_seq):
                    f"layer; times scaled x{f:g} to the batch"),
         "dense_us_per_layer": round(us["dense_layer"], 1),
         "estimation_us_per_step": round(us["score_target"] + us["score_draft"] + us["select"], 1),
+        "one_thread": {"sparse_us_per_layer": round(one_sparse, 1), "target_score_us": round(one_score, 1),
+                       "sample": f"sequence 0 on one thread, times scaled x{s.B} to the batch"},
         "wall_s": round(sum(times.values()), 2),
     }
 
@@ -613,6 +631,7 @@ def main():
             "avg_launch_us": round(sp_us, 3),
             "timing": f"events around {L} back-to-back launches per step, divided by {L}",
             "avg_launch_us_with_event_between_launches": round(mean(sp_ev) * 1e3, 3) if sp_ev else None,
+            "overfetch": round(traffic / sb, 4) if traffic else None,
             "measured_copy_GBps": copy_gbps,
             "frac_of_measured_copy": round(achieved / copy_gbps, 4) if copy_gbps else None,
         },
