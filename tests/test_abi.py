@@ -245,3 +245,23 @@ def test_arr_rejects(L):
     assert call(hpg=0) == D.ERR_INVALID_ARG
     assert call(sb=-1) == D.ERR_INVALID_ARG
     assert call(b=None) == D.ERR_INVALID_ARG
+
+
+def test_score_per_layer_rejects(L):
+    kvs = (D.DustinKV * 2)(_kv(), _kv())
+    qs = (ctypes.c_void_p * 2)(FAKE, FAKE)
+    heads = (ctypes.c_int32 * 2)(0, 3)
+    bt = _batch()
+
+    def call(n=2, q=qs, kv=kvs, sl=1 << 20, out=FAKE, ws_bytes=1 << 30, nh=2, b=bt):
+        return L.dustin_score_per_layer(n, q, 800 * 8 * 128, 8 * 128, 128, 8, heads, nh, kv, ctypes.byref(b), 0.1,
+                                        1, out, sl, 0, 0, FAKE, ws_bytes, None)
+
+    assert call(n=0) == D.ERR_UNSUPPORTED
+    assert call(n=33) == D.ERR_UNSUPPORTED                            # at most 32 layers
+    assert call(sl=-1) == D.ERR_INVALID_ARG
+    assert call(out=None) == D.ERR_INVALID_ARG
+    assert call(ws_bytes=16) == D.ERR_WORKSPACE
+    other = (D.DustinKV * 2)(_kv(), _kv(cap=300))                     # layers must share the layout
+    assert call(kv=other) == D.ERR_INVALID_ARG
+    assert call(b=_batch(nq=17)) == D.ERR_UNSUPPORTED
