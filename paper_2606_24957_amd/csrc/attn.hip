@@ -268,11 +268,13 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
     int st[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) st[j] = 4 * lane + j < a.pairs ? steps_of(pn[j], pt[j], pc[j]) : 0;
-    // ceil(x / s) splits of size ceil(x / k), and with that size no empty trailing split
+    // k = ceil(x / s) splits of size ceil(x / k).  None of them is empty: with that size
+    // ceil(x / size) = k again (size <= s gives x / size >= x / s, and size >= x / k gives
+    // x / size <= k).
     auto splits_for = [](int x, int s, int& size) {
       const int k0 = x ? small_div(x + s - 1, s) : 0;
       size = k0 ? small_div(x + k0 - 1, k0) : 0;
-      return k0 ? small_div(x + size - 1, size) : 0;
+      return k0;
     };
     const int st0 = __builtin_amdgcn_readfirstlane(st[0]);
     bool differs = false;
@@ -297,6 +299,13 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) loc += st[j];
       const int W = __builtin_amdgcn_readlane(wave_inclusive_sum(loc), 63);
+      // the number of units split size s needs (one division per pair: the search's probe)
+      auto units_for = [&](int s) {
+        int tot = 0;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) tot += st[j] ? small_div(st[j] + s - 1, s) : 0;
+        return __builtin_amdgcn_readlane(wave_inclusive_sum(tot), 63);
+      };
       // splits per pair for split size s, each pair's first unit, and the total
       auto plan = [&](int s) {
         int tot = 0;
@@ -312,16 +321,16 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
         return __builtin_amdgcn_readlane(incl, 63);
       };
       int s = max((W + U - 1) / U, a.min_split_steps);
-      int A = plan(s);
-      if (A > U) {
+      if (units_for(s) > U) {
         int lo = s + 1, hi = max(lo, (W + (U - a.pairs) - 1) / (U - a.pairs));
         while (lo < hi) {
           const int mid = (lo + hi) >> 1;
-          if (plan(mid) <= U) hi = mid;
+          if (units_for(mid) <= U) hi = mid;
           else lo = mid + 1;
         }
-        A = plan(lo);
+        s = lo;
       }
+      const int A = plan(s);
       int my = 0;
       const bool ok = A <= U && unit_of(A, my);
       // the pair whose units contain this unit: one lane and slot holds it
