@@ -89,6 +89,12 @@ CASES = {
     "gamma8_rows72": (2, 900, 9, 64, 8, 200, False),
     "group16_rows64": (1, 1000, 4, 32, 2, 128, False),
     "ragged_paged": (3, [700, 1234, 95], [3, 9, 6], 64, 8, 160, True),
+    # six and eight row tiles, up to the 128 rows per KV head the kernels take
+    "rows96_rt6": (2, 1000, 12, 64, 8, 200, False),
+    "rows112_rt8": (1, 1500, 14, 64, 8, 300, False),
+    "rows128_max": (2, 1200, 16, 64, 8, 256, False),
+    "group16_rows128": (1, 1100, 8, 32, 2, 256, False),
+    "ragged_paged_rows128": (3, [900, 1300, 60], [16, 2, 11], 64, 8, 160, True),
 }
 
 
@@ -98,7 +104,8 @@ def test_sparse_matches_oracle(name):
     _run_sparse_case(_shape(B, n, t, Hq, Hkv, k, paged, name=name), G=1, seed=3, short=(0,))
 
 
-@pytest.mark.parametrize("name", ["qwen7b_like", "single_query", "ragged_paged", "gamma8_rows72"])
+@pytest.mark.parametrize("name", ["qwen7b_like", "single_query", "ragged_paged", "gamma8_rows72", "rows96_rt6",
+                                  "rows128_max", "ragged_paged_rows128"])
 def test_dense_matches_oracle(name):
     B, n, t, Hq, Hkv, k, paged = CASES[name]
     _run_dense_case(_shape(B, n, t, Hq, Hkv, k, paged, name=name))

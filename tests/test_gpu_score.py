@@ -93,7 +93,8 @@ def test_score_full_size_target_and_draft():
         check_score(host(sd)[b, 0, :s.seq_lens[b]], rd[0, 0, :s.seq_lens[b]], s.seq_lens[b], f"draft b={b}")
 
 
-@pytest.mark.parametrize("n_layers,with_init,paged", [(3, False, False), (2, True, False), (3, False, True)])
+@pytest.mark.parametrize("n_layers,with_init,paged", [(3, False, False), (2, True, False), (3, False, True),
+                                                       (32, True, False)])
 def test_score_layers_sums_layers_in_one_call(n_layers, with_init, paged):
     """dustin_score_layers: Eq. 5 summed over layers in two launches equals init plus the
     oracle's per-layer scores, summed in fp64."""
@@ -155,6 +156,12 @@ def test_score_all_target_heads():
     """Every head of a Qwen2.5-72B-shaped layer (the naive estimator's per-layer work):
     64 heads, 2 queries, 16 pairs per KV head."""
     _case(2, 0, 2, 64, 8, 128, list(range(64)), n_list=[2000, 555], seed=7)
+
+
+def test_score_maximum_rows():
+    """The largest score call: 64 heads times 16 queries, 1024 (head, query) rows, eight
+    column tiles per KV head."""
+    _case(2, 0, 16, 64, 8, 128, list(range(64)), n_list=[1500, 301], seed=8)
 
 
 @pytest.mark.parametrize("groups", [1, 2])

@@ -67,7 +67,7 @@ def test_topk_bit_exact(kind):
     _compare(_scores(kind, B, N, 1), _scores(kind, B, N, 2), [N] * B, k)
 
 
-@pytest.mark.parametrize("N", [21, 33, 1000, 4097, 32768, 131072])
+@pytest.mark.parametrize("N", [21, 33, 1000, 4097, 32768, 131072, 1 << 19])
 def test_topk_lengths(N):
     k = min(2048, max(20, N // 8))
     _compare(_scores("uniform", 2, N, N), _scores("dirichlet", 2, N, N + 1), [N, N - 1], k)
