@@ -97,12 +97,16 @@ __device__ __forceinline__ int wave_inclusive_sum(int v) {
   return v;
 }
 
-// floor(a / b) for 0 <= a < 2^22 and b >= 1: the fp32 reciprocal estimate is within one of
-// the quotient there, and one correction each way makes it exact.
+// floor(a / b) for 0 <= a < 2^22 and 1 <= b < 2^22: the fp32 reciprocal estimate is within
+// one of the quotient there, and one correction each way makes it exact.  The products
+// checked, q b and (q + 1) b with q at most one above the quotient, stay below 2^23, so
+// 24-bit multiplies are exact.  (A plain 32-bit multiply-add is lowered to a 64-bit
+// multiply-add whose unused high addend can land in a register with a load still pending,
+// and the wait for that load then stalls this arithmetic behind every earlier load.)
 __device__ __forceinline__ int small_div(int a, int b) {
   int q = (int)((float)a * __builtin_amdgcn_rcpf((float)b));
-  q -= q * b > a ? 1 : 0;
-  q += (q + 1) * b <= a ? 1 : 0;
+  q -= (int)__umul24((unsigned)q, (unsigned)b) > a ? 1 : 0;
+  q += (int)__umul24((unsigned)(q + 1), (unsigned)b) <= a ? 1 : 0;
   return q;
 }
 
@@ -237,21 +241,49 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
       for (int i = 0; i < 8; ++i) first_sel[i] = idx_row[min(first_v0 + i, a.dims.k_max - 1)];
     }
   };
-  prologue_loads();
-  // sizes of pairs 4 lane .. 4 lane + 3 (every wave; issued with the prologue loads)
+  if constexpr (kPaged) prologue_loads();
+  // sizes of pairs 4 lane .. 4 lane + 3 (every wave).  With a contiguous cache they are
+  // issued before the prologue loads, so that waiting for them leaves those in flight while
+  // the schedule is planned; with a paged cache the positions go first, since they feed
+  // the page-table lookups of the first rows (each order measured faster for its kind).
+  // Buffer loads at 32-bit offsets computed up front: 64-bit address arithmetic between
+  // the loads had the compiler reuse a register of a pending load, and the wait for it
+  // (vmcnt(0)) held back the later loads until every earlier one had returned.
   // (unconditional loads: a lane past the last pair reads the last pair's sizes, which
   // count for nothing, see steps_of's callers)
   int pn[4], pt[4], pc[4];
   if (balance) {
+    const int nb = small_div(a.pairs, a.num_kv_heads);  // the batch (pairs <= 256 here)
+    int on[4], oc[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int p = min(4 * lane + j, a.pairs - 1);
       const int pb = small_div(p, a.num_kv_heads), pg = p - pb * a.num_kv_heads;
-      pn[j] = a.dims.seq_lens[pb];
-      pt[j] = a.dims.n_query ? a.dims.n_query[pb] : a.dims.nq_max;
-      pc[j] = kSparse ? a.count[pb * a.groups + (a.groups == 1 ? 0 : pg)] : 0;
+      on[j] = pb * 4;
+      oc[j] = (pb * a.groups + (a.groups == 1 ? 0 : pg)) * 4;
+    }
+    const auto rs_n = __builtin_amdgcn_make_buffer_rsrc(const_cast<int32_t*>(a.dims.seq_lens), 0, nb * 4, 0x00020000);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) pn[j] = __builtin_amdgcn_raw_buffer_load_b32(rs_n, on[j], 0, 0);
+    if (a.dims.n_query) {  // kernel-uniform
+      const auto rs_t = __builtin_amdgcn_make_buffer_rsrc(const_cast<int32_t*>(a.dims.n_query), 0, nb * 4, 0x00020000);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) pt[j] = __builtin_amdgcn_raw_buffer_load_b32(rs_t, on[j], 0, 0);
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) pt[j] = a.dims.nq_max;
+    }
+    if constexpr (kSparse) {
+      const auto rs_c = __builtin_amdgcn_make_buffer_rsrc(const_cast<int32_t*>(a.count), 0, nb * a.groups * 4,
+                                                          0x00020000);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) pc[j] = __builtin_amdgcn_raw_buffer_load_b32(rs_c, oc[j], 0, 0);
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) pc[j] = 0;
     }
   }
+  if constexpr (!kPaged) prologue_loads();
 
   // 32-token steps of a pair: its selected (or all) positions, then its window
   auto steps_of = [&](int n, int t, int c) {
