@@ -757,22 +757,35 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
   const int nel = rows * (kD / 4);
   f32x4 o[KE];
   float Mk[KE], Lk[KE];
+  // Every LDS read of the merge is issued before any of its arithmetic.  (Written as one
+  // loop, the compiler waited for each batch of reads in turn, some thirty LDS round trips
+  // in a row.)
+  float mw[KE][kNB], lw[KE][kNB];
+  f32x4 xw[KE][kNB];
 #pragma unroll
   for (int k = 0; k < KE; ++k) {
     const int e = min((int)threadIdx.x + k * nthreads, nel - 1);
     const int r = e / (kD / 4), c0 = (e % (kD / 4)) * 4;
+#pragma unroll
+    for (int w = 0; w < kNB; ++w) {
+      mw[k][w] = sm_m[w][r];
+      lw[k][w] = sm_l[w][r];
+      xw[k][w] = *reinterpret_cast<const f32x4*>(bufs + w * kBufFloats + r * kPitch + c0);
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < KE; ++k) {
     float M = -INFINITY;
 #pragma unroll
-    for (int w = 0; w < kNB; ++w) M = fmaxf(M, sm_m[w][r]);
+    for (int w = 0; w < kNB; ++w) M = fmaxf(M, mw[k][w]);
     const float Mu = M == -INFINITY ? 0.f : M;
     float L = 0.f;
     f32x4 sum = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int w = 0; w < kNB; ++w) {
-      const float mw = sm_m[w][r];
-      const float f = mw == -INFINITY ? 0.f : fast_exp2(mw - Mu);
-      L += sm_l[w][r] * f;
-      sum += *reinterpret_cast<const f32x4*>(bufs + w * kBufFloats + r * kPitch + c0) * f;
+      const float f = mw[k][w] == -INFINITY ? 0.f : fast_exp2(mw[k][w] - Mu);
+      L += lw[k][w] * f;
+      sum += xw[k][w] * f;
     }
     o[k] = sum;
     Mk[k] = M;
