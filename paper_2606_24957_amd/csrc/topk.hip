@@ -173,11 +173,15 @@ struct KeyStage {
   }
 };
 
-// ORs the ballot of the 64 positions starting at n (a multiple of 64) into the bitmap.
+// ORs the ballot of the 64 positions starting at n (a multiple of 64) into the bitmap, with
+// LDS atomic ORs whose result is not used: one instruction each and no wait, where a read,
+// OR and write would wait for the read (the word is the calling wave's alone either way).
 __device__ __forceinline__ void mark64(uint32_t* bm, int n, int N, uint64_t m) {
   const int lane = threadIdx.x & (kWave - 1);
-  if (lane == 0 && n < N && (uint32_t)m) bm[n >> 5] |= (uint32_t)m;
-  if (lane == 32 && n + 32 < N && (uint32_t)(m >> 32)) bm[(n >> 5) + 1] |= (uint32_t)(m >> 32);
+  if (lane == 0 && n < N && (uint32_t)m)
+    __hip_atomic_fetch_or(&bm[n >> 5], (uint32_t)m, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  if (lane == 32 && n + 32 < N && (uint32_t)(m >> 32))
+    __hip_atomic_fetch_or(&bm[(n >> 5) + 1], (uint32_t)(m >> 32), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
 
 __device__ void select_tier(TopkSmem& s, KeyStage& ks, uint32_t need, uint32_t* bm) {
