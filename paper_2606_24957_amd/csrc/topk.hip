@@ -52,15 +52,16 @@ __device__ __forceinline__ void hist_add(uint32_t* hist, uint32_t bin, bool acti
 struct TopkSmem {
   uint32_t hist[kBins1];
   uint32_t wave_cnt[kTopkWaves];
+  uint32_t digit_cnt[kTopkWaves];  // find_digit's own per-wave sums (see there)
   uint32_t misc[4];
 };
 
-// Exclusive prefix over the 16 per-wave counts (after a barrier) and their total.
-__device__ __forceinline__ uint32_t wave_offset(const TopkSmem& s, int wave, uint32_t* total) {
+// Exclusive prefix over 16 per-wave counts (after a barrier) and their total.
+__device__ __forceinline__ uint32_t wave_offset(const uint32_t* cnt, int wave, uint32_t* total) {
   uint32_t off = 0, tot = 0;
 #pragma unroll
   for (int w = 0; w < kTopkWaves; ++w) {
-    const uint32_t c = s.wave_cnt[w];
+    const uint32_t c = cnt[w];
     off += w < wave ? c : 0u;
     tot += c;
   }
@@ -73,39 +74,52 @@ __device__ __forceinline__ uint32_t block_offsets(TopkSmem& s, uint32_t wave_cou
   const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
   if (lane == 0) s.wave_cnt[wave] = wave_count;
   __syncthreads();
-  const uint32_t off = wave_offset(s, wave, total);
+  const uint32_t off = wave_offset(s.wave_cnt, wave, total);
   __syncthreads();
   return off;
 }
 
-// The digit where the count of keys from the top of hist[0..nbins) reaches `remaining`;
-// writes (digit, remaining within that digit) to s.misc[0..1].
-__device__ void find_digit(TopkSmem& s, int nbins, uint32_t remaining) {
+// The digit where the count of keys from the top of hist[0..kN) reaches `remaining`;
+// writes (digit, remaining within that digit) to s.misc[0..1].  Each thread reads its own
+// bins once, keeps them in registers and returns them to zero, so that hist[0..kN) is zero
+// again when this returns (the next histogram over at most kN bins needs no clearing).
+// Its scan goes through digit_cnt, not wave_cnt, which other waves may still be reading
+// when a wave enters here.
+template <int kN>
+__device__ void find_digit(TopkSmem& s, uint32_t remaining) {
+  constexpr int per = kN / kTopkThreads;
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
-  const int per = nbins / kTopkThreads;
   const int lo = (kTopkThreads - 1 - tid) * per;  // thread 0 owns the highest bins
+  uint32_t v[per];
   uint32_t mine = 0;
-  for (int i = 0; i < per; ++i) mine += s.hist[lo + i];
+#pragma unroll
+  for (int i = 0; i < per; ++i) {
+    v[i] = s.hist[lo + i];
+    mine += v[i];
+  }
+#pragma unroll
+  for (int i = 0; i < per; ++i) s.hist[lo + i] = 0u;
   uint32_t inc = mine;  // inclusive scan in tid order = from the top bin down
 #pragma unroll
   for (int off = 1; off < kWave; off <<= 1) {
     const uint32_t y = __shfl_up(inc, off);
     if (lane >= off) inc += y;
   }
-  if (lane == kWave - 1) s.wave_cnt[wave] = inc;
+  if (lane == kWave - 1) s.digit_cnt[wave] = inc;
   __syncthreads();
   uint32_t tot;
-  const uint32_t above = wave_offset(s, wave, &tot) + inc - mine;  // keys in higher bins
+  const uint32_t above = wave_offset(s.digit_cnt, wave, &tot) + inc - mine;  // keys in higher bins
   if (above < remaining && above + mine >= remaining) {
     uint32_t run = above;
+    bool found = false;
+#pragma unroll
     for (int i = per - 1; i >= 0; --i) {
-      const uint32_t c = s.hist[lo + i];
-      if (run + c >= remaining) {
+      if (!found && run + v[i] >= remaining) {
         s.misc[0] = (uint32_t)(lo + i);
         s.misc[1] = remaining - run;
-        break;
+        found = true;
       }
-      run += c;
+      run += v[i];
     }
   }
   __syncthreads();
@@ -210,7 +224,10 @@ __device__ void select_tier(TopkSmem& s, KeyStage& ks, uint32_t need, uint32_t* 
       }
     }
     __syncthreads();
-    find_digit(s, nbins, remaining);
+    if (pass == 0)
+      find_digit<kBins1>(s, remaining);
+    else
+      find_digit<kBins>(s, remaining);
     prefix |= s.misc[0] << sh;
     pmask |= dmask << sh;
     remaining = s.misc[1];
@@ -322,7 +339,7 @@ __device__ void select_tier_fast(TopkSmem& s, KeyStage& ks, uint32_t need, uint3
     }
   }
   __syncthreads();
-  find_digit(s, kBins1, need);
+  find_digit<kBins1>(s, need);
   const uint32_t d1 = s.misc[0], r1 = s.misc[1];
 
   // ---- B (each wave appends to its own slice of the candidate list)
@@ -358,6 +375,7 @@ __device__ void select_tier_fast(TopkSmem& s, KeyStage& ks, uint32_t need, uint3
     }
   }
   if (lane == 0) s.wave_cnt[wave] = wcount;
+  if (tid == 0) s.misc[3] = 0u;  // the tie count below
   __syncthreads();
   bool overflow = false;
 #pragma unroll
@@ -373,14 +391,13 @@ __device__ void select_tier_fast(TopkSmem& s, KeyStage& ks, uint32_t need, uint3
   uint32_t prefix = d1 << 20, pmask = 4095u << 20, remaining = r1;
   for (int pass = 0; pass < 2; ++pass) {
     const int sh = pass == 0 ? 10 : 0;
-    for (int i = tid; i < kBins; i += kTopkThreads) s.hist[i] = 0u;
-    __syncthreads();
+    // hist is zero here: the previous find_digit left it so
     for (uint32_t c = lane; c < wcount; c += kWave) {
       const uint32_t key = wlist[2 * c];
       if ((key & pmask) == prefix) atomicAdd(&s.hist[(key >> sh) & 1023u], 1u);
     }
     __syncthreads();
-    find_digit(s, kBins, remaining);
+    find_digit<kBins>(s, remaining);
     prefix |= s.misc[0] << sh;
     pmask |= 1023u << sh;
     remaining = s.misc[1];
@@ -389,8 +406,6 @@ __device__ void select_tier_fast(TopkSmem& s, KeyStage& ks, uint32_t need, uint3
 
   // ---- candidates above tau are taken; the ties at tau are collected
   uint32_t* const ties = s.hist;  // positions of the candidates equal to tau
-  if (tid == 0) s.misc[3] = 0u;
-  __syncthreads();
   for (uint32_t c = lane; c < wcount; c += kWave) {
     const uint32_t key = wlist[2 * c], n = wlist[2 * c + 1];
     if (key > tau) {
@@ -447,15 +462,14 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(TopkArgs a, int seg)
   uint32_t* bm = dyn + seg;
   // protected positions (and the padding past N) start out taken
   const int nwords = (N + 31) / 32;
-  for (int w = tid; w < nwords; w += kTopkThreads) {
-    uint32_t bits = 0;
-    const int n0 = w * 32;
-    for (int i = 0; i < 32; ++i) {
-      const int n = n0 + i;
-      if (n >= N || n < a.n_sink || n >= N - a.n_window) bits |= 1u << i;
-    }
-    bm[w] = bits;
-  }
+  // (bit i of word w is position 32 w + i; taken: below n_sink, or at or above N - n_window,
+  // which includes every position at or above N)
+  auto below = [](int x, int n0) -> uint32_t {  // bits i with n0 + i < x
+    const int c = x - n0;
+    return c <= 0 ? 0u : (c >= 32 ? ~0u : (1u << c) - 1u);
+  };
+  for (int w = tid; w < nwords; w += kTopkThreads)
+    bm[w] = below(a.n_sink, w * 32) | ~below(N - a.n_window, w * 32);
   // a row shorter than the segment uses a shorter one (still a multiple of kSegQuantum)
   const int rseg = min(seg, (N + kSegQuantum - 1) / kSegQuantum * kSegQuantum);
   KeyStage ks{nullptr, dyn, bm, N, rseg, (N + rseg - 1) / rseg, -1};
