@@ -199,6 +199,12 @@ constexpr int kFinishBatch = 8;  // logits rows loaded together per thread
 // order (every layer, or layer lo alone when each layer has its own output), with each
 // row's softmax max M (log2 domain) and 1 / Z merged from the pass-1 chunk statistics.
 // Returns the number of rows.
+// Rows up to which a wave merges each row's chunk statistics (one round trip); past it one
+// thread per row does (the same count for every caller, so a row's merge never depends on
+// the workgroup size of the kernel that calls this).
+constexpr int kFinishFewRows = 16;
+
+template <int kThreads>
 __device__ int finish_setup(const ScoreArgs& a, int b, int go, int lo, int nq, int n_rows, int* sm_row,
                             float* sm_M, float* sm_iz, int* sm_slots, int* sm_ns) {
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
@@ -211,15 +217,15 @@ __device__ int finish_setup(const ScoreArgs& a, int b, int go, int lo, int nq, i
   __syncthreads();
   const int ns = *sm_ns, per_layer = ns * nq;
   const int l0 = a.per_layer ? lo : 0, np = (a.per_layer ? 1 : a.n_layers) * per_layer;
-  for (int i = tid; i < np; i += kFinishThreads) {
+  for (int i = tid; i < np; i += kThreads) {
     const int l = l0 + i / per_layer, r = i % per_layer, s = r / nq, j = r - s * nq;
     sm_row[i] = ((l * a.batch + b) * a.n_heads + sm_slots[s]) * a.nq_max + j;
   }
   __syncthreads();
   const int nch = (n_rows + a.chunk - 1) / a.chunk;
-  if (np <= kFinishThreads / kWave * 4) {
-    // few rows: each wave merges every fourth row, one chunk per lane (one round trip)
-    for (int i = wave; i < np; i += kFinishThreads / kWave) {
+  if (np <= kFinishFewRows) {
+    // few rows: the waves take the rows in turn, one chunk per lane (one round trip)
+    for (int i = wave; i < np; i += kThreads / kWave) {
       const float* st = a.stats + (int64_t)sm_row[i] * a.n_chunks * 2;
       float M = -INFINITY;
       for (int c = lane; c < nch; c += kWave) M = fmaxf(M, st[2 * c]);
@@ -236,7 +242,7 @@ __device__ int finish_setup(const ScoreArgs& a, int b, int go, int lo, int nq, i
   } else {
     // many rows: one row per thread, its chunks' (max, sum) loaded kFinishBatch at a time
     // and merged in chunk order
-    for (int i = tid; i < np; i += kFinishThreads) {
+    for (int i = tid; i < np; i += kThreads) {
       const float2* st = reinterpret_cast<const float2*>(a.stats + (int64_t)sm_row[i] * a.n_chunks * 2);
       float M = -INFINITY, Z = 0.f;
       for (int c0 = 0; c0 < nch; c0 += kFinishBatch) {
@@ -271,7 +277,7 @@ __global__ __launch_bounds__(kFinishThreads) void score_finish_kernel(ScoreArgs 
   __shared__ float sm_M[kScoreMaxPairs], sm_iz[kScoreMaxPairs];
   __shared__ int sm_slots[kScoreMaxHeads];
   __shared__ int sm_ns;
-  const int np = finish_setup(a, b, go, lo, nq, N, sm_row, sm_M, sm_iz, sm_slots, &sm_ns);
+  const int np = finish_setup<kFinishThreads>(a, b, go, lo, nq, N, sm_row, sm_M, sm_iz, sm_slots, &sm_ns);
 
   // four consecutive positions per thread (the logits rows are 64-element aligned, so
   // the vector load stays inside a row even past N)
@@ -309,7 +315,12 @@ __global__ __launch_bounds__(kFinishThreads) void score_finish_kernel(ScoreArgs 
 // Page mode: kScoreFinishPages pages per workgroup; wave w sums the rows i = w mod 4 of
 // lane's page, the four partial sums are added in wave order, and every position of the
 // page below N_b receives init + the page's sum.
-__global__ __launch_bounds__(kFinishThreads) void score_finish_pages_kernel(ScoreArgs a) {
+// 16 waves per workgroup: each wave's share of a page's rows (320 with every head of a
+// Qwen2.5-72B-shaped layer) is loaded in two batches instead of five, and a CU keeps about
+// twice as many loads in flight.
+constexpr int kFinishPagesThreads = 1024;
+
+__global__ __launch_bounds__(kFinishPagesThreads) void score_finish_pages_kernel(ScoreArgs a) {
   const int chunk = blockIdx.x, go = blockIdx.y % a.groups, lo = blockIdx.y / a.groups, b = blockIdx.z;
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
   const int N = a.dims.len(b);
@@ -322,14 +333,14 @@ __global__ __launch_bounds__(kFinishThreads) void score_finish_pages_kernel(Scor
   __shared__ float sm_M[kScoreMaxPairs], sm_iz[kScoreMaxPairs];
   __shared__ int sm_slots[kScoreMaxHeads];
   __shared__ int sm_ns;
-  __shared__ float sm_acc[kFinishThreads / kWave][kScoreFinishPages];
-  const int np = finish_setup(a, b, go, lo, nq, P, sm_row, sm_M, sm_iz, sm_slots, &sm_ns);
+  __shared__ float sm_acc[kFinishPagesThreads / kWave][kScoreFinishPages];
+  const int np = finish_setup<kFinishPagesThreads>(a, b, go, lo, nq, P, sm_row, sm_M, sm_iz, sm_slots, &sm_ns);
 
   static_assert(kScoreFinishPages == kWave, "one page per lane");
   const int p = p0 + lane;
   const bool live = p < P;
   float acc = 0.f;
-  constexpr int kWaves = kFinishThreads / kWave;
+  constexpr int kWaves = kFinishPagesThreads / kWave;
   constexpr int kBatch = 2 * kFinishBatch;  // rows loaded together per lane
   for (int i0 = wave; i0 < np; i0 += kWaves * kBatch) {
     float x[kBatch];
@@ -350,7 +361,7 @@ __global__ __launch_bounds__(kFinishThreads) void score_finish_pages_kernel(Scor
   const float* init_row = a.init ? a.init + (int64_t)b * a.init_sb + (int64_t)go * a.init_sg : nullptr;
   float* out_row = a.out + (int64_t)b * a.out_sb + (int64_t)go * a.out_sg + (int64_t)lo * a.out_sl;
   const int n_end = min(N, (p0 + kScoreFinishPages) << a.page_shift);
-  for (int n = (p0 << a.page_shift) + tid; n < n_end; n += kFinishThreads) {
+  for (int n = (p0 << a.page_shift) + tid; n < n_end; n += kFinishPagesThreads) {
     const int pp = (n >> a.page_shift) - p0;
     float v = sm_acc[0][pp];
 #pragma unroll
@@ -390,7 +401,7 @@ hipError_t launch_score(const ScoreArgs& a, int B, int n_groups, int max_group, 
   if (pages) {
     const int max_pages = (a.dims.max_len + (1 << a.page_shift) - 1) >> a.page_shift;
     dim3 grid2((max_pages + kScoreFinishPages - 1) / kScoreFinishPages, a.groups * outs, B);
-    hipLaunchKernelGGL(score_finish_pages_kernel, grid2, dim3(kFinishThreads), 0, stream, a);
+    hipLaunchKernelGGL(score_finish_pages_kernel, grid2, dim3(kFinishPagesThreads), 0, stream, a);
   } else {
     dim3 grid2((a.dims.max_len + kScoreFinishChunk - 1) / kScoreFinishChunk, a.groups * outs, B);
     hipLaunchKernelGGL(score_finish_kernel, grid2, dim3(kFinishThreads), 0, stream, a);
