@@ -167,18 +167,29 @@ class Call:
 _WS = {}
 
 
-def workspace(nbytes: int, device, tag: str) -> Optional[torch.Tensor]:
-    """A cached, zero-initialised device scratch buffer per (device, tag) of at least
-    nbytes (the attention kernels leave their counters at zero after each call)."""
+def workspace(nbytes: int, device, tag: str, stream=None) -> Optional[torch.Tensor]:
+    """A cached, zero-initialised device scratch buffer per (device, stream, tag) of at
+    least nbytes.  Calls that share a workspace must not overlap on the device (the split
+    attention's counters and partials, the score's logits); keying by stream keeps calls
+    planned on different streams apart, and calls on one stream run in order."""
     if nbytes == 0:
         return None
-    key = (str(device), tag)
+    s = torch.cuda.current_stream(device) if stream is None else stream
+    key = (str(torch.device(device)), int(s.cuda_stream), tag)
     buf = _WS.get(key)
     if buf is None or buf.numel() < nbytes:
         buf = torch.zeros(int(nbytes) + 256, dtype=torch.uint8, device=device)
         _WS[key] = buf
     off = (-buf.data_ptr()) % 256
     return buf[off:off + nbytes]
+
+
+def release_workspaces() -> None:
+    """Drops the cached workspaces (after synchronising the device), so that a program can
+    return their memory to the allocator before it exits."""
+    if _WS:
+        torch.cuda.synchronize()
+    _WS.clear()
 
 
 def kv_view(cache: torch.Tensor, page_table: Optional[torch.Tensor] = None) -> DustinKV:
@@ -258,7 +269,7 @@ def plan_score(q: torch.Tensor, k: torch.Tensor, seq_lens, heads: Sequence[int],
     heads_host = (ctypes.c_int32 * len(heads))(*[int(h) for h in heads])
     bt = _batch(B, max_len, nq_max, 0, seq, nqa)
     nbytes = lib().dustin_score_workspace(B, max_len, nq_max, len(heads))
-    ws = workspace(nbytes, dev, "score")
+    ws = workspace(nbytes, dev, "score", stream)
     scale = 1.0 / math.sqrt(d) if scale is None else scale
     ins = (init.stride(0), init.stride(1)) if init is not None else (0, 0)
     args = (_ptr(q), q.stride(0), q.stride(1), q.stride(2), Hq, heads_host, len(heads),
@@ -303,7 +314,7 @@ def plan_score_layers(qs: Sequence[torch.Tensor], ks: Sequence[torch.Tensor], se
     q_host = (ctypes.c_void_p * len(qs))(*[q.data_ptr() for q in qs])
     bt = _batch(B, max_len, nq_max, 0, seq, nqa)
     nbytes = lib().dustin_score_workspace(B, max_len, nq_max, len(heads) * len(qs))
-    ws = workspace(nbytes, dev, "score")
+    ws = workspace(nbytes, dev, "score", stream)
     scale = 1.0 / math.sqrt(d) if scale is None else scale
     ins = (init.stride(0), init.stride(1)) if init is not None else (0, 0)
     args = (len(qs), q_host, q0.stride(0), q0.stride(1), q0.stride(2), Hq, heads_host, len(heads),
@@ -349,7 +360,7 @@ def plan_score_per_layer(qs: Sequence[torch.Tensor], ks: Sequence[torch.Tensor],
     q_host = (ctypes.c_void_p * len(qs))(*[q.data_ptr() for q in qs])
     bt = _batch(B, max_len, nq_max, 0, seq, nqa)
     nbytes = lib().dustin_score_workspace(B, max_len, nq_max, len(heads) * len(qs))
-    ws = workspace(nbytes, dev, "score")
+    ws = workspace(nbytes, dev, "score", stream)
     scale = 1.0 / math.sqrt(d) if scale is None else scale
     args = (len(qs), q_host, q0.stride(0), q0.stride(1), q0.stride(2), Hq, heads_host, len(heads),
             kvs, ctypes.byref(bt), float(scale), int(groups), _ptr(out), out.stride(0), out.stride(1),
@@ -436,7 +447,7 @@ def plan_page_score(q: torch.Tensor, meta: torch.Tensor, seq_lens, heads: Sequen
     heads_host = (ctypes.c_int32 * len(heads))(*[int(h) for h in heads])
     bt = _batch(B, max_len, nq_max, 0, seq, nqa)
     nbytes = lib().dustin_page_score_workspace(B, max_len, int(page_size), nq_max, len(heads))
-    ws = workspace(nbytes, dev, "page_score")
+    ws = workspace(nbytes, dev, "page_score", stream)
     scale = 1.0 / math.sqrt(d) if scale is None else scale
     ins = (init.stride(0), init.stride(1)) if init is not None else (0, 0)
     args = (_ptr(q), q.stride(0), q.stride(1), q.stride(2), Hq, heads_host, len(heads), _ptr(meta),
@@ -567,7 +578,7 @@ def plan_sparse_verify_attn(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor,
     G, k_max = idx.shape[1], idx.shape[2]
     bt = _batch(B, max_len, nq_max, k_max, seq, nqa)
     nbytes = lib().dustin_attn_workspace(B, Hq, kv.num_kv_heads, nq_max, k_max, 1)
-    ws = workspace(nbytes, dev, "attn")
+    ws = workspace(nbytes, dev, "attn", stream)
     scale = 1.0 / math.sqrt(d) if scale is None else scale
     count = count.contiguous()
     args = (_ptr(q), q.stride(0), q.stride(1), q.stride(2), Hq, ctypes.byref(kv),
@@ -595,7 +606,7 @@ def plan_dense_verify_attn(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, se
     nqa = _i32_dev(n_query, dev)
     bt = _batch(B, max_len, nq_max, 0, seq, nqa)
     nbytes = lib().dustin_attn_workspace(B, Hq, kv.num_kv_heads, nq_max, max_len, 0)
-    ws = workspace(nbytes, dev, "attn")
+    ws = workspace(nbytes, dev, "attn", stream)
     scale = 1.0 / math.sqrt(d) if scale is None else scale
     args = (_ptr(q), q.stride(0), q.stride(1), q.stride(2), Hq, ctypes.byref(kv),
             ctypes.byref(vv), ctypes.byref(bt), float(scale), _ptr(out), out.stride(0),

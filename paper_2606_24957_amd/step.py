@@ -46,29 +46,31 @@ class VerifyStep:
         self.graph = None
         self.ops = self._plan()
 
-    def _plan(self) -> List:
-        """The step's operations, bound to the current stream."""
+    def _plan(self, stream=None) -> List:
+        """The step's operations, bound to `stream` (None: the current stream)."""
         s, est, N = self.s, self.est, self.s.n_max
         init = est.init_target
         if init is not None and s.groups > 1:  # one historical row, the same for every group
             init = init.expand(s.B, s.groups, N)
         ops = [plan_score(est.q_target, self.layers[0].k, self.seq, s.target_heads, groups=s.groups,
-                          init=init, out=self.s_t, max_len=N, page_table=self.layers[0].page_table)]
+                          init=init, out=self.s_t, max_len=N, page_table=self.layers[0].page_table,
+                          stream=stream)]
         if est.s_draft_given is not None:
             given = est.s_draft_given
             ops.append(lambda: self.s_d.copy_(given))
         else:
             ops.append(plan_score_layers(est.draft_q, est.draft_k, self.seq, s.draft.heads,
-                                         n_query=self.gam, out=self.s_d, max_len=N))
+                                         n_query=self.gam, out=self.s_d, max_len=N, stream=stream))
         ops.append(plan_topk(self.s_d, self.s_t, self.seq, s.k_max, budget=self.bud, m=self.mm,
                              n_sink=s.n_sink, n_window=s.n_window, groups=s.groups, idx=self.idx,
-                             count=self.cnt))
+                             count=self.cnt, stream=stream))
         for L, o, (k_new, v_new) in zip(self.layers, self.outs, self.windows):
             if self.append:
                 ops.append(plan_kv_append(k_new, v_new, L.k, L.v, self.seq, n_query=self.nq,
-                                          page_table=L.page_table, max_len=N))
+                                          page_table=L.page_table, max_len=N, stream=stream))
             ops.append(plan_sparse_verify_attn(L.q, L.k, L.v, self.idx, self.cnt, self.seq,
-                                               n_query=self.nq, page_table=L.page_table, out=o))
+                                               n_query=self.nq, page_table=L.page_table, out=o,
+                                               stream=stream))
         return ops
 
     def run(self):
@@ -76,16 +78,20 @@ class VerifyStep:
             op()
 
     def capture(self):
-        """Records the step in a HIP graph (after one eager run, so that every workspace
-        exists before capture)."""
+        """Records the step in a HIP graph on a capture stream of its own.  The capture
+        stream's workspaces are allocated (zeroed) by a planning pass before the capture
+        starts, so nothing is allocated or cleared while recording."""
         self.run()
+        cs = torch.cuda.Stream()
+        self._plan(stream=cs)
         torch.cuda.synchronize()
         g = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(g):
-            ops = self._plan()
+        with torch.cuda.graph(g, stream=cs):
+            ops = self._plan(stream=cs)
             for op in ops:
                 op()
         self._graph_ops = ops  # keeps the marshalled arguments alive
+        self._capture_stream = cs
         self.graph = g
         return g
 

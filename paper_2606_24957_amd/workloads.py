@@ -321,3 +321,34 @@ def bf16_bits(t: torch.Tensor):
     """Raw uint16 patterns of a bf16 tensor as a numpy array (host copy)."""
     import numpy as np
     return t.detach().cpu().contiguous().view(torch.int16).numpy().view(np.uint16)
+
+
+def plant_ramp(s: Shape, layer: Layer, positions, coefs, window_coef: Optional[float] = None,
+               window_slot: int = 1):
+    """Peaked attention for the parity tests: K[b, p_j, g] = bf16(c_j * mean(q over the KV
+    head's query rows)) for the positions p_j of positions[b] and the coefficients c_j
+    (the same positions in every KV head), and, when window_coef is given, the same with
+    window_coef at window position N_b + window_slot (seen by queries t >= window_slot).
+    With queries scaled by a power of two beforehand, these keys' logits lie tens of units
+    apart, so an online softmax meets its running maximum at many steps.  Writes through
+    the page table when the layer is paged."""
+    Hkv, d, gs = s.num_kv_heads, s.head_dim, s.group_size
+    for b in range(s.B):
+        t = s.n_query[b]
+        if t == 0:
+            continue
+        rows = layer.q[b, :t].float()  # [t, Hq, d]
+        qbar = rows.reshape(t, Hkv, gs, d).mean(dim=(0, 2))  # [Hkv, d]
+        pos = list(positions[b]) if positions is not None else []
+        coef = list(coefs)[:len(pos)]
+        if window_coef is not None and window_slot < t:
+            pos.append(s.seq_lens[b] + window_slot)
+            coef.append(window_coef)
+        for p, c in zip(pos, coef):
+            row = (float(c) * qbar).to(torch.bfloat16)  # [Hkv, d]
+            if layer.page_table is None:
+                layer.k[b, int(p)] = row
+            else:
+                ps = s.page_size
+                page = int(layer.page_table[b, int(p) // ps].item())
+                layer.k[page, int(p) % ps] = row
