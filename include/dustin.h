@@ -61,7 +61,9 @@ typedef enum {
   DUSTIN_ERR_INVALID_ARG = 1, /* null pointer, bad size, bad stride or alignment         */
   DUSTIN_ERR_UNSUPPORTED = 2, /* valid but not implemented (head_dim, rows per group...) */
   DUSTIN_ERR_WORKSPACE = 3,   /* workspace missing, misaligned or smaller than required   */
-  DUSTIN_ERR_LAUNCH = 4       /* the HIP runtime refused a launch                          */
+  DUSTIN_ERR_LAUNCH = 4,      /* the HIP runtime refused a launch                          */
+  DUSTIN_ERR_SCRATCH_LIMIT = 5 /* more split scratch than dustin_sparse_verify_attn_noalloc's
+                                  fixed array holds                                        */
 } dustin_status;
 
 /* A bf16 K or V cache of one layer.
@@ -320,6 +322,35 @@ dustin_status dustin_sparse_verify_attn(const void* q, int64_t q_sb, int64_t q_s
                                         const int32_t* count, int32_t groups, float scale,
                                         void* out, int64_t o_sb, int64_t o_st, int64_t o_sh,
                                         void* workspace, size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------------
+ * dustin_sparse_verify_attn_noalloc -- dustin_sparse_verify_attn for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc): the same arguments without the workspace, the same kernels and
+ * the same split schedule, so the output is bit-identical to dustin_sparse_verify_attn's.
+ * It calls no hipMalloc or hipFree.
+ *
+ * Scratch: the split partials and counters live in a fixed device array of the library,
+ * DUSTIN_NOALLOC_SCRATCH_BYTES (48 MiB) per GPU, held until the process ends.  A call that
+ * needs more than that (dustin_attn_workspace(..., sparse = 1) > the limit) returns
+ * DUSTIN_ERR_SCRATCH_LIMIT with nothing enqueued; at the headline shape (B = 16, 8 KV
+ * heads, 40 rows per KV head) a call needs 6.6 MB.  The first call on a device looks the
+ * array up and enqueues one small fill kernel on `stream` that zeroes its counter region:
+ * make that first call outside graph capture.  Every call on one GPU shares that GPU's array, which keeps
+ * the last call's contents (the counters return to zero after each call): calls that
+ * overlap on one GPU, on any streams, race and give wrong outputs.
+ * Returns as dustin_sparse_verify_attn, plus DUSTIN_ERR_SCRATCH_LIMIT, or
+ * DUSTIN_ERR_LAUNCH when the array cannot be found on the current device.
+ * --------------------------------------------------------------------------------- */
+#define DUSTIN_NOALLOC_SCRATCH_BYTES (48u << 20)
+dustin_status dustin_sparse_verify_attn_noalloc(const void* q, int64_t q_sb, int64_t q_st,
+                                                int64_t q_sh, int32_t num_q_heads,
+                                                const dustin_kv* k, const dustin_kv* v,
+                                                const dustin_batch* bt, const int32_t* idx,
+                                                int64_t idx_sb, int64_t idx_sg,
+                                                const int32_t* count, int32_t groups,
+                                                float scale, void* out, int64_t o_sb,
+                                                int64_t o_st, int64_t o_sh, void* stream);
 
 /* ---------------------------------------------------------------------------------
  * dense_verify_attn -- full-cache verification attention (the baseline every speedup

@@ -23,13 +23,14 @@ import torch
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libdustin.so")
 
-OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_LAUNCH = range(5)
+OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_LAUNCH, ERR_SCRATCH_LIMIT = range(6)
 
 EXPORTED = ("dustin_status_string", "dustin_version", "dustin_score_workspace", "dustin_score",
             "dustin_topk_workspace", "dustin_topk", "dustin_attn_workspace",
             "dustin_sparse_verify_attn", "dense_verify_attn", "dustin_kv_append", "dustin_kv_commit",
             "dustin_score_layers", "dustin_page_meta", "dustin_page_score_workspace",
-            "dustin_page_score", "dustin_arr", "dustin_score_per_layer")
+            "dustin_page_score", "dustin_arr", "dustin_score_per_layer",
+            "dustin_sparse_verify_attn_noalloc")
 
 
 class DustinError(RuntimeError):
@@ -88,6 +89,10 @@ def lib():
         L.dustin_sparse_verify_attn.argtypes = [_vp, _i64, _i64, _i64, _i32, P_KV, P_KV, P_BT,
                                                 _vp, _i64, _i64, _vp, _i32, ctypes.c_float,
                                                 _vp, _i64, _i64, _i64, _vp, _sz, _vp]
+        L.dustin_sparse_verify_attn_noalloc.restype = ctypes.c_int
+        L.dustin_sparse_verify_attn_noalloc.argtypes = [_vp, _i64, _i64, _i64, _i32, P_KV, P_KV, P_BT,
+                                                        _vp, _i64, _i64, _vp, _i32, ctypes.c_float,
+                                                        _vp, _i64, _i64, _i64, _vp]
         L.dense_verify_attn.restype = ctypes.c_int
         L.dense_verify_attn.argtypes = [_vp, _i64, _i64, _i64, _i32, P_KV, P_KV, P_BT,
                                         ctypes.c_float, _vp, _i64, _i64, _i64, _vp, _sz, _vp]
@@ -587,6 +592,36 @@ def plan_sparse_verify_attn(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor,
             _ptr(ws), nbytes, _stream(stream))
     return Call(lib().dustin_sparse_verify_attn, args, "dustin_sparse_verify_attn",
                 (q, k, v, idx, count, kv, vv, bt, ws), out)
+
+
+def plan_sparse_verify_attn_noalloc(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor,
+                                    idx: torch.Tensor, count: torch.Tensor, seq_lens, *, out: torch.Tensor,
+                                    n_query=None, page_table: Optional[torch.Tensor] = None,
+                                    scale: Optional[float] = None, max_len: Optional[int] = None,
+                                    stream=None) -> Call:
+    """Prepared dustin_sparse_verify_attn_noalloc: the same attention with the split scratch
+    taken from the library's fixed per-GPU array (no workspace; the caller passes out, and
+    per-sequence arrays as int32 device tensors, so that calling the plan allocates nothing)."""
+    B, nq_max, Hq, d, dev, kv, vv, max_len, out = _attn_common(q, k, v, seq_lens, n_query,
+                                                                page_table, max_len, out)
+    _on_gpu(idx, count)
+    seq = _i32_dev(seq_lens, dev)
+    nqa = _i32_dev(n_query, dev)
+    G, k_max = idx.shape[1], idx.shape[2]
+    bt = _batch(B, max_len, nq_max, k_max, seq, nqa)
+    scale = 1.0 / math.sqrt(d) if scale is None else scale
+    count = count.contiguous()
+    args = (_ptr(q), q.stride(0), q.stride(1), q.stride(2), Hq, ctypes.byref(kv),
+            ctypes.byref(vv), ctypes.byref(bt), _ptr(idx), idx.stride(0), idx.stride(1),
+            _ptr(count), G, float(scale), _ptr(out), out.stride(0), out.stride(1), out.stride(2),
+            _stream(stream))
+    return Call(lib().dustin_sparse_verify_attn_noalloc, args, "dustin_sparse_verify_attn_noalloc",
+                (q, k, v, idx, count, kv, vv, bt), out)
+
+
+def sparse_verify_attn_noalloc(q, k, v, idx, count, seq_lens, **kw):
+    """dustin_sparse_verify_attn_noalloc; returns out."""
+    return plan_sparse_verify_attn_noalloc(q, k, v, idx, count, seq_lens, **kw)()
 
 
 def sparse_verify_attn(q, k, v, idx, count, seq_lens, **kw):

@@ -6,6 +6,8 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <mutex>
+
 #include "kernels.hpp"
 
 using namespace dustin;
@@ -141,12 +143,22 @@ size_t attn_ws_bytes(int batch, int num_q_heads, int num_kv_heads, int nq_max, i
   return attn_ws_layout(batch, num_kv_heads, rt * 16, splits).total;
 }
 
-dustin_status run_attention(bool sparse, const void* q, int64_t q_sb, int64_t q_st, int64_t q_sh,
-                            int32_t num_q_heads, const dustin_kv* k, const dustin_kv* v,
-                            const dustin_batch* bt, const int32_t* idx, int64_t idx_sb,
-                            int64_t idx_sg, const int32_t* count, int32_t groups, float scale,
-                            void* out, int64_t o_sb, int64_t o_st, int64_t o_sh, void* ws,
-                            size_t ws_bytes, void* stream) {
+// A validated attention call: its kernel arguments (workspace fields still unset), the row
+// tiles and cache kind that pick the kernel, and the workspace it needs.  `empty` marks a
+// valid call with nothing to compute.
+struct AttnCall {
+  AttnArgs a;
+  int rt;
+  bool paged, empty;
+  size_t need_ws;
+};
+
+dustin_status prepare_attention(bool sparse, const void* q, int64_t q_sb, int64_t q_st, int64_t q_sh,
+                                int32_t num_q_heads, const dustin_kv* k, const dustin_kv* v,
+                                const dustin_batch* bt, const int32_t* idx, int64_t idx_sb,
+                                int64_t idx_sg, const int32_t* count, int32_t groups, float scale,
+                                void* out, int64_t o_sb, int64_t o_st, int64_t o_sh, AttnCall* call) {
+  memset(call, 0, sizeof *call);
   if (!batch_ok(bt) || !q || !out || !k || !v) return DUSTIN_ERR_INVALID_ARG;
   if (!isfinite(scale) || !(scale > 0.f)) return DUSTIN_ERR_INVALID_ARG;
   const int Hkv = k->num_kv_heads;
@@ -183,13 +195,14 @@ dustin_status run_attention(bool sparse, const void* q, int64_t q_sb, int64_t q_
     if ((rows - 1) * c->stride_n * 2 + 256 > (int64_t)UINT32_MAX) return DUSTIN_ERR_UNSUPPORTED;
   }
   const int B = bt->batch;
-  if (B == 0 || bt->nq_max == 0) return DUSTIN_OK;
+  if (B == 0 || bt->nq_max == 0) {
+    call->empty = true;
+    return DUSTIN_OK;
+  }
   const int64_t tokens = sparse ? (int64_t)bt->k_max : (int64_t)bt->max_len;
-  const size_t need_ws = attn_ws_bytes(B, num_q_heads, Hkv, bt->nq_max, tokens);
-  if (need_ws && (!ws || ws_bytes < need_ws || !aligned(ws, kAlign))) return DUSTIN_ERR_WORKSPACE;
+  call->need_ws = attn_ws_bytes(B, num_q_heads, Hkv, bt->nq_max, tokens);
 
-  AttnArgs a;
-  memset(&a, 0, sizeof a);
+  AttnArgs& a = call->a;
   a.q = static_cast<const uint16_t*>(q);
   a.q_sb = q_sb;
   a.q_st = q_st;
@@ -217,16 +230,37 @@ dustin_status run_attention(bool sparse, const void* q, int64_t q_sb, int64_t q_
   const int64_t steps_max = (tokens_max + 31) / 32;
   a.split_steps = (int)((steps_max + a.splits - 1) / a.splits);
   a.min_split_steps = env_int("DUSTIN_ATTN_SPLITS", 0) > 0 ? 1 : 8;
+  call->rt = rt;
+  call->paged = kv.page_table != nullptr;
+  return DUSTIN_OK;
+}
+
+// Points the split fields at a workspace of at least call.need_ws bytes and launches.
+dustin_status launch_attention(AttnCall& call, bool sparse, void* ws, void* stream) {
+  AttnArgs& a = call.a;
   if (a.splits > 1) {
-    const AttnWs w = attn_ws_layout(B, Hkv, a.rows_pad, a.splits);
+    const AttnWs w = attn_ws_layout(a.pairs / a.num_kv_heads, a.num_kv_heads, a.rows_pad, a.splits);
     char* base = static_cast<char*>(ws);
     a.counters = reinterpret_cast<int32_t*>(base);
     a.part_acc = reinterpret_cast<float*>(base + w.counters);
     a.part_ml = reinterpret_cast<float*>(base + w.counters + w.acc);
   }
-  const hipError_t e = launch_verify_attn(a, rt, sparse, kv.page_table != nullptr,
-                                          static_cast<hipStream_t>(stream));
+  const hipError_t e = launch_verify_attn(a, call.rt, sparse, call.paged, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? DUSTIN_OK : DUSTIN_ERR_LAUNCH;
+}
+
+dustin_status run_attention(bool sparse, const void* q, int64_t q_sb, int64_t q_st, int64_t q_sh,
+                            int32_t num_q_heads, const dustin_kv* k, const dustin_kv* v,
+                            const dustin_batch* bt, const int32_t* idx, int64_t idx_sb,
+                            int64_t idx_sg, const int32_t* count, int32_t groups, float scale,
+                            void* out, int64_t o_sb, int64_t o_st, int64_t o_sh, void* ws,
+                            size_t ws_bytes, void* stream) {
+  AttnCall call;
+  const dustin_status st = prepare_attention(sparse, q, q_sb, q_st, q_sh, num_q_heads, k, v, bt, idx, idx_sb,
+                                             idx_sg, count, groups, scale, out, o_sb, o_st, o_sh, &call);
+  if (st != DUSTIN_OK || call.empty) return st;
+  if (call.need_ws && (!ws || ws_bytes < call.need_ws || !aligned(ws, kAlign))) return DUSTIN_ERR_WORKSPACE;
+  return launch_attention(call, sparse, ws, stream);
 }
 
 }  // namespace
@@ -240,6 +274,8 @@ const char* dustin_status_string(dustin_status status) {
     case DUSTIN_ERR_UNSUPPORTED: return "unsupported configuration";
     case DUSTIN_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
     case DUSTIN_ERR_LAUNCH: return "kernel launch failed";
+    case DUSTIN_ERR_SCRATCH_LIMIT:
+      return "the call needs more split scratch than the no-allocation entry point's fixed array holds";
   }
   return "unknown status";
 }
@@ -721,3 +757,61 @@ dustin_status dense_verify_attn(const void* q, int64_t q_sb, int64_t q_st, int64
 }
 
 }  // extern "C"
+
+// ------------------------------------------------------------------ attention without allocation
+//
+// The split partials and counters of dustin_sparse_verify_attn_noalloc live in this fixed
+// array, one copy per GPU that the library runs on, held until the process ends.  In host
+// code its name is only a stand-in: its device address comes from hipGetSymbolAddress, once
+// per device, and only that address is handed to kernels.
+
+static __device__ __align__(256) unsigned char scratch[DUSTIN_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[kMaxDevices];  // device address of `scratch` per device, once looked up
+
+__global__ void zero_words_kernel(uint32_t* p, uint32_t n) {
+  for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) p[i] = 0u;
+}
+
+// The current device's scratch address.  At the first call on a device it is looked up and
+// the counter region (which must read zero before the first split call) is cleared by a
+// fill kernel on `stream`, ahead of the call's own launch.
+dustin_status device_scratch(hipStream_t stream, void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return DUSTIN_ERR_LAUNCH;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return DUSTIN_ERR_LAUNCH;
+    const uint32_t words = (uint32_t)(kAttnMaxPairs * sizeof(int32_t) / 4);
+    hipLaunchKernelGGL(zero_words_kernel, dim3(64), dim3(256), 0, stream, static_cast<uint32_t*>(p), words);
+    if (hipGetLastError() != hipSuccess) return DUSTIN_ERR_LAUNCH;
+    g_scratch[dev] = p;
+  }
+  *out = g_scratch[dev];
+  return DUSTIN_OK;
+}
+
+}  // namespace
+
+extern "C" dustin_status dustin_sparse_verify_attn_noalloc(
+    const void* q, int64_t q_sb, int64_t q_st, int64_t q_sh, int32_t num_q_heads, const dustin_kv* k,
+    const dustin_kv* v, const dustin_batch* bt, const int32_t* idx, int64_t idx_sb, int64_t idx_sg,
+    const int32_t* count, int32_t groups, float scale, void* out, int64_t o_sb, int64_t o_st, int64_t o_sh,
+    void* stream) {
+  AttnCall call;
+  dustin_status st = prepare_attention(true, q, q_sb, q_st, q_sh, num_q_heads, k, v, bt, idx, idx_sb, idx_sg,
+                                       count, groups, scale, out, o_sb, o_st, o_sh, &call);
+  if (st != DUSTIN_OK || call.empty) return st;
+  if (call.need_ws > (size_t)DUSTIN_NOALLOC_SCRATCH_BYTES) return DUSTIN_ERR_SCRATCH_LIMIT;
+  void* ws = nullptr;
+  if (call.need_ws) {
+    st = device_scratch(static_cast<hipStream_t>(stream), &ws);
+    if (st != DUSTIN_OK) return st;
+  }
+  return launch_attention(call, true, ws, stream);
+}
