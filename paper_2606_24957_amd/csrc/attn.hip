@@ -140,6 +140,14 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
   // LDS object of their own: the compiler can then see that the direct-to-LDS row loads in
   // flight never write them, and reads them without waiting for those loads.
   __shared__ __attribute__((aligned(16))) uint16_t sm_q[RT * 16 * kQPitch];
+  // The verification window's tokens as a step of their own (when sep_window is set): one
+  // wave of the pair's last split loads them in the prologue, beside its first step, into
+  // this tile (K then V, the same layout as the wave tiles), and computes them while that
+  // step is in flight.  The selected tokens then fill whole 32-token steps, so a pair of
+  // 2048 selected tokens takes 64 steps, 8 per wave over two splits, and no wave spends a
+  // ninth load round trip on a step of a few window tokens.
+  __shared__ __attribute__((aligned(1024))) char sm_win[2 * kTile];
+  __shared__ uint32_t sm_wphys[kStep];  // paged: physical rows of the window's tokens
 
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);  // wave-uniform
@@ -285,11 +293,18 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
   }
   if constexpr (!kPaged) prologue_loads();
 
-  // 32-token steps of a pair: its selected (or all) positions, then its window
+  // 32-token steps of a pair that the splits share: its selected (or all) positions, then
+  // its window -- or, with sep_window, the positions alone (at least one step)
+  // Row tiles up to which the window has a step of its own.  Beyond three the window tile
+  // no longer fits beside four wave accumulators in LDS, and the second copy of the step
+  // code makes the five-tile kernel spill.
+  constexpr int kSepMaxRT = 3;
+  const bool sep = RT <= kSepMaxRT && a.sep_window != 0;  // kernel-uniform
   auto steps_of = [&](int n, int t, int c) {
     const int Nc = clampi(n, 0, a.dims.max_len), Tc = clampi(t, 0, a.dims.nq_max);
-    const int tot = (kSparse ? clampi(c, 0, a.dims.k_max) : Nc) + Tc;
-    return Tc == 0 ? 0 : (tot + kStep - 1) / kStep;
+    const int body = kSparse ? clampi(c, 0, a.dims.k_max) : Nc;
+    if (Tc == 0) return 0;
+    return sep ? max(1, (body + kStep - 1) / kStep) : (body + Tc + kStep - 1) / kStep;
   };
   if (balance) {
     // The smallest split size s (at least min_split_steps) whose splits fit the U slots:
@@ -413,9 +428,15 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
   const int wstart = kSparse ? clampi(c_raw, 0, a.dims.k_max) : N;
   const int total = wstart + T;        // virtual tokens: selected (or all) then window
   const int rows = T * a.group_size;   // <= RT * 16 (checked on the host via nq_max)
-  const int nsteps = (total + kStep - 1) / kStep;
+  const int nsteps = sep ? max(1, (wstart + kStep - 1) / kStep) : (total + kStep - 1) / kStep;
   if (s_begin >= nsteps) return;
   const int s_end = min(nsteps, s_begin + split_steps);
+  // the wave that takes the window step: in the pair's last split, the last wave with the
+  // fewest steps of the split (wave 3, or the last wave with a step when there are fewer
+  // than four)
+  const bool has_window = sep && split == nsplit - 1 && wave == min(kW - 1, s_end - s_begin - 1);
+  // with sep_window, tokens from wstart on are the window step's: body steps mask them
+  const int body_limit = sep ? wstart - 1 : INT32_MAX;
 
   // Rows are addressed as uniform base + 32-bit byte offset phys * stride_n (the host
   // checks that every offset fits): phys is the position (contiguous) or
@@ -485,14 +506,15 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
   // Loads of one step into this wave's tiles: this lane moves chunk lr of tokens 8 lg + i
   // (i = 0..7) of the step, whose physical rows are ph[i]; one instruction per i for K and
   // one for V.
-  auto issue_rows = [&](const uint32_t (&ph)[8]) {
+  auto issue_rows_to = [&](const uint32_t (&ph)[8], char* kt, char* vt) {
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       const int j = 8 * lg + i;
-      load_lds16(kbase + ph[i] * kstride + 16 * k_chunk(j, lr), ktile + i * 1024);
-      load_lds16(vbase + ph[i] * vstride + 16 * v_chunk(j, lr), vtile + i * 1024);
+      load_lds16(kbase + ph[i] * kstride + 16 * k_chunk(j, lr), kt + i * 1024);
+      load_lds16(vbase + ph[i] * vstride + 16 * v_chunk(j, lr), vt + i * 1024);
     }
   };
+  auto issue_rows = [&](const uint32_t (&ph)[8]) { issue_rows_to(ph, ktile, vtile); };
   auto issue = [&](int st) {
     const int v0 = st * kStep + 8 * lg;
     uint32_t ph[8];
@@ -524,29 +546,30 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
   // V^T operand of 16-column tile dt: lane lr of a 16-lane group addresses token
   // 4 lg + lr / 4 (+16 for the second half of k), columns 16 dt + 4 (lr % 4) .. + 3; it
   // receives V[token 4 lg + e (+16)][16 dt + lr]
-  auto read_vt = [&](int dt) -> bf16x8 {
+  auto read_vt = [&](const char* vt, int dt) -> bf16x8 {
     const int j0 = 4 * lg + (lr >> 2), j1 = j0 + 16;
     const int c = 2 * dt + ((lr >> 1) & 1);
-    const v4i16 lo = lds_read_tr16(vtile + tile_row(j0) * 256 + 8 * (lr & 1) + 16 * v_chunk(j0, c));
-    const v4i16 hi = lds_read_tr16(vtile + tile_row(j1) * 256 + 8 * (lr & 1) + 16 * v_chunk(j1, c));
+    const v4i16 lo = lds_read_tr16(vt + tile_row(j0) * 256 + 8 * (lr & 1) + 16 * v_chunk(j0, c));
+    const v4i16 hi = lds_read_tr16(vt + tile_row(j1) * 256 + 8 * (lr & 1) + 16 * v_chunk(j1, c));
     return as_bf16x8(u32x4{__builtin_bit_cast(u32x2, lo)[0], __builtin_bit_cast(u32x2, lo)[1],
                            __builtin_bit_cast(u32x2, hi)[0], __builtin_bit_cast(u32x2, hi)[1]});
   };
 
-  // Reads the step's operands out of this wave's tiles (after its loads completed).
-  auto read_tiles = [&](Operands& op) {
+  // Reads a step's operands out of a K and a V tile (after their loads completed).
+  auto read_tiles_from = [&](const char* kt, const char* vt, Operands& op) {
 #pragma unroll
     for (int t2 = 0; t2 < 2; ++t2) {
       const int j = 16 * t2 + lr;
-      const char* row = ktile + tile_row(j) * 256;
+      const char* row = kt + tile_row(j) * 256;
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks)
         op.k[t2][ks] = as_bf16x8(*reinterpret_cast<const u32x4*>(row + 16 * k_chunk(j, 4 * ks + lg)));
     }
     if constexpr (kOverlap)
 #pragma unroll
-      for (int dt = 0; dt < NDT; ++dt) op.vt[dt] = read_vt(dt);
+      for (int dt = 0; dt < NDT; ++dt) op.vt[dt] = read_vt(vt, dt);
   };
+  auto read_tiles = [&](Operands& op) { read_tiles_from(ktile, vtile, op); };
 
   // One 32-token step on register operands, one 16-row tile at a time (its scores,
   // probabilities and softmax decision live only while the tile is processed, which keeps
@@ -554,9 +577,11 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
   // one wave-uniform decision whether to move the tile's reference maxima; (3) its value
   // product.  Scores stay in raw units until one FMA forms (s * scale * log2 e - m) inside
   // exp2; the reference max m is in scaled units.
-  auto compute = [&](int st, const Operands& op) {
-    const int v0 = st * kStep;
-    const bool edge = v0 + kStep - 1 >= wstart;  // wave-uniform: masking only near the window
+  // v0: the virtual token of the tile's first row; vt: its V tile; win: the window step
+  // (causal mask per query row), else a body step (with sep_window, tokens from wstart on
+  // belong to the window step and are masked here).
+  auto compute = [&](int v0, const Operands& op, const char* vt, bool win) {
+    const bool edge = win || v0 + kStep - 1 >= wstart;  // wave-uniform: masking only near the window
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt) {
       // (1) S^T tile: lane holds tokens v0 + 16 i + 4 lg + e for query row rt*16 + lr
@@ -570,11 +595,12 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
       }
       // (2) masked row maxima, lazy rescale, probabilities
       if (edge) {
+        const int lim = win ? limit[rt] : min(limit[rt], body_limit);
 #pragma unroll
         for (int i = 0; i < 2; ++i)
 #pragma unroll
           for (int e = 0; e < 4; ++e)
-            if (v0 + 16 * i + 4 * lg + e > limit[rt]) sc[i][e] = -INFINITY;
+            if (v0 + 16 * i + 4 * lg + e > lim) sc[i][e] = -INFINITY;
       }
       const float m = fmaxf(fmaxf(fmaxf(sc[0][0], sc[0][1]), fmaxf(sc[0][2], sc[0][3])),
                             fmaxf(fmaxf(sc[1][0], sc[1][1]), fmaxf(sc[1][2], sc[1][3])));
@@ -602,7 +628,7 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
 #pragma unroll
       for (int dt = 0; dt < NDT; ++dt) {
         if constexpr (kOverlap) acc[rt][dt] = mfma16x16x32(op.vt[dt], pT, acc[rt][dt]);
-        else acc[rt][dt] = mfma16x16x32(read_vt(dt), pT, acc[rt][dt]);
+        else acc[rt][dt] = mfma16x16x32(read_vt(vt, dt), pT, acc[rt][dt]);
       }
     }
   };
@@ -628,11 +654,30 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
       if (e < nv) sm_phys[e] = staged[j];
     }
   };
-  // the first chunk's table is written before anything else is issued
+  // the first chunk's table is written before anything else is issued (and, paged, the
+  // window step's rows, by the first 32 threads of the workgroup that takes it)
+  const bool wg_window = sep && split == nsplit - 1;
   if constexpr (kStage) {
     stage_rows(s_begin);
+    if constexpr (kPaged) {
+      if (wg_window && threadIdx.x < kStep) {
+        const int pos = pos_of(wstart + (int)threadIdx.x, 0);
+        sm_wphys[threadIdx.x] = phys_at(pos, page_of(pos));
+      }
+    }
     store_staged(s_begin, min(s_end, s_begin + kStageSteps));
   }
+  // The window step's rows go to its own tile, before the wave's first step, so that a
+  // wait for all but the last 16 loads (the step's) finds them in place.
+  auto issue_window = [&]() {
+    uint32_t ph[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      if constexpr (kPaged) ph[i] = sm_wphys[8 * lg + i];
+      else ph[i] = (uint32_t)pos_of(wstart + 8 * lg + i, 0);
+    }
+    issue_rows_to(ph, sm_win, sm_win + kTile);
+  };
 
   // This wave's first step, if it lies in the first chunk, is issued right away: after
   // every prologue load has been consumed, so that no later wait waits for its rows.
@@ -640,6 +685,8 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
   __builtin_amdgcn_sched_barrier(0);
   bool first_issued = false;
   if constexpr (!kPaged) {
+    if (has_window) issue_window();
+    __builtin_amdgcn_sched_barrier(0);  // the window's loads stay ahead of the step's
     if (s_begin + wave < min(s_end, s_begin + kStageSteps)) {
       uint32_t ph[8];
 #pragma unroll
@@ -674,7 +721,19 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
     // this wave's steps: cs + wave + i kW
     int st = cs + wave;
     if (st >= ce) continue;
+    if constexpr (kPaged) {
+      if (has_window && cs == s_begin) issue_window();
+      __builtin_amdgcn_sched_barrier(0);  // the window's loads stay ahead of the step's
+    }
     if (!(first_issued && cs == s_begin)) issue(st);
+    if (has_window && cs == s_begin) {
+      // the window's 16 loads were issued before the step's 16: wait for them alone and
+      // compute the window while the step is in flight
+      __builtin_amdgcn_s_waitcnt(0x4F70);  // vmcnt(16)
+      Operands opw;
+      read_tiles_from(sm_win, sm_win + kTile, opw);
+      compute(wstart, opw, sm_win + kTile, true);
+    }
     while (true) {
       wait_vmem_all();  // this step's rows are in the tiles
       Operands op;
@@ -685,9 +744,9 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
           wait_lds_all();  // the tiles have been read out before the next loads overwrite them
           issue(next);
         }
-        compute(st, op);
+        compute(st * kStep, op, vtile, false);
       } else {
-        compute(st, op);
+        compute(st * kStep, op, vtile, false);
         if (next < ce) {
           wait_lds_all();
           issue(next);
