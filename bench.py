@@ -45,6 +45,8 @@ def parse():
                    help="index sets per sequence: one (the paper's global set) or one per KV head")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-sample-seqs", type=int, default=16)
+    p.add_argument("--no-secondary", action="store_true",
+                   help="skip the other workloads (ragged, 131k, k = 512) that the headline run also times")
     p.add_argument("--copy-probe", action="store_true",
                    help="also run one plain 1 GiB device copy (counter calibration)")
     p.add_argument("--only", choices=["all", "sparse", "dense", "estimate", "page"], default="all",
@@ -129,6 +131,131 @@ def measured_traffic(workload, k):
     if rec.get("source_sha256") != kernel_sources_sha():
         return None
     return rec.get("bytes_per_launch")
+
+
+# ----------------------------------------------------------------------------- timing
+
+def med(x):
+    x = sorted(x)
+    return x[len(x) // 2] if x else float("nan")
+
+
+def mean(x):
+    return sum(x) / len(x) if x else float("nan")
+
+
+class StepTimer:
+    """The prepared launches of one step of a workload -- target score, draft scores, top-k,
+    then L sparse layers and L dense layers with the one index set -- and their timing with
+    HIP events recorded on the launch stream (around each stage; the L layers of a block run
+    back to back, as in a forward pass, since an event between launches adds an end-of-pipe
+    wait of its own)."""
+
+    def __init__(self, s, layers, est, dev):
+        import torch
+        import paper_2606_24957_amd as D
+        self.s, self.L = s, len(layers)
+        B, N, G = s.B, s.n_max, s.groups
+        i32 = lambda x: torch.tensor(list(x), dtype=torch.int32, device=dev)
+        self.seq, self.nq, self.gam = i32(s.seq_lens), i32(s.n_query), i32(s.draft_gamma)
+        self.bud, self.mm = i32(s.budget), i32(s.m)
+        self.s_t = torch.zeros((B, G, N), dtype=torch.float32, device=dev)
+        self.s_d = torch.zeros((B, 1, N), dtype=torch.float32, device=dev)
+        self.idx = torch.zeros((B, G, s.k_max), dtype=torch.int32, device=dev)
+        self.cnt = torch.zeros((B, G), dtype=torch.int32, device=dev)
+        self.outs = [torch.empty_like(l.q) for l in layers]
+        self.outs_d = [torch.empty_like(l.q) for l in layers]
+        init_t = est.init_target
+        if init_t is not None and G > 1:  # one historical row, the same for every group
+            init_t = init_t.expand(B, G, N)
+        self.score_t = D.plan_score(est.q_target, layers[0].k, self.seq, s.target_heads, groups=G, init=init_t,
+                                    out=self.s_t, max_len=N, page_table=layers[0].page_table)
+        self.score_d = []
+        if est.s_draft_given is not None:
+            self.s_d.copy_(est.s_draft_given)
+        else:
+            self.score_d.append(D.plan_score_layers(est.draft_q, est.draft_k, self.seq, s.draft.heads,
+                                                    n_query=self.gam, out=self.s_d, max_len=N))
+        self.sel = D.plan_topk(self.s_d, self.s_t, self.seq, s.k_max, budget=self.bud, m=self.mm, n_sink=s.n_sink,
+                               n_window=s.n_window, groups=G, idx=self.idx, count=self.cnt)
+        self.sparse = [D.plan_sparse_verify_attn(l.q, l.k, l.v, self.idx, self.cnt, self.seq, n_query=self.nq,
+                                                 page_table=l.page_table, out=o)
+                       for l, o in zip(layers, self.outs)]
+        self.dense = [D.plan_dense_verify_attn(l.q, l.k, l.v, self.seq, n_query=self.nq, page_table=l.page_table,
+                                               out=o) for l, o in zip(layers, self.outs_d)]
+
+    @staticmethod
+    def _ev():
+        import torch
+        e = torch.cuda.Event(enable_timing=True)
+        e.record()
+        return e
+
+    def step(self, rec, only="all"):
+        marks = [self._ev()] if rec else None
+        if only in ("all", "estimate", "sparse"):
+            self.score_t()
+            if rec: marks.append(self._ev())
+            for c in self.score_d:
+                c()
+            if rec: marks.append(self._ev())
+            self.sel()
+            if rec: marks.append(self._ev())
+        if only in ("all", "sparse"):
+            for c in self.sparse:
+                c()
+            if rec: marks.append(self._ev())
+        if only in ("all", "dense"):
+            for c in self.dense:
+                c()
+            if rec: marks.append(self._ev())
+        return marks
+
+    def run(self, steps, warmup, only="all", copy_probe=False):
+        """Stage durations (ms) of `steps` timed steps after `warmup` untimed ones."""
+        import torch
+        for _ in range(warmup):
+            self.step(False, only)
+        torch.cuda.synchronize()
+        if copy_probe:
+            a = torch.empty(1 << 30, dtype=torch.uint8, device=self.seq.device)
+            b_ = torch.empty_like(a)
+            b_.copy_(a)
+            torch.cuda.synchronize()
+            del a, b_
+        all_marks = []
+        t_start = time.perf_counter()
+        for _ in range(steps):
+            all_marks.append(self.step(True, only))
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t_start
+        out = {"est_t": [], "est_d": [], "est_k": [], "sp": [], "dn": [], "ms_per_step": wall * 1e3 / steps}
+        for m in all_marks:
+            i = 0
+            if only in ("all", "estimate", "sparse"):
+                out["est_t"].append(m[0].elapsed_time(m[1]))
+                out["est_d"].append(m[1].elapsed_time(m[2]))
+                out["est_k"].append(m[2].elapsed_time(m[3]))
+                i = 3
+            if only in ("all", "sparse"):
+                out["sp"].append(m[i].elapsed_time(m[i + 1]) / self.L)
+                i += 1
+            if only in ("all", "dense"):
+                out["dn"].append(m[i].elapsed_time(m[i + 1]) / self.L)
+        return out
+
+    def sparse_with_events(self, reps):
+        """Per-launch event times (ms) of the sparse layers with an event between launches."""
+        import torch
+        sp_ev = []
+        for _ in range(reps):
+            es = [self._ev()]
+            for c in self.sparse:
+                c()
+                es.append(self._ev())
+            torch.cuda.synchronize()
+            sp_ev += [es[j].elapsed_time(es[j + 1]) for j in range(self.L)]
+        return sp_ev
 
 
 # ----------------------------------------------------------------------------- page estimator
@@ -366,6 +493,60 @@ def cpu_baseline(s, layer0, est, n_seq):
     }
 
 
+# ----------------------------------------------------------------------------- other workloads
+
+SECONDARY = (("qwen72b", 512), ("ragged", None), ("long131k", None))
+
+
+def secondary(name, k, steps, warmup, dev):
+    """One more workload through the same timed step as the headline (estimation, then its L
+    sparse and L dense layers back to back): per-layer and per-step figures."""
+    import torch
+    from paper_2606_24957_amd import workloads as W
+    s = W.config(name)
+    if k is not None:
+        s = s.replace(budget=(k,) * s.B, m=((k - s.n_sink - s.n_window) // 2,) * s.B)
+    t0 = time.perf_counter()
+    layers = [W.make_layer(s, l, dev) for l in range(s.layers)]
+    est = W.make_estimation(s, layers[0], dev)
+    torch.cuda.synchronize()
+    gen_s = time.perf_counter() - t0
+    T = StepTimer(s, layers, est, dev)
+    r = T.run(steps, warmup)
+    L = s.layers
+    sp_us, dn_us = mean(r["sp"]) * 1e3, mean(r["dn"]) * 1e3
+    est_t, est_d, est_k = (mean(r[x]) * 1e3 for x in ("est_t", "est_d", "est_k"))
+    est_us = est_t + est_d + est_k
+    sb, db = sparse_bytes(s), dense_bytes(s)
+    eb = score_bytes(s, True) + score_bytes(s, False) + topk_bytes(s)
+    rec = {
+        "config": {"batch": s.B, "context": list(s.seq_lens) if len(set(s.seq_lens)) > 1 else s.n_max,
+                   "verify_queries": list(s.n_query) if len(set(s.n_query)) > 1 else s.t_max,
+                   "budget_k": list(s.budget) if len(set(s.budget)) > 1 else s.k_max,
+                   "stacked_layers": L, "paged": bool(s.page_size)},
+        "sparse_us_per_layer": round(sp_us, 3), "sparse_GBps": round(sb / (sp_us * 1e-6) / 1e9, 1),
+        "sparse_frac": round(sb / (sp_us * 1e-6) / 1e9 / PEAK_HBM_GBPS, 4), "sparse_bytes": sb,
+        "dense_us_per_layer": round(dn_us, 3), "dense_GBps": round(db / (dn_us * 1e-6) / 1e9, 1),
+        "dense_bytes": db,
+        "estimation_us_per_step": round(est_us, 3), "target_score_us": round(est_t, 3),
+        "draft_score_us": round(est_d, 3), "topk_us": round(est_k, 3),
+        "estimation_GBps": round(eb / (est_us * 1e-6) / 1e9, 1),
+        "speedup": {"per_layer": round(dn_us / sp_us, 3),
+                    f"per_step_L{L}": round(L * dn_us / (est_us + L * sp_us), 3),
+                    "per_step_L80": round(80 * dn_us / (est_us + 80 * sp_us), 3)},
+        "steps": steps, "warmup": warmup,
+    }
+    tag = name + ("" if k is None else f"_k{k}")
+    log(f"[bench] {tag}: sparse {sp_us:.2f} us/layer ({rec['sparse_GBps']} GB/s), dense {dn_us:.1f} us/layer, "
+        f"estimation {est_us:.1f} us/step (target {est_t:.1f}, draft {est_d:.1f}, topk {est_k:.1f}); "
+        f"speedup per layer {rec['speedup']['per_layer']}x, per step L={L} {rec['speedup'][f'per_step_L{L}']}x, "
+        f"L=80 {rec['speedup']['per_step_L80']}x (inputs {gen_s:.1f}s)")
+    del T, layers, est
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return tag, rec
+
+
 # ----------------------------------------------------------------------------- main
 
 def main():
@@ -399,117 +580,14 @@ def main():
     torch.cuda.synchronize()
     log(f"[bench] inputs generated in {time.perf_counter() - t0:.1f}s")
 
-    B, N = s.B, s.n_max
-    seq = torch.tensor(s.seq_lens, dtype=torch.int32, device=dev)
-    nq = torch.tensor(s.n_query, dtype=torch.int32, device=dev)
-    gam = torch.tensor(s.draft_gamma, dtype=torch.int32, device=dev)
-    bud = torch.tensor(s.budget, dtype=torch.int32, device=dev)
-    mm = torch.tensor(s.m, dtype=torch.int32, device=dev)
-    G = s.groups
-    s_t = torch.zeros((B, G, N), dtype=torch.float32, device=dev)
-    s_d = torch.zeros((B, 1, N), dtype=torch.float32, device=dev)
-    idx = torch.zeros((B, s.groups, s.k_max), dtype=torch.int32, device=dev)
-    cnt = torch.zeros((B, s.groups), dtype=torch.int32, device=dev)
-    outs = [torch.empty_like(l.q) for l in layers]
-    outs_d = [torch.empty_like(l.q) for l in layers]
-
-    # prepared launches (arguments marshalled once)
-    init_t = est.init_target
-    if init_t is not None and G > 1:  # one historical row, the same for every group
-        init_t = init_t.expand(B, G, N)
-    score_t = D.plan_score(est.q_target, layers[0].k, seq, s.target_heads, groups=G, init=init_t,
-                           out=s_t, max_len=N, page_table=layers[0].page_table)
-    score_d = []
-    if est.s_draft_given is not None:
-        s_d.copy_(est.s_draft_given)
-    else:
-        score_d.append(D.plan_score_layers(est.draft_q, est.draft_k, seq, s.draft.heads,
-                                           n_query=gam, out=s_d, max_len=N))
-    sel = D.plan_topk(s_d, s_t, seq, s.k_max, budget=bud, m=mm, n_sink=s.n_sink,
-                      n_window=s.n_window, groups=s.groups, idx=idx, count=cnt)
-    sparse = [D.plan_sparse_verify_attn(l.q, l.k, l.v, idx, cnt, seq, n_query=nq,
-                                        page_table=l.page_table, out=o)
-              for l, o in zip(layers, outs)]
-    dense = [D.plan_dense_verify_attn(l.q, l.k, l.v, seq, n_query=nq, page_table=l.page_table,
-                                      out=o) for l, o in zip(layers, outs_d)]
-
-    def ev():
-        e = torch.cuda.Event(enable_timing=True)
-        e.record()
-        return e
-
-    def step(rec):
-        marks = [ev()] if rec else None
-        if args.only in ("all", "estimate", "sparse"):
-            score_t()
-            if rec: marks.append(ev())
-            for c in score_d:
-                c()
-            if rec: marks.append(ev())
-            sel()
-            if rec: marks.append(ev())
-        # the layers run back to back, events only around each block of L layers (an event
-        # between launches adds its own end-of-pipe wait, which a forward pass does not have)
-        if args.only in ("all", "sparse"):
-            for c in sparse:
-                c()
-            if rec: marks.append(ev())
-        if args.only in ("all", "dense"):
-            for c in dense:
-                c()
-            if rec: marks.append(ev())
-        return marks
-
-    for _ in range(args.warmup):
-        step(False)
-    torch.cuda.synchronize()
-    if args.copy_probe:
-        a = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
-        b_ = torch.empty_like(a)
-        b_.copy_(a)
-        torch.cuda.synchronize()
-        del a, b_
-    all_marks = []
-    torch.cuda.synchronize()
-    t_start = time.perf_counter()
-    for _ in range(args.steps):
-        all_marks.append(step(True))
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t_start
-    ms_per_step = wall * 1e3 / args.steps
-
-    # per-stage durations from the events (ms)
-    est_t, est_d, est_k, sp, dn = [], [], [], [], []
-    for m in all_marks:
-        i = 0
-        if args.only in ("all", "estimate", "sparse"):
-            est_t.append(m[0].elapsed_time(m[1]))
-            est_d.append(m[1].elapsed_time(m[2]))
-            est_k.append(m[2].elapsed_time(m[3]))
-            i = 3
-        if args.only in ("all", "sparse"):
-            sp.append(m[i].elapsed_time(m[i + 1]) / L)
-            i += 1
-        if args.only in ("all", "dense"):
-            dn.append(m[i].elapsed_time(m[i + 1]) / L)
-
-    def med(x):
-        x = sorted(x)
-        return x[len(x) // 2] if x else float("nan")
-
-    def mean(x):
-        return sum(x) / len(x) if x else float("nan")
-
+    T = StepTimer(s, layers, est, dev)
+    seq, nq, bud, mm = T.seq, T.nq, T.bud, T.mm
+    s_t, s_d, idx, cnt = T.s_t, T.s_d, T.idx, T.cnt
+    r = T.run(args.steps, args.warmup, args.only, copy_probe=args.copy_probe)
+    est_t, est_d, est_k, sp, dn = r["est_t"], r["est_d"], r["est_k"], r["sp"], r["dn"]
+    ms_per_step = r["ms_per_step"]
     # the same sparse launches with an event between each (for comparison only)
-    sp_ev = []
-    if args.only in ("all", "sparse"):
-        for _ in range(max(1, args.steps // 3)):
-            es = [ev()]
-            for c in sparse:
-                c()
-                es.append(ev())
-            torch.cuda.synchronize()
-            sp_ev += [es[j].elapsed_time(es[j + 1]) for j in range(L)]
+    sp_ev = T.sparse_with_events(max(1, args.steps // 3)) if args.only in ("all", "sparse") else []
     sp_us, dn_us = mean(sp) * 1e3, mean(dn) * 1e3
     est_us = (mean(est_t) + mean(est_d) + mean(est_k)) * 1e3
     sb, db = sparse_bytes(s), dense_bytes(s)
@@ -599,6 +677,18 @@ def main():
         del src, dst
         log(f"[bench] 1 GiB device copy: {copy_gbps} GB/s (read + write)")
 
+    # the other workloads through the same timed step, after the headline's buffers are gone
+    others = None
+    if args.only == "all" and not args.no_secondary and args.workload == "qwen72b" and args.k is None \
+            and args.layers is None and args.groups == "1":
+        del T, layers, est, s_t, s_d, idx, cnt
+        D.release_workspaces()
+        torch.cuda.empty_cache()
+        others = {}
+        for name, k in SECONDARY:
+            tag, r2 = secondary(name, k, min(args.steps, 10), min(args.warmup, 2), dev)
+            others[tag] = r2
+
     traffic = measured_traffic(s.name, s.k_max)
     rec = {
         "metric": "sparse verify-attention us/layer + achieved HBM GB/s, B=16 ctx=32k 72B-shape",
@@ -614,7 +704,7 @@ def main():
         "dtype": "bf16",
         "data": "synthetic (seeded; Qwen2.5-72B/0.5B-shaped attention, planted salient keys)",
         "config": {
-            "workload": s.name, "batch": B, "context": N, "num_q_heads": s.num_q_heads,
+            "workload": s.name, "batch": s.B, "context": s.n_max, "num_q_heads": s.num_q_heads,
             "num_kv_heads": s.num_kv_heads, "head_dim": s.head_dim, "verify_queries": s.t_max,
             "budget_k": s.k_max, "draft_share_m": s.m[0], "sinks": s.n_sink, "window": s.n_window,
             "scoring_heads": list(s.target_heads),
@@ -650,13 +740,15 @@ def main():
         "selection_arr": fidelity,
         "per_layer_selection": per_layer,
         "cpu_baseline": cpu,
+        "other_workloads": others,
     }
     print(json.dumps(_finite(rec)), flush=True)
     # Release every device buffer while the HIP runtime is whole: the prepared calls, the
     # stacked layers, the cached workspaces, then torch's cached blocks.  (A run under
     # rocprofv3 once died in exit() inside the runtime's teardown, after the profiler had
     # finalised, with all of these still held.)
-    del score_t, score_d, sel, sparse, dense, layers, est, outs, outs_d, s_t, s_d, idx, cnt
+    if others is None:
+        del T, layers, est, s_t, s_d, idx, cnt
     D.release_workspaces()
     import gc
     gc.collect()

@@ -105,8 +105,10 @@ typedef struct {
   int32_t m_scalar;
 } dustin_batch;
 
-/* Human-readable name of a status code (static storage). */
-const char* dustin_status_string(dustin_status status);
+/* Human-readable name of a status code (static storage); any other value gives
+ * "unknown status".  The code is taken as a plain integer, so that a caller may pass any
+ * value it holds. */
+const char* dustin_status_string(int32_t status);
 
 /* Library version, (major << 16) | minor. */
 int32_t dustin_version(void);

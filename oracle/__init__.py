@@ -14,7 +14,8 @@ import os
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+# DUSTIN_ORACLE_LIB selects another build of oracle.c (the sanitizer build of the CPU suite)
+_LIB_PATH = os.environ.get("DUSTIN_ORACLE_LIB") or os.path.join(_HERE, "liboracle.so")
 _lib = None
 
 _i64 = ctypes.c_int64

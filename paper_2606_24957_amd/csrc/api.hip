@@ -270,7 +270,7 @@ dustin_status run_attention(bool sparse, const void* q, int64_t q_sb, int64_t q_
 
 extern "C" {
 
-const char* dustin_status_string(dustin_status status) {
+const char* dustin_status_string(int32_t status) {
   switch (status) {
     case DUSTIN_OK: return "ok";
     case DUSTIN_ERR_INVALID_ARG: return "invalid argument";
