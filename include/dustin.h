@@ -281,7 +281,13 @@ dustin_status dustin_arr(const float* s, int64_t s_sb, int64_t s_sg, const int32
  *   bt       seq_lens, budget/k_max, m/m_scalar; 1 <= max_len <= 1 << 19
  *   groups   1 or the KV head count
  *   idx      int32 [B, groups, >= k_max] (strides idx_sb, idx_sg), count int32 [B*groups]
- *   workspace  dustin_topk_workspace() bytes (may be 0 bytes: pass NULL, 0)
+ *   workspace  dustin_topk_workspace(batch, groups, max_len) bytes, 256-byte aligned,
+ *       required when both s_draft and s_target are given (else NULL, 0 will do): the two
+ *       tiers of a row are selected side by side (I_D, and C_T = the k - |P| best free
+ *       positions by S_T, of which I_T is the k - m - |P| best outside I_D) and hand off
+ *       through it.  It holds an arrival counter per (b, go), then two bitmaps of max_len
+ *       bits per (b, go).  Zero-fill it once before its first use: every call leaves the
+ *       counters at zero again.  Calls sharing a workspace must not overlap.
  * The result is a pure function of the fp32 inputs: bit-exact and deterministic.
  * --------------------------------------------------------------------------------- */
 size_t dustin_topk_workspace(int32_t batch, int32_t groups, int32_t max_len);

@@ -541,10 +541,12 @@ def plan_topk(s_draft: Optional[torch.Tensor], s_target: Optional[torch.Tensor],
     dsb, dsg = st(s_draft)
     tsb, tsg = st(s_target)
     bt = _batch(B, max_len, 0, k_max, seq, None, bud, ma, m_scalar)
+    nbytes = lib().dustin_topk_workspace(B, int(groups), max_len) if s_draft is not None and s_target is not None else 0
+    ws = workspace(nbytes, dev, "topk", stream)
     args = (_ptr(s_draft), dsb, dsg, _ptr(s_target), tsb, tsg, ctypes.byref(bt), int(groups),
             int(n_sink), int(n_window), _ptr(idx), idx.stride(0), idx.stride(1), _ptr(count),
-            None, 0, _stream(stream))
-    return Call(lib().dustin_topk, args, "dustin_topk", (s_draft, s_target, bt), (idx, count))
+            _ptr(ws), nbytes, _stream(stream))
+    return Call(lib().dustin_topk, args, "dustin_topk", (s_draft, s_target, bt, ws), (idx, count))
 
 
 def topk(s_draft, s_target, seq_lens, k_max, **kw):

@@ -630,11 +630,30 @@ dustin_status dustin_arr(const float* s, int64_t s_sb, int64_t s_sg, const int32
 
 // ------------------------------------------------------------------ top-k
 
+namespace {
+
+// Top-k workspace: an arrival counter per (b, go), then two bitmaps of the row's positions
+// per (b, go) for the hand-off between its two tiers.
+struct TopkWs {
+  size_t counters, bitmaps, total;
+  int32_t words;
+};
+
+TopkWs topk_ws_layout(int32_t batch, int32_t groups, int32_t max_len) {
+  TopkWs w{0, 0, 0, 0};
+  if (batch <= 0 || groups <= 0 || max_len <= 0) return w;
+  const size_t rows = (size_t)batch * groups;
+  w.words = (max_len + 31) / 32;
+  w.counters = round_up(rows * sizeof(uint32_t), kAlign);
+  w.bitmaps = round_up(rows * 2 * (size_t)w.words * sizeof(uint32_t), kAlign);
+  w.total = w.counters + w.bitmaps;
+  return w;
+}
+
+}  // namespace
+
 size_t dustin_topk_workspace(int32_t batch, int32_t groups, int32_t max_len) {
-  (void)batch;
-  (void)groups;
-  (void)max_len;
-  return 0;
+  return topk_ws_layout(batch, groups, max_len).total;
 }
 
 dustin_status dustin_topk(const float* s_draft, int64_t d_sb, int64_t d_sg,
@@ -643,8 +662,6 @@ dustin_status dustin_topk(const float* s_draft, int64_t d_sb, int64_t d_sg,
                           int32_t n_window, int32_t* idx, int64_t idx_sb, int64_t idx_sg,
                           int32_t* count, void* workspace, size_t workspace_bytes,
                           void* stream) {
-  (void)workspace;
-  (void)workspace_bytes;
   if (!batch_ok(bt) || !idx || !count) return DUSTIN_ERR_INVALID_ARG;
   if (!s_draft && !s_target) return DUSTIN_ERR_INVALID_ARG;
   if (groups < 1 || groups > 65535 || n_sink < 0 || n_window < 0) return DUSTIN_ERR_INVALID_ARG;
@@ -660,8 +677,19 @@ dustin_status dustin_topk(const float* s_draft, int64_t d_sb, int64_t d_sg,
     return DUSTIN_ERR_INVALID_ARG;
   const int B = bt->batch;
   if (B == 0) return DUSTIN_OK;
+  // with both score arrays the two tiers of a row run side by side and hand off through
+  // the workspace
+  const TopkWs w = topk_ws_layout(B, groups, bt->max_len);
+  const bool hand_off = s_draft && s_target && w.total > 0;
+  if (hand_off && (!workspace || workspace_bytes < w.total || !aligned(workspace, kAlign)))
+    return DUSTIN_ERR_WORKSPACE;
   TopkArgs a;
   memset(&a, 0, sizeof a);
+  if (hand_off) {
+    a.counters = static_cast<uint32_t*>(workspace);
+    a.bitmaps = reinterpret_cast<uint32_t*>(static_cast<char*>(workspace) + w.counters);
+    a.words = w.words;
+  }
   a.s_draft = s_draft;
   a.d_sb = d_sb;
   a.d_sg = d_sg;

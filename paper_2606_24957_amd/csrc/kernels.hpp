@@ -127,6 +127,11 @@ struct TopkArgs {
   int32_t* idx;
   int64_t idx_sb, idx_sg;
   int32_t* count;
+  // hand-off between the two tiers of a row (both score arrays given): per (b, go) an
+  // arrival counter (zero between calls) and two chosen-set bitmaps of `words` words
+  uint32_t* counters;  // [B * groups]
+  uint32_t* bitmaps;   // [B * groups][2][words]
+  int32_t words;
 };
 
 hipError_t launch_topk(const TopkArgs& a, int B, hipStream_t stream);

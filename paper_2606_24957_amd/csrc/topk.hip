@@ -286,7 +286,7 @@ __device__ void select_tier(TopkSmem& s, KeyStage& ks, uint32_t need, uint32_t* 
 constexpr int kMaxRankedTies = 1024;
 constexpr int kFastBatch = 8;  // 64-position groups of a wave loaded together
 
-__device__ void select_tier_fast(TopkSmem& s, KeyStage& ks, uint32_t need, uint32_t* bm, uint32_t* cand,
+__device__ __forceinline__ void select_tier_fast(TopkSmem& s, KeyStage& ks, uint32_t need, uint32_t* bm, uint32_t* cand,
                                  int cap) {
   if (need == 0) return;
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
@@ -432,6 +432,12 @@ __device__ void select_tier_fast(TopkSmem& s, KeyStage& ks, uint32_t need, uint3
   __syncthreads();
 }
 
+// The same, as a call of its own (the rare fallback of the tier hand-off below).
+__device__ __noinline__ void select_tier_fast_outlined(TopkSmem& s, KeyStage& ks, uint32_t need, uint32_t* bm,
+                                                       uint32_t* cand, int cap) {
+  select_tier_fast(s, ks, need, bm, cand, cap);
+}
+
 // Key-segment length for rows of up to max_len positions: the LDS left beside the
 // static state and the bitmap, a multiple of kSegQuantum, at most the row rounded up.
 static int topk_segment(int max_len) {
@@ -442,56 +448,17 @@ static int topk_segment(int max_len) {
   return row < cap ? row : cap;
 }
 
-__global__ __launch_bounds__(kTopkThreads) void topk_kernel(TopkArgs a, int seg) {
-  extern __shared__ __align__(16) uint32_t dyn[];  // [seg] staged keys | [nwords] chosen bitmap
-  __shared__ TopkSmem s;
-  const int go = blockIdx.x, b = blockIdx.y;
-  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
-  const int N = a.dims.len(b);
-  const int P = a.n_sink + a.n_window;
-  const int k = clampi(a.dims.budget ? a.dims.budget[b] : a.dims.k_max, P, a.dims.k_max);
-  int m = clampi(a.dims.m ? a.dims.m[b] : a.dims.m_scalar, 0, k - P);
-  if (!a.s_draft) m = 0;
-  if (!a.s_target) m = k - P;
-  int32_t* out = a.idx + (int64_t)b * a.idx_sb + (int64_t)go * a.idx_sg;
-  if (N <= k) {
-    for (int n = tid; n < N; n += kTopkThreads) out[n] = n;
-    if (tid == 0) a.count[b * a.groups + go] = N;
-    return;
-  }
-  uint32_t* bm = dyn + seg;
-  // protected positions (and the padding past N) start out taken
-  const int nwords = (N + 31) / 32;
-  // (bit i of word w is position 32 w + i; taken: below n_sink, or at or above N - n_window,
-  // which includes every position at or above N)
-  auto below = [](int x, int n0) -> uint32_t {  // bits i with n0 + i < x
-    const int c = x - n0;
-    return c <= 0 ? 0u : (c >= 32 ? ~0u : (1u << c) - 1u);
-  };
-  for (int w = tid; w < nwords; w += kTopkThreads)
-    bm[w] = below(a.n_sink, w * 32) | ~below(N - a.n_window, w * 32);
-  // a row shorter than the segment uses a shorter one (still a multiple of kSegQuantum)
-  const int rseg = min(seg, (N + kSegQuantum - 1) / kSegQuantum * kSegQuantum);
-  KeyStage ks{nullptr, dyn, bm, N, rseg, (N + rseg - 1) / rseg, -1};
-  __syncthreads();
-  // the candidate list of the fast tier uses the key-staging area: (key, position) pairs
-  const int cap = rseg / 2;
-  if (a.s_draft) {
-    ks.row = a.s_draft + (int64_t)b * a.d_sb + (int64_t)go * a.d_sg;
-    ks.loaded = -1;
-    select_tier_fast(s, ks, (uint32_t)m, bm, dyn, cap);
-  }
-  if (a.s_target) {
-    ks.row = a.s_target + (int64_t)b * a.t_sb + (int64_t)go * a.t_sg;
-    ks.loaded = -1;
-    select_tier_fast(s, ks, (uint32_t)(k - m - P), bm, dyn, cap);
-  }
-
-  // ascending write-out: wave w owns bitmap words [w W, (w + 1) W), one word per lane
+// Calls emit(i, n) for the set bits n of words(w), w < nwords, positions below N, in
+// ascending order of n, i = 0, 1, ...; returns how many there were.  Wave w owns the
+// words [w W, (w + 1) W), one word per lane per iteration (two passes: counts, then
+// positions).
+template <class Words, class Emit>
+__device__ uint32_t ordered_bits(TopkSmem& s, int nwords, int N, Words words, Emit emit) {
+  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
   const int wper = (nwords + kTopkWaves - 1) / kTopkWaves;
   const int w0 = min(nwords, wave * wper), w1 = min(nwords, w0 + wper);
   auto word_bits = [&](int w) -> uint32_t {
-    uint32_t bits = w < w1 ? bm[w] : 0u;
+    uint32_t bits = w < w1 ? words(w) : 0u;
     if (w == nwords - 1 && (N & 31)) bits &= (1u << (N & 31)) - 1u;
     return bits;
   };
@@ -519,10 +486,180 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(TopkArgs a, int seg)
     while (bits) {
       const int i = __ffs(bits) - 1;
       bits &= bits - 1u;
-      if (pos < (uint32_t)k) out[pos] = w * 32 + i;  // never past the budget
+      emit(pos, w * 32 + i);
       ++pos;
     }
   }
+  return total;
+}
+
+// The `need` best of a list of c (key, position) pairs in LDS, the positions ascending
+// (key[i] = list[2 i], position = list[2 i + 1]), by (key desc, position asc): the three
+// digits of the threshold key tau as in select_tier, over the listed keys, then every key
+// above tau and the first `remaining` keys equal to it in list order are marked in bm.
+__device__ void select_list(TopkSmem& s, const uint32_t* list, int c, uint32_t need, uint32_t* bm) {
+  if (need == 0) return;
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+  for (int i = tid; i < kBins1; i += kTopkThreads) s.hist[i] = 0u;
+  __syncthreads();
+  uint32_t prefix = 0, pmask = 0, remaining = need;
+  for (int pass = 0; pass < 3; ++pass) {
+    const int sh = pass == 0 ? 20 : (pass == 1 ? 10 : 0);
+    const uint32_t dmask = pass == 0 ? 4095u : 1023u;
+    for (int i = tid; i < c; i += kTopkThreads) {
+      const uint32_t key = list[2 * i];
+      if ((key & pmask) == prefix) atomicAdd(&s.hist[(key >> sh) & dmask], 1u);
+    }
+    __syncthreads();
+    if (pass == 0)
+      find_digit<kBins1>(s, remaining);
+    else
+      find_digit<kBins>(s, remaining);
+    prefix |= s.misc[0] << sh;
+    pmask |= dmask << sh;
+    remaining = s.misc[1];
+  }
+  const uint32_t tau = prefix;
+  // the list in chunks of the block, in order: ties at tau ranked by list position
+  uint32_t rank = 0;
+  for (int i0 = 0; i0 < c; i0 += kTopkThreads) {
+    const int i = i0 + tid;
+    const uint32_t key = i < c ? list[2 * i] : 0u, n = i < c ? list[2 * i + 1] : 0u;
+    const bool eq = i < c && key == tau;
+    const uint64_t em = __ballot(eq);
+    uint32_t chunk_total;
+    const uint32_t before = rank + block_offsets(s, __popcll(em), &chunk_total) + __popcll(em & lanemask_lt(lane));
+    if (i < c && (key > tau || (eq && before < remaining))) atomicOr(&bm[n >> 5], 1u << (n & 31));
+    rank += chunk_total;
+  }
+  __syncthreads();
+}
+
+// Agent-scope (cross-XCD) write-through stores and loads of the tier hand-off, through a
+// buffer resource over the row's two bitmaps.
+constexpr int kSC1 = 16;
+
+// One workgroup per (selection group, tier, sequence).  The two tiers of Eq. 6 are
+// independent up to a final filter: with C_T the k - |P| best free positions by S_T,
+// I_T is the k - m - |P| best of C_T \ I_D (|I_D| = m, so C_T holds at least k - m - |P|
+// positions outside I_D, and every position that beats one of those in S_T order is in
+// C_T).  So, when both tiers are present, workgroup 0 of the row selects I_D and
+// workgroup 1 selects C_T at the same time; each publishes its chosen set as a bitmap and
+// counts itself in, and the one that arrives second lists C_T \ I_D in position order,
+// selects its k - m - |P| best by S_T among the list alone, and writes I.  A row with one
+// tier (m = 0, or m = k - |P|, or one score array absent) is selected by workgroup 0 alone.
+__global__ __launch_bounds__(kTopkThreads) void topk_kernel(TopkArgs a, int seg) {
+  extern __shared__ __align__(16) uint32_t dyn[];  // [seg] staged keys | [nwords] chosen bitmap
+  __shared__ TopkSmem s;
+  const int go = blockIdx.x % a.groups, tier = blockIdx.x / a.groups, b = blockIdx.y;
+  const int tid = threadIdx.x;
+  const int N = a.dims.len(b);
+  const int P = a.n_sink + a.n_window;
+  const int k = clampi(a.dims.budget ? a.dims.budget[b] : a.dims.k_max, P, a.dims.k_max);
+  int m = clampi(a.dims.m ? a.dims.m[b] : a.dims.m_scalar, 0, k - P);
+  if (!a.s_draft) m = 0;
+  if (!a.s_target) m = k - P;
+  int32_t* out = a.idx + (int64_t)b * a.idx_sb + (int64_t)go * a.idx_sg;
+  if (N <= k) {
+    if (tier == 0) {
+      for (int n = tid; n < N; n += kTopkThreads) out[n] = n;
+      if (tid == 0) a.count[b * a.groups + go] = N;
+    }
+    return;
+  }
+  const bool has_d = a.s_draft && m > 0;
+  const bool has_t = a.s_target && k - m - P > 0;
+  const bool both = has_d && has_t && a.counters;  // kernel-uniform but for m
+  if (tier == 1 && !both) return;
+  const bool run_d = both ? tier == 0 : has_d;
+  const bool run_t = both ? tier == 1 : has_t;
+
+  uint32_t* bm = dyn + seg;
+  // protected positions (and the padding past N) start out taken
+  const int nwords = (N + 31) / 32;
+  // (bit i of word w is position 32 w + i; taken: below n_sink, or at or above N - n_window,
+  // which includes every position at or above N)
+  auto below = [](int x, int n0) -> uint32_t {  // bits i with n0 + i < x
+    const int c = x - n0;
+    return c <= 0 ? 0u : (c >= 32 ? ~0u : (1u << c) - 1u);
+  };
+  for (int w = tid; w < nwords; w += kTopkThreads)
+    bm[w] = below(a.n_sink, w * 32) | ~below(N - a.n_window, w * 32);
+  // a row shorter than the segment uses a shorter one (still a multiple of kSegQuantum)
+  const int rseg = min(seg, (N + kSegQuantum - 1) / kSegQuantum * kSegQuantum);
+  KeyStage ks{nullptr, dyn, bm, N, rseg, (N + rseg - 1) / rseg, -1};
+  __syncthreads();
+  // the candidate list of the fast tier uses the key-staging area: (key, position) pairs
+  const int cap = rseg / 2;
+  const float* row_t = a.s_target ? a.s_target + (int64_t)b * a.t_sb + (int64_t)go * a.t_sg : nullptr;
+  // the tiers this workgroup selects, in order (one call site, so that the tier code is
+  // inlined once): D, then T -- with both tiers side by side T takes C_T, the k - |P|
+  // best, alone it takes I_T itself
+  const float* rows[2];
+  uint32_t needs[2];
+  int jobs = 0;
+  if (run_d) {
+    rows[jobs] = a.s_draft + (int64_t)b * a.d_sb + (int64_t)go * a.d_sg;
+    needs[jobs++] = (uint32_t)m;
+  }
+  if (run_t) {
+    rows[jobs] = row_t;
+    needs[jobs++] = (uint32_t)(both ? k - P : k - m - P);
+  }
+  for (int j = 0; j < jobs; ++j) {
+    ks.row = j == 0 ? rows[0] : rows[1];
+    ks.loaded = -1;
+    select_tier_fast(s, ks, j == 0 ? needs[0] : needs[1], bm, dyn, cap);
+  }
+
+  if (both) {
+    // publish this tier's bitmap, count in; the second to arrive merges
+    const int r = b * a.groups + go;
+    uint32_t* const maps = a.bitmaps + (int64_t)r * 2 * a.words;
+    const auto rs = __builtin_amdgcn_make_buffer_rsrc(maps, 0, 2 * a.words * 4, 0x00020000);
+    for (int w = tid; w < nwords; w += kTopkThreads)
+      __builtin_amdgcn_raw_buffer_store_b32(bm[w], rs, (tier * a.words + w) * 4, 0, kSC1);
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this thread's stores have completed
+    __syncthreads();                     // ... and every other thread's
+    if (tid == 0)
+      s.misc[2] = __hip_atomic_fetch_add(a.counters + r, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 1u;
+    __syncthreads();
+    if (!s.misc[2]) return;
+    if (tid == 0) __hip_atomic_store(a.counters + r, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    // the other tier's bitmap; then bm := P u I_D and the candidates C_T \ I_D listed in
+    // position order (in the key-staging area, (key, position) pairs; keys filled below)
+    const int other = 1 - tier;
+    for (int w = tid; w < nwords; w += kTopkThreads) {
+      const uint32_t mine = bm[w];
+      const uint32_t theirs = __builtin_amdgcn_raw_buffer_load_b32(rs, (other * a.words + w) * 4, 0, kSC1);
+      const uint32_t bd = tier == 0 ? mine : theirs, bt = tier == 0 ? theirs : mine;
+      bm[w] = bd;
+      dyn[seg - nwords + w] = bt & ~bd;  // C_T \ I_D, at the end of the key-staging area
+    }
+    __syncthreads();
+    const uint32_t* cand_words = dyn + seg - nwords;
+    const uint32_t c = ordered_bits(s, nwords, N, [&](int w) { return cand_words[w]; }, [](uint32_t, int) {});
+    const uint32_t need = (uint32_t)(k - m - P);
+    if (2 * c + nwords > (uint32_t)seg) {
+      // too many to list beside the words: the target tier again over the whole row, with
+      // P u I_D taken (the sequential form of Eq. 6)
+      ks.row = row_t;
+      ks.loaded = -1;
+      select_tier_fast_outlined(s, ks, need, bm, dyn, cap);
+    } else {
+      ordered_bits(s, nwords, N, [&](int w) { return cand_words[w]; },
+                   [&](uint32_t i, int n) { dyn[2 * i + 1] = (uint32_t)n; });
+      __syncthreads();
+      for (uint32_t i = tid; i < c; i += kTopkThreads) dyn[2 * i] = order_key(row_t[dyn[2 * i + 1]]);
+      __syncthreads();
+      select_list(s, dyn, (int)c, need, bm);
+    }
+  }
+
+  // ascending write-out of P u I_D u I_T
+  const uint32_t total = ordered_bits(s, nwords, N, [&](int w) { return bm[w]; }, [&](uint32_t pos, int n) {
+    if (pos < (uint32_t)k) out[pos] = n;  // never past the budget
+  });
   if (tid == 0) a.count[b * a.groups + go] = (int32_t)min(total, (uint32_t)k);
 }
 
@@ -543,7 +680,9 @@ hipError_t launch_topk(const TopkArgs& a, int B, hipStream_t stream) {
     if (e != hipSuccess) return e;
     if (dev >= 0 && dev < 64) lds_raised[dev] = true;
   }
-  dim3 grid(a.groups, B);
+  // two workgroups per (group, sequence) when the tiers hand off (the second of a row
+  // returns at once when its row has one tier)
+  dim3 grid(a.groups * (a.counters ? 2 : 1), B);
   hipLaunchKernelGGL(topk_kernel, grid, dim3(kTopkThreads), dyn, stream, a, seg);
   return hipGetLastError();
 }

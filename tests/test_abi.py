@@ -44,7 +44,9 @@ def test_status_strings_and_version(L):
 
 
 def test_workspace_sizes(L):
-    assert L.dustin_topk_workspace(16, 1, 32768) == 0
+    t = L.dustin_topk_workspace(16, 1, 32768)   # counters and two bitmaps per row
+    assert t >= 16 * 2 * 1024 * 4 and t % 256 == 0
+    assert L.dustin_topk_workspace(0, 1, 32768) == 0
     s = L.dustin_score_workspace(16, 32768, 4, 4)
     assert s >= 16 * 4 * 4 * 32768 * 4 and s % 256 == 0
     assert L.dustin_score_workspace(0, 10, 1, 1) == 0
@@ -69,9 +71,9 @@ def _kv(Hkv=2, d=128, cap=200):
     return kv
 
 
-def _topk(L, bt, sd=FAKE, st=FAKE, groups=1, ns=4, nw=16, idx=FAKE, cnt=FAKE):
+def _topk(L, bt, sd=FAKE, st=FAKE, groups=1, ns=4, nw=16, idx=FAKE, cnt=FAKE, ws=FAKE, ws_bytes=1 << 30):
     return L.dustin_topk(sd, 0, 0, st, 0, 0, ctypes.byref(bt), groups, ns, nw, idx, 0, 0, cnt,
-                         None, 0, None)
+                         ws, ws_bytes, None)
 
 
 def test_topk_rejects(L):
@@ -84,6 +86,10 @@ def test_topk_rejects(L):
     assert _topk(L, _batch(), idx=None) == D.ERR_INVALID_ARG
     assert _topk(L, _batch(), groups=0) == D.ERR_INVALID_ARG
     assert _topk(L, _batch(max_len=(1 << 19) + 1)) == D.ERR_UNSUPPORTED
+    # both tiers hand off through the workspace; one tier alone needs none
+    assert _topk(L, _batch(), ws=None, ws_bytes=0) == D.ERR_WORKSPACE
+    assert _topk(L, _batch(), ws=FAKE + 4) == D.ERR_WORKSPACE
+    assert _topk(L, _batch(), ws_bytes=64) == D.ERR_WORKSPACE
     bt = _batch()
     bt.seq_lens = None
     assert _topk(L, bt) == D.ERR_INVALID_ARG
