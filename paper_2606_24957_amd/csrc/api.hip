@@ -227,10 +227,10 @@ dustin_status prepare_attention(bool sparse, const void* q, int64_t q_sb, int64_
   a.rows_pad = rt * 16;
   const int64_t tokens_max = tokens + bt->nq_max;
   a.splits = attn_splits(B, Hkv, tokens_max);
-  a.sep_window = rt <= 3 ? 1 : 0;  // the kernels give the window a step of its own there
+  const bool sep = rt <= kAttnSepMaxRT;  // the kernels give the window a step of its own there
   // 32-token steps of the longest pair that the splits share: its selected (or committed)
-  // tokens, with the window's tokens as a step of their own when sep_window is set
-  const int64_t steps_max = a.sep_window ? (tokens > 0 ? (tokens + 31) / 32 : 1) : (tokens_max + 31) / 32;
+  // tokens, with the window's tokens as a step of their own when sep is set
+  const int64_t steps_max = sep ? (tokens > 0 ? (tokens + 31) / 32 : 1) : (tokens_max + 31) / 32;
   a.split_steps = (int)((steps_max + a.splits - 1) / a.splits);
   a.min_split_steps = env_int("DUSTIN_ATTN_SPLITS", 0) > 0 ? 1 : 8;
   call->rt = rt;

@@ -10,8 +10,9 @@
 //          congruent mod 8 (one XCD) and the last one to finish merges them (below).
 //   wave   walks 32-token steps of its workgroup's range (the four waves interleave
 //          steps).  A step's K and V rows go straight from HBM into a wave-private LDS
-//          tile with the gfx950 direct-to-LDS load (global_load_lds_dwordx4): every load
-//          instruction moves four whole 256-byte rows, and no VGPR holds data in flight.
+//          tile with a gfx950 direct-to-LDS load (buffer_load_dwordx4 ... lds, or
+//          global_load_lds_dwordx4; see load_lds16): every load instruction moves four
+//          whole 256-byte rows, and no VGPR holds data in flight.
 //          The chunks of a row are XOR-swizzled so that the MFMA operand reads below are
 //          free of bank conflicts.  Per step:
 //            wait for the step's rows, read K (MFMA A layout) and V^T (LDS transpose
@@ -34,6 +35,8 @@
 //
 // Gathered positions (sparse) and page translations (paged) are resolved into an LDS table
 // of physical rows before the token loop, so the loop does no dependent global loads.
+#include <type_traits>
+
 #include "kernels.hpp"
 
 namespace dustin {
@@ -59,9 +62,23 @@ __device__ __forceinline__ v4i16 lds_read_tr16(const char* p) {
   return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4i16*)(const_cast<char*>(p)));
 }
 
-// gfx950 direct-to-LDS load: lane l's 16 bytes at src land at lds + 16 l.
-__device__ __forceinline__ void load_lds16(const void* src, char* lds) {
-  __builtin_amdgcn_global_load_lds(src, (lds_void*)(lds), 16, 0, 0);
+// gfx950 direct-to-LDS loads: lane l's 16 bytes land at lds + 16 l.
+// The buffer form (byte offset off into a resource; past its extent reads zeros) is not a
+// FLAT instruction, so while such loads are in flight the compiler keeps counting loads in
+// order and waits for an earlier ordinary load with a partial vmcnt; with global_load_lds
+// in flight it waits with vmcnt(0).  Kernels that issue their first step speculatively use
+// the buffer form throughout; the others keep the global form, which measured faster for
+// them (and about 1% faster per launch in a plain full-chip gather, while the buffer form is
+// faster for one CU alone).
+__device__ __forceinline__ void load_lds16(__amdgpu_buffer_rsrc_t rs, uint32_t off, char* lds) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)(lds), 16, (int)off, 0, 0, 0);
+}
+__device__ __forceinline__ void load_lds16(const char* base, uint32_t off, char* lds) {
+  __builtin_amdgcn_global_load_lds(base + off, (lds_void*)(lds), 16, 0, 0);
+}
+// Resource over [base, base + bytes) (gfx9 raw buffer: stride 0, 32-bit data format)
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t byte_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, (int)bytes, 0x00020000);
 }
 
 __device__ __forceinline__ uint32_t cvt_pk_bf16(float lo, float hi) {
@@ -127,20 +144,25 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
   constexpr int kQPitch = kD + 8;  // LDS row pitch (bf16) of staged queries
   constexpr int kPitch = kD + 4;   // LDS row pitch (fp32) of the merged accumulator
   constexpr int kTilesBytes = kW * 2 * kTile;                    // K and V tiles of every wave
-  constexpr int kStageBytes = kStage ? kStageSteps * kStep * 4 : 0;
+  // The table of staged rows is an LDS object of its own up to three row tiles (then the
+  // compiler can tell that writing it does not touch a tile whose rows are in flight);
+  // beyond that it shares the tile area's object to leave LDS for the wave accumulators.
+  constexpr bool kOwnStage = kStage && RT <= 3;
+  constexpr int kStageBytes = kStage && !kOwnStage ? kStageSteps * kStep * 4 : 0;
   constexpr int kLoopBytes = kTilesBytes + kStageBytes;
   constexpr int kBufFloats = RT * 16 * kPitch;                  // one wave's accumulator
   constexpr int kNB = RT <= 4 ? kW : (RT <= 6 ? 2 : 1);          // wave accumulators LDS holds
   constexpr int kFinalBytes = kNB * kBufFloats * 4;
   __shared__ __attribute__((aligned(1024))) char smem[kLoopBytes > kFinalBytes ? kLoopBytes : kFinalBytes];
-  uint32_t* const sm_phys = reinterpret_cast<uint32_t*>(smem + kTilesBytes);
+  __shared__ __attribute__((aligned(16))) uint32_t sm_phys_own[kOwnStage ? kStageSteps * kStep : 4];
+  uint32_t* const sm_phys = kOwnStage ? sm_phys_own : reinterpret_cast<uint32_t*>(smem + kTilesBytes);
   // The queries are loaded once per workgroup (each thread a few 16-byte chunks) and
   // staged in LDS; with up to three row tiles every wave then copies them to registers
   // after the staging barrier, else they are read from LDS at every step.  They live in an
   // LDS object of their own: the compiler can then see that the direct-to-LDS row loads in
   // flight never write them, and reads them without waiting for those loads.
   __shared__ __attribute__((aligned(16))) uint16_t sm_q[RT * 16 * kQPitch];
-  // The verification window's tokens as a step of their own (when sep_window is set): one
+  // The verification window's tokens as a step of their own (up to three row tiles): one
   // wave of the pair's last split loads them in the prologue, beside its first step, into
   // this tile (K then V, the same layout as the wave tiles), and computes them while that
   // step is in flight.  The selected tokens then fill whole 32-token steps, so a pair of
@@ -194,6 +216,7 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
   // query slot, positions below k_max), which stays in bounds whatever the sizes are.
   int b = 0, g = 0, gi = 0;
   const int32_t* idx_row = nullptr;
+  bool idx_vec = false;  // the index row is 16-byte aligned (wave-uniform)
   int n_raw = 0, t_raw = 0, c_raw = 0;
   const int rows_mem = a.dims.nq_max * a.group_size;  // query rows present in memory
   auto q_row_ptr = [&](int r) {
@@ -205,13 +228,30 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
   bf16x8 qreg[kQReg ? RT : 1][4];
   constexpr int kQChunks = RT * 16 * (kD / 8), kQPer = (kQChunks + kW * kWave - 1) / (kW * kWave);
   u32x4 qx[kQPer];
-  int32_t sel[kStageBatch];  // selected positions of this thread's tokens in a chunk
-  auto load_selection = [&](int cs) {
+  // Entries v .. v + 7 of the index row (v a multiple of 8; entries from k_max on read the
+  // last one): two 16-byte loads where the row is aligned and the eight are inside it.
+  auto load_idx8 = [&](int v, int32_t (&dst)[8]) {
+    if (idx_vec && v + 8 <= a.dims.k_max) {
+      const u32x4 x0 = *reinterpret_cast<const u32x4*>(idx_row + v);
+      const u32x4 x1 = *reinterpret_cast<const u32x4*>(idx_row + v + 4);
 #pragma unroll
-    for (int j = 0; j < kStageBatch; ++j) {
-      const int v = cs * kStep + (int)threadIdx.x + j * kW * kWave;
-      sel[j] = kSparse ? idx_row[min(v, a.dims.k_max - 1)] : 0;
+      for (int i = 0; i < 4; ++i) {
+        dst[i] = (int32_t)x0[i];
+        dst[4 + i] = (int32_t)x1[i];
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) dst[i] = idx_row[min(v + i, a.dims.k_max - 1)];
     }
+  };
+  // selected positions of this thread's tokens in a chunk: tokens 8 t .. 8 t + 7 of it
+  int32_t sel[kStageBatch];
+  static_assert(kStageBatch == 8 && kStageSteps * kStep == 8 * kW * kWave, "staging layout");
+  auto load_selection = [&](int cs) {
+    if constexpr (kSparse) load_idx8(cs * kStep + 8 * (int)threadIdx.x, sel);
+    else
+#pragma unroll
+      for (int j = 0; j < kStageBatch; ++j) sel[j] = 0;
   };
   // the positions of this lane's tokens in the wave's first step, so that its loads can
   // start before the block-wide staging pass (contiguous caches; a paged one needs the
@@ -219,11 +259,19 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
   int first_v0 = 0;
   int32_t first_sel[8];
   int own_sizes = 0;  // lane 0: N_b, lane 1: T_b (if given), lane 2: the selection count
-  auto prologue_loads = [&]() {
+  auto locate = [&]() {
     b = pair / a.num_kv_heads;
     g = pair - b * a.num_kv_heads;
     gi = a.groups == 1 ? 0 : g;
     idx_row = kSparse ? a.idx + (int64_t)b * a.idx_sb + (int64_t)gi * a.idx_sg : nullptr;
+    idx_vec = ((uintptr_t)idx_row & 15) == 0;
+    first_v0 = (s_begin + wave) * kStep + 8 * lg;
+  };
+  // the first step's positions go first (contiguous caches): the first rows wait for them
+  auto first_loads = [&]() {
+    if constexpr (kStage && !kPaged) load_idx8(first_v0, first_sel);
+  };
+  auto prologue_loads = [&]() {
     // one gather by three lanes (read back lane by lane where first needed, so that no
     // wait for it lands among the loads below)
     {
@@ -243,13 +291,10 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
       qx[j] = load16(q_row_ptr(min(r, rows_mem - 1)) + c0);
     }
     if constexpr (kStage) load_selection(s_begin);
-    first_v0 = (s_begin + wave) * kStep + 8 * lg;
-    if constexpr (kStage && !kPaged) {
-#pragma unroll
-      for (int i = 0; i < 8; ++i) first_sel[i] = idx_row[min(first_v0 + i, a.dims.k_max - 1)];
-    }
   };
+  locate();
   if constexpr (kPaged) prologue_loads();
+  else first_loads();
   // sizes of pairs 4 lane .. 4 lane + 3 (every wave).  With a contiguous cache they are
   // issued before the prologue loads, so that waiting for them leaves those in flight while
   // the schedule is planned; with a paged cache the positions go first, since they feed
@@ -293,13 +338,88 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
   }
   if constexpr (!kPaged) prologue_loads();
 
+  // Rows are addressed as uniform base + 32-bit byte offset phys * stride_n (the host
+  // checks that every offset fits): phys is the position (contiguous) or
+  // page * page_size + slot (paged, pages laid out back to back).  The loads go through
+  // buffer resources over the pair's K and V rows, whose extent, (rows - 1) * stride +
+  // 256 bytes, bounds every offset the kernel forms.
+  const uint32_t kstride = (uint32_t)a.k.stride_n * 2u, vstride = (uint32_t)a.v.stride_n * 2u;
+  auto extent = [&](int64_t nrows, uint32_t stride) -> uint32_t {
+    const int64_t e = (nrows - 1) * (int64_t)stride + 256;
+    return (uint32_t)(e < (int64_t)UINT32_MAX ? e : (int64_t)UINT32_MAX);
+  };
+  __amdgpu_buffer_rsrc_t krs, vrs;
+  const char *kbase, *vbase;
+  auto set_rows = [&]() {
+    kbase = reinterpret_cast<const char*>(a.k.data + (kPaged ? 0 : (int64_t)b * a.k.stride_b) +
+                                          (int64_t)g * a.k.stride_h);
+    vbase = reinterpret_cast<const char*>(a.v.data + (kPaged ? 0 : (int64_t)b * a.v.stride_b) +
+                                          (int64_t)g * a.v.stride_h);
+    krs = byte_rsrc(kbase, extent(kPaged ? ((int64_t)a.k.num_pages << a.k.page_shift) : a.k.capacity, kstride));
+    vrs = byte_rsrc(vbase, extent(kPaged ? ((int64_t)a.v.num_pages << a.v.page_shift) : a.v.capacity, vstride));
+  };
+  set_rows();
+  // positions are 32-bit: N_b + T_b and the selected positions are int32 (a capacity
+  // beyond that bound leaves every int32 position inside it)
+  const int cap_m1 = (int)(a.k.capacity - 1 < INT32_MAX ? a.k.capacity - 1 : INT32_MAX - 1);
+
+  // Loads of one step into a K and a V tile: this lane moves chunk lr of tokens 8 lg + i
+  // (i = 0..7) of the step, whose physical rows are ph[i]; one instruction per i for K and
+  // one for V.  Buffer loads in the prologue (see load_lds16), global ones in the loop.
+  auto issue_rows_to = [&](const uint32_t (&ph)[8], char* kt, char* vt, auto buffered) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int j = 8 * lg + i;
+      if constexpr (decltype(buffered)::value) {
+        load_lds16(krs, ph[i] * kstride + 16 * k_chunk(j, lr), kt + i * 1024);
+        load_lds16(vrs, ph[i] * vstride + 16 * v_chunk(j, lr), vt + i * 1024);
+      } else {
+        load_lds16(kbase, ph[i] * kstride + 16 * k_chunk(j, lr), kt + i * 1024);
+        load_lds16(vbase, ph[i] * vstride + 16 * v_chunk(j, lr), vt + i * 1024);
+      }
+    }
+  };
+  using Buffered = std::true_type;
+  using Global = std::false_type;
+
+  // With a contiguous cache every wave issues its first step before the split schedule
+  // is known: the step of the guessed unit, from the positions it loaded first (the
+  // selected ones, or the positions themselves when dense), clamped into the cache.  The
+  // sizes, queries and row table then arrive and are staged while the step's rows are in
+  // flight.  Those are the step's right rows: a sparse kernel here has a window step of
+  // its own, so body tokens from the selection count on are masked, and a dense cache's
+  // window positions follow its committed ones.  If the guess was wrong, the wave waits
+  // for the rows to land and issues the step again.  The 16 loads are issued by every
+  // wave, so that the same number of loads follows the queries and positions on every
+  // path and the compiler can wait for them with a partial vmcnt.  (A paged cache needs
+  // the staged page translations first, and beyond three row tiles the table shares the
+  // tile area's LDS object: both issue the first step after staging, as do dense kernels
+  // beyond four row tiles, where the extra live registers would spill.)
+  constexpr bool kSpec = !kPaged && (kOwnStage || (!kStage && RT <= 4));
+  static_assert(!kSpec || !kSparse || RT <= kAttnSepMaxRT, "speculative sparse rows need the window step");
+  auto issue_first = [&](auto exact_pos) {
+    uint32_t ph[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      if constexpr (kStage) ph[i] = (uint32_t)exact_pos(first_v0 + i, first_sel[i]);
+      else ph[i] = (uint32_t)exact_pos(first_v0 + i, 0);
+    }
+    issue_rows_to(ph, ktile, vtile, Buffered{});
+  };
+  if constexpr (kSpec)
+    issue_first([&](int v, int32_t selected) { return clampi(kStage ? (int)selected : v, 0, cap_m1); });
+  bool relocate = false;  // the guess was wrong
+  // a wave leaves only once its speculative rows have landed in its tile
+  auto drain = [&]() {
+    if constexpr (kSpec) wait_vmem_all();
+  };
+
   // 32-token steps of a pair that the splits share: its selected (or all) positions, then
-  // its window -- or, with sep_window, the positions alone (at least one step)
+  // its window -- or, with a window step of its own, the positions alone (at least one step)
   // Row tiles up to which the window has a step of its own.  Beyond three the window tile
   // no longer fits beside four wave accumulators in LDS, and the second copy of the step
   // code makes the five-tile kernel spill.
-  constexpr int kSepMaxRT = 3;
-  const bool sep = RT <= kSepMaxRT && a.sep_window != 0;  // kernel-uniform
+  constexpr bool sep = RT <= kAttnSepMaxRT;
   auto steps_of = [&](int n, int t, int c) {
     const int Nc = clampi(n, 0, a.dims.max_len), Tc = clampi(t, 0, a.dims.nq_max);
     const int body = kSparse ? clampi(c, 0, a.dims.k_max) : Nc;
@@ -400,7 +520,10 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
     nsplit = __builtin_amdgcn_readfirstlane(nsplit);
     split_steps = __builtin_amdgcn_readfirstlane(split_steps);
     slot0 = __builtin_amdgcn_readfirstlane(slot0);
-    if (p_new < 0 || p_new >= a.pairs || slot0 < 0 || nsplit < 1 || slot0 + nsplit > U) return;
+    if (p_new < 0 || p_new >= a.pairs || slot0 < 0 || nsplit < 1 || slot0 + nsplit > U) {
+      drain();
+      return;
+    }
     // the pair's sizes, from the lane and slot that loaded them
     const int ol = p_new >> 2, oj = p_new & 3;
     auto owner = [&](const int (&v)[4]) {
@@ -412,11 +535,14 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
     if (p_new != pair || split_new * split_steps != s_begin) {  // the guess was wrong
       pair = p_new;
       s_begin = split_new * split_steps;
-      prologue_loads();
+      relocate = true;
     }
     split = split_new;
   } else {
-    if (!guess_ok) return;
+    if (!guess_ok) {
+      drain();
+      return;
+    }
     n_raw = __builtin_amdgcn_readlane(own_sizes, 0);
     t_raw = a.dims.n_query ? __builtin_amdgcn_readlane(own_sizes, 1) : a.dims.nq_max;
     c_raw = kSparse ? __builtin_amdgcn_readlane(own_sizes, 2) : 0;
@@ -424,34 +550,28 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
 
   const int N = clampi(n_raw, 0, a.dims.max_len);
   const int T = clampi(t_raw, 0, a.dims.nq_max);
-  if (T == 0) return;
+  if (T == 0) {
+    drain();
+    return;
+  }
   const int wstart = kSparse ? clampi(c_raw, 0, a.dims.k_max) : N;
   const int total = wstart + T;        // virtual tokens: selected (or all) then window
   const int rows = T * a.group_size;   // <= RT * 16 (checked on the host via nq_max)
   const int nsteps = sep ? max(1, (wstart + kStep - 1) / kStep) : (total + kStep - 1) / kStep;
-  if (s_begin >= nsteps) return;
+  if (s_begin >= nsteps) {
+    drain();
+    return;
+  }
   const int s_end = min(nsteps, s_begin + split_steps);
   // the wave that takes the window step: in the pair's last split, the last wave with the
   // fewest steps of the split (wave 3, or the last wave with a step when there are fewer
   // than four)
   const bool has_window = sep && split == nsplit - 1 && wave == min(kW - 1, s_end - s_begin - 1);
-  // with sep_window, tokens from wstart on are the window step's: body steps mask them
+  // with a window step, tokens from wstart on are the window's: body steps mask them
   const int body_limit = sep ? wstart - 1 : INT32_MAX;
-
-  // Rows are addressed as uniform base + 32-bit byte offset phys * stride_n (the host
-  // checks that every offset fits): phys is the position (contiguous) or
-  // page * page_size + slot (paged, pages laid out back to back).
-  const char* kbase = reinterpret_cast<const char*>(
-      a.k.data + (kPaged ? 0 : (int64_t)b * a.k.stride_b) + (int64_t)g * a.k.stride_h);
-  const char* vbase = reinterpret_cast<const char*>(
-      a.v.data + (kPaged ? 0 : (int64_t)b * a.v.stride_b) + (int64_t)g * a.v.stride_h);
-  const uint32_t kstride = (uint32_t)a.k.stride_n * 2u, vstride = (uint32_t)a.v.stride_n * 2u;
 
   // Position of virtual token v (clamped into the cache; past-the-end -> 0) and its
   // physical row.
-  // positions are 32-bit: N_b + T_b and the selected positions are int32 (a capacity
-  // beyond that bound leaves every int32 position inside it)
-  const int cap_m1 = (int)(a.k.capacity - 1 < INT32_MAX ? a.k.capacity - 1 : INT32_MAX - 1);
   auto pos_of = [&](int v, int32_t selected) -> int {
     const int pos = v < wstart ? (kSparse ? selected : v) : (v < total ? N + (v - wstart) : 0);
     return clampi(pos, 0, cap_m1);
@@ -466,6 +586,32 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
     else
       return (uint32_t)pos;
   };
+  // The window step's rows go to a tile of their own.
+  auto issue_window = [&](auto buffered) {
+    uint32_t ph[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      if constexpr (kPaged) ph[i] = sm_wphys[8 * lg + i];
+      else ph[i] = (uint32_t)pos_of(wstart + 8 * lg + i, 0);
+    }
+    issue_rows_to(ph, sm_win, sm_win + kTile, buffered);
+  };
+  if (relocate) {
+    if constexpr (kSpec) wait_vmem_all();  // the speculative rows have landed in this wave's tile
+    locate();
+    set_rows();
+    first_loads();
+    prologue_loads();
+  }
+  bool first_issued = false;
+  if constexpr (kSpec) {
+    // the speculative step was the wrong unit's: issue it again
+    if (relocate) issue_first([&](int v, int32_t selected) { return (int)phys_at(pos_of(v, selected), 0); });
+    first_issued = s_begin + wave < min(s_end, s_begin + kStageSteps);
+    // a wave whose first step lies beyond the first chunk issues it into the same tile
+    // later: the speculative rows land first
+    if (!first_issued) wait_vmem_all();
+  }
 
   int limit[RT];  // token v is visible to this lane's row iff v <= limit
 #pragma unroll
@@ -503,18 +649,6 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
 
   int chunk_v0 = 0;  // first virtual token staged in sm_phys
 
-  // Loads of one step into this wave's tiles: this lane moves chunk lr of tokens 8 lg + i
-  // (i = 0..7) of the step, whose physical rows are ph[i]; one instruction per i for K and
-  // one for V.
-  auto issue_rows_to = [&](const uint32_t (&ph)[8], char* kt, char* vt) {
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int j = 8 * lg + i;
-      load_lds16(kbase + ph[i] * kstride + 16 * k_chunk(j, lr), kt + i * 1024);
-      load_lds16(vbase + ph[i] * vstride + 16 * v_chunk(j, lr), vt + i * 1024);
-    }
-  };
-  auto issue_rows = [&](const uint32_t (&ph)[8]) { issue_rows_to(ph, ktile, vtile); };
   auto issue = [&](int st) {
     const int v0 = st * kStep + 8 * lg;
     uint32_t ph[8];
@@ -530,7 +664,7 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
 #pragma unroll
       for (int i = 0; i < 8; ++i) ph[i] = v0 + i < total ? (uint32_t)(v0 + i) : 0u;
     }
-    issue_rows(ph);
+    issue_rows_to(ph, ktile, vtile, std::integral_constant<bool, kSpec>{});
   };
 
   // With up to four row tiles a wave reads all of a step's operands into registers and
@@ -578,7 +712,7 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
   // product.  Scores stay in raw units until one FMA forms (s * scale * log2 e - m) inside
   // exp2; the reference max m is in scaled units.
   // v0: the virtual token of the tile's first row; vt: its V tile; win: the window step
-  // (causal mask per query row), else a body step (with sep_window, tokens from wstart on
+  // (causal mask per query row), else a body step (with a window step, tokens from wstart on
   // belong to the window step and are masked here).
   auto compute = [&](int v0, const Operands& op, const char* vt, bool win) {
     const bool edge = win || v0 + kStep - 1 >= wstart;  // wave-uniform: masking only near the window
@@ -639,7 +773,7 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
     int pos[kStageBatch];
     int page[kStageBatch];
 #pragma unroll
-    for (int j = 0; j < kStageBatch; ++j) pos[j] = pos_of(cs * kStep + (int)threadIdx.x + j * kW * kWave, sel[j]);
+    for (int j = 0; j < kStageBatch; ++j) pos[j] = pos_of(cs * kStep + 8 * (int)threadIdx.x + j, sel[j]);
 #pragma unroll
     for (int j = 0; j < kStageBatch; ++j) page[j] = kPaged ? page_of(pos[j]) : 0;
 #pragma unroll
@@ -647,15 +781,15 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
   };
   auto store_staged = [&](int cs, int ce) {
     chunk_v0 = cs * kStep;
-    const int nv = ce * kStep - chunk_v0;
-#pragma unroll
-    for (int j = 0; j < kStageBatch; ++j) {
-      const int e = (int)threadIdx.x + j * kW * kWave;
-      if (e < nv) sm_phys[e] = staged[j];
+    const int nv = ce * kStep - chunk_v0;  // a multiple of 32
+    if (8 * (int)threadIdx.x < nv) {
+      u32x4* dst = reinterpret_cast<u32x4*>(sm_phys + 8 * threadIdx.x);
+      dst[0] = u32x4{staged[0], staged[1], staged[2], staged[3]};
+      dst[1] = u32x4{staged[4], staged[5], staged[6], staged[7]};
     }
   };
-  // the first chunk's table is written before anything else is issued (and, paged, the
-  // window step's rows, by the first 32 threads of the workgroup that takes it)
+  // the first chunk's table (and, paged, the window step's rows, by the first 32 threads
+  // of the workgroup that takes it)
   const bool wg_window = sep && split == nsplit - 1;
   if constexpr (kStage) {
     stage_rows(s_begin);
@@ -667,34 +801,27 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
     }
     store_staged(s_begin, min(s_end, s_begin + kStageSteps));
   }
-  // The window step's rows go to its own tile, before the wave's first step, so that a
-  // wait for all but the last 16 loads (the step's) finds them in place.
-  auto issue_window = [&]() {
-    uint32_t ph[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      if constexpr (kPaged) ph[i] = sm_wphys[8 * lg + i];
-      else ph[i] = (uint32_t)pos_of(wstart + 8 * lg + i, 0);
-    }
-    issue_rows_to(ph, sm_win, sm_win + kTile);
-  };
-
-  // This wave's first step, if it lies in the first chunk, is issued right away: after
-  // every prologue load has been consumed, so that no later wait waits for its rows.
-  wait_vmem_all();
-  __builtin_amdgcn_sched_barrier(0);
-  bool first_issued = false;
-  if constexpr (!kPaged) {
-    if (has_window) issue_window();
+  if constexpr (kSpec) {
+    // The window's rows go after the staging (a conditional load between the queries' and
+    // positions' loads and their waits would cost the compiler its count); the wave
+    // computes them after its last step.
+    if (has_window) issue_window(Buffered{});
+  }
+  if constexpr (!kSpec) {
+    // every prologue load is consumed before the first global_load_lds (with those in
+    // flight the compiler would wait for all loads at the first use of any)
+    wait_vmem_all();
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  if constexpr (!kPaged && !kSpec) {
+    // the table shares the tiles' LDS object: the first step goes after its stores
+    if (has_window) issue_window(Global{});
     __builtin_amdgcn_sched_barrier(0);  // the window's loads stay ahead of the step's
     if (s_begin + wave < min(s_end, s_begin + kStageSteps)) {
       uint32_t ph[8];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        if constexpr (kStage) ph[i] = phys_at(pos_of(first_v0 + i, first_sel[i]), 0);
-        else ph[i] = first_v0 + i < total ? (uint32_t)(first_v0 + i) : 0u;
-      }
-      issue_rows(ph);
+      for (int i = 0; i < 8; ++i) ph[i] = phys_at(pos_of(first_v0 + i, first_sel[i]), 0);
+      issue_rows_to(ph, ktile, vtile, Global{});
       first_issued = true;
     }
   }
@@ -722,11 +849,11 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
     int st = cs + wave;
     if (st >= ce) continue;
     if constexpr (kPaged) {
-      if (has_window && cs == s_begin) issue_window();
+      if (has_window && cs == s_begin) issue_window(Global{});
       __builtin_amdgcn_sched_barrier(0);  // the window's loads stay ahead of the step's
     }
     if (!(first_issued && cs == s_begin)) issue(st);
-    if (has_window && cs == s_begin) {
+    if (!kSpec && has_window && cs == s_begin) {
       // the window's 16 loads were issued before the step's 16: wait for them alone and
       // compute the window while the step is in flight
       __builtin_amdgcn_s_waitcnt(0x4F70);  // vmcnt(16)
@@ -754,6 +881,14 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
       }
       if (next >= ce) break;
       st = next;
+    }
+  }
+  if constexpr (kSpec) {
+    if (has_window) {
+      wait_vmem_all();
+      Operands opw;
+      read_tiles_from(sm_win, sm_win + kTile, opw);
+      compute(wstart, opw, sm_win + kTile, true);
     }
   }
 

@@ -26,11 +26,15 @@ struct AttnArgs {
   int32_t split_steps;      // 32-token steps per split when every pair is as long as the longest
   int32_t min_split_steps;  // smallest split the kernel's balancing may choose
   int32_t rows_pad;
-  int32_t sep_window;       // 1: the window's tokens are one step of their own (T_max <= 32)
   float* part_acc;          // [pairs * splits, rows_pad, 128], by unit  (splits > 1 only)
   float* part_ml;           // [pairs * splits, rows_pad, 2]
   int32_t* counters;        // [pairs], zero between calls
 };
+
+// Row tiles (16 query rows each) up to which the attention kernel gives the verification
+// window's tokens a step of their own; beyond that they share the last step with the
+// selected (or committed) positions.
+constexpr int kAttnSepMaxRT = 3;
 
 // Pairs the attention kernel's split balancing handles (four per lane of one wave); with
 // more pairs there is one workgroup per pair.
