@@ -132,9 +132,24 @@ int32_t dustin_version(void);
  *   groups   1 or k->num_kv_heads
  *   init     fp32 [B, groups, >= max_len] (strides init_sb, init_sg) or NULL (= 0)
  *   out      fp32 [B, groups, >= max_len] (strides out_sb, out_sg); may alias init
- *   workspace  device scratch of dustin_score_workspace() bytes, 256-byte aligned
+ *   workspace  device scratch of dustin_score_workspace() bytes, 256-byte aligned.  Its
+ *              first DUSTIN_SCORE_SYNC_BYTES bytes must be zero before the first call;
+ *              every call leaves them zero (the int32 at DUSTIN_SCORE_SYNC_FLAG_OFFSET
+ *              aside, see below).  Calls that share a workspace must not overlap.
  * Rounding: fp32 dot products (bf16 products are exact), fp32 exp and sums.
+ * Two forms compute the same sums.  When every (head, query) pair fits one 16-column
+ * MFMA tile (n_heads * nq_max <= 16, scoring heads over at most 4 KV heads), groups == 1
+ * and batch <= 2048, one launch does everything: each workgroup keeps the logits of a
+ * chunk of positions in registers and the chunks of a sequence exchange only their
+ * softmax statistics, through per-sequence counters at the start of the workspace (a
+ * bounded wait; the chunks of a sequence are dispatched together and are few against the
+ * GPU's compute units).  Should that wait ever time out, the kernel writes 1 to the
+ * int32 at byte DUSTIN_SCORE_SYNC_FLAG_OFFSET of the workspace and its output is
+ * unspecified; zero the first DUSTIN_SCORE_SYNC_BYTES bytes again before reusing the
+ * workspace.  Otherwise the logits go through the workspace in two launches.
  * --------------------------------------------------------------------------------- */
+#define DUSTIN_SCORE_SYNC_BYTES 16896u
+#define DUSTIN_SCORE_SYNC_FLAG_OFFSET 16384u
 size_t dustin_score_workspace(int32_t batch, int32_t max_len, int32_t nq_max, int32_t n_heads);
 dustin_status dustin_score(const void* q, int64_t q_sb, int64_t q_sj, int64_t q_sh,
                            int32_t num_q_heads, const int32_t* heads_host, int32_t n_heads,
@@ -147,13 +162,15 @@ dustin_status dustin_score(const void* q, int64_t q_sb, int64_t q_sj, int64_t q_
  * dustin_score_layers -- Eq. 5 summed over n_layers scored layers in one call (the draft
  * side: S_D sums the scoring heads of the draft model's scoring layers, Eq. 5 upper):
  *   out = init + sum over layers l of the dustin_score sum of layer l
- * in two launches whatever n_layers is.  The layers share every shape and stride:
+ * in at most two launches whatever n_layers is.  The layers share every shape and stride:
  *   q_layers_host  host array of n_layers device pointers, each laid out as q above
  *   k_layers_host  host array of n_layers dustin_kv that differ only in `data`
  *   1 <= n_layers <= 32; n_layers * n_heads * nq_max <= 1024; batch * n_layers <= 65535
  *   workspace  dustin_score_workspace(batch, max_len, nq_max, n_heads * n_layers) bytes
  * Every other argument is as for dustin_score.  The sum over layers is accumulated in
- * fp32 together with the heads' and queries' terms and rounded once at the end.
+ * fp32 together with the heads' and queries' terms and rounded once at the end.  The
+ * single-pass form applies as for dustin_score (the pair limit counts one layer's pairs),
+ * in one launch whatever n_layers is.
  * --------------------------------------------------------------------------------- */
 dustin_status dustin_score_layers(int32_t n_layers, const void* const* q_layers_host, int64_t q_sb,
                                   int64_t q_sj, int64_t q_sh, int32_t num_q_heads,

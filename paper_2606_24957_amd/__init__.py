@@ -189,6 +189,24 @@ def workspace(nbytes: int, device, tag: str, stream=None) -> Optional[torch.Tens
     return buf[off:off + nbytes]
 
 
+# Layout of a score workspace's first bytes (include/dustin.h): per-sequence counters of
+# the single-pass form, zero between calls, and its timeout flag.
+SCORE_SYNC_BYTES = 16896
+SCORE_SYNC_FLAG_OFFSET = 16384
+
+
+def score_sync_region(device=None, stream=None, tag: str = "score") -> Optional[torch.Tensor]:
+    """The counters and flag at the start of the cached score workspace of (device,
+    stream), as uint8 (None if no score call has made one)."""
+    dev = torch.device("cuda", torch.cuda.current_device()) if device is None else torch.device(device)
+    s = torch.cuda.current_stream(dev) if stream is None else stream
+    buf = _WS.get((str(dev), int(s.cuda_stream), tag))
+    if buf is None:
+        return None
+    off = (-buf.data_ptr()) % 256
+    return buf[off:off + SCORE_SYNC_BYTES]
+
+
 def release_workspaces() -> None:
     """Drops the cached workspaces (after synchronising the device), so that a program can
     return their memory to the allocator before it exits."""

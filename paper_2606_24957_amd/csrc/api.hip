@@ -289,12 +289,72 @@ int32_t dustin_version(void) { return (1 << 16) | 0; }
 
 namespace {
 
-// workspace of one score call: fp32 logits rows of `cols` entries (a multiple of 64) and
-// per-chunk statistics, for `rows` (layer, sequence, head, query) rows
+// workspace of one score call: the single-pass form's counters (kScoreSyncBytes, zero
+// between calls, at the start whatever form a call takes), then fp32 logits rows of `cols`
+// entries (a multiple of 64) and per-chunk statistics, for `rows` (layer, sequence, head,
+// query) rows.  The single-pass form keeps its per-chunk statistics where the logits go.
 size_t score_ws_bytes(size_t rows, size_t cols, size_t chunk) {
   const size_t ld = round_up(cols, 64);
   const size_t n_chunks = (cols + chunk - 1) / chunk;
-  return round_up(rows * ld * sizeof(float), kAlign) + round_up(rows * n_chunks * 2 * sizeof(float), kAlign);
+  return kScoreSyncBytes + round_up(rows * ld * sizeof(float), kAlign) +
+         round_up(rows * n_chunks * 2 * sizeof(float), kAlign);
+}
+
+// The single-pass form (score_sync.hip) for a call with at most 16 (head, query) pairs over
+// at most 4 KV heads, one output group and one output: fills the sync fields of a and
+// returns the tiles per wave (0: the call takes the two-pass form).
+int score_sync_plan(ScoreArgs& a, int32_t n_heads, int32_t nq_max, int row_dim, int B, int64_t max_len,
+                    int32_t groups, size_t logits_bytes, int* nu_out) {
+  if (a.page_mode || a.per_layer || groups != 1 || B > kScoreSyncMaxBatch) return 0;
+  if (row_dim != 64 && row_dim != 128) return 0;
+  if ((int64_t)n_heads * nq_max > 16) return 0;
+  // used KV heads in ascending order; columns KV head by KV head, then head slot, then query
+  int nu = 0;
+  for (int i = 0; i < n_heads; ++i) {
+    const int g = a.heads[i] / a.group_size;
+    int at = 0;
+    while (at < nu && a.sync_kv[at] < g) ++at;
+    if (at < nu && a.sync_kv[at] == g) continue;
+    if (nu == 4) return 0;
+    for (int v = nu; v > at; --v) a.sync_kv[v] = a.sync_kv[v - 1];
+    a.sync_kv[at] = g;
+    ++nu;
+  }
+  if (nu == 0) return 0;
+  int np = 0;
+  for (int u = 0; u < nu; ++u)
+    for (int i = 0; i < n_heads; ++i) {
+      if (a.heads[i] / a.group_size != a.sync_kv[u]) continue;
+      for (int jq = 0; jq < nq_max; ++jq) {
+        a.sync_col_slot[np] = (uint8_t)i;
+        a.sync_col_query[np] = (uint8_t)jq;
+        a.sync_col_u[np] = (uint8_t)u;
+        ++np;
+      }
+    }
+  // Chunks of 256 tw positions: eight tiles per wave once the batch fills the chip with
+  // them.  The form keeps one workgroup on a CU for the whole call, so it is taken only
+  // when every chunk the sizes allow gets a CU at once (beyond that, the two-pass form's
+  // many small workgroups balance the load better).
+  int tw = (int64_t)B * max_len >= (int64_t)192 * 2048 ? 8 : 2;
+  const int64_t chunks = (max_len + 256 * tw - 1) / (256 * tw);
+  if (chunks > kScoreSyncMaxChunks || (int64_t)B * chunks > kScoreSyncCUs) return 0;
+  // a sequence's chunks on one XCD when they fit there with the other sequences of that XCD
+  a.sync_local = (B + 7) / 8 * chunks <= kScoreSyncCUs / 8 ? 1 : 0;
+  if ((size_t)a.n_layers * B * chunks * 16 * 2 * sizeof(float) > logits_bytes) return 0;
+  // every K row the kernel reads lies within 2^31 bytes of its buffer resource's base (a
+  // sequence's rows, or the page pool)
+  const int64_t rows_bytes = a.k.page_table
+                                 ? (int64_t)(a.k.num_pages - 1) * a.k.stride_page * 2 +
+                                       (int64_t)((1 << a.k.page_shift) - 1) * a.k.stride_n * 2
+                                 : (a.k.capacity - 1) * a.k.stride_n * 2;
+  const int64_t extent = rows_bytes + (int64_t)a.sync_kv[nu - 1] * a.k.stride_h * 2 + (int64_t)row_dim * 2;
+  if (rows_bytes < 0 || extent > INT32_MAX) return 0;
+  a.sync_extent = (int32_t)extent;
+  a.sync_np = np;
+  a.sync_chunks = (int32_t)chunks;
+  *nu_out = nu;
+  return tw;
 }
 
 int log2_exact(int x) {
@@ -375,10 +435,20 @@ dustin_status score_launch(ScoreArgs& a, int n_groups, int max_group, int row_di
   a.nq_max = nq_max;
   a.ld = (int64_t)round_up((size_t)cols, 64);
   a.n_chunks = (int32_t)((cols + a.chunk - 1) / a.chunk);
-  a.logits = static_cast<float*>(workspace);
-  a.stats = reinterpret_cast<float*>(static_cast<char*>(workspace) +
-                                     round_up(rows * a.ld * sizeof(float), kAlign));
-  const hipError_t e = launch_score(a, B, n_groups, max_group, row_dim, static_cast<hipStream_t>(stream));
+  char* const base = static_cast<char*>(workspace);
+  a.sync = reinterpret_cast<int32_t*>(base);
+  a.logits = reinterpret_cast<float*>(base + kScoreSyncBytes);
+  const size_t logits_bytes = round_up(rows * a.ld * sizeof(float), kAlign);
+  a.stats = reinterpret_cast<float*>(base + kScoreSyncBytes + logits_bytes);
+  int nu = 0;
+  const int tw = score_sync_plan(a, a.n_heads, nq_max, row_dim, B, cols, groups, logits_bytes, &nu);
+  hipError_t e;
+  if (tw) {
+    a.stats = a.logits;  // the single-pass form's per-chunk statistics
+    e = launch_score_sync(a, row_dim, nu, tw, static_cast<hipStream_t>(stream));
+  } else {
+    e = launch_score(a, B, n_groups, max_group, row_dim, static_cast<hipStream_t>(stream));
+  }
   return e == hipSuccess ? DUSTIN_OK : DUSTIN_ERR_LAUNCH;
 }
 

@@ -53,6 +53,17 @@ constexpr int kScoreMaxEntries = 64;     // pass-1 column tiles: (KV head, up to
 constexpr int kScoreGroupTiles = 3;      // column tiles of one KV head per pass-1 workgroup
 constexpr int kScoreMaxLayers = 32;
 constexpr int kScoreMaxPairs = 1024;     // (layer, head, query) rows one output sums
+// Single-pass form (score_sync.hip): the workspace starts with kScoreSyncBytes of
+// per-sequence counters (zero between calls) and a timeout flag; every form of the score
+// keeps its logits and statistics after them.
+constexpr int kSyncWaves = 16;             // waves per single-pass workgroup
+constexpr int kScoreSyncMaxBatch = 2048;   // sequences the counters cover
+constexpr int kScoreSyncMaxChunks = 128;   // chunks of one sequence (far below the chip's CUs)
+constexpr int kScoreSyncCUs = 256;         // MI355X compute units: one single-pass workgroup each
+constexpr size_t kScoreSyncBytes = 16896;  // 2 * kScoreSyncMaxBatch counters + the flag, 256-aligned
+static_assert(kScoreSyncBytes >= (2 * kScoreSyncMaxBatch + 1) * 4 && kScoreSyncBytes % 256 == 0, "sync region");
+static_assert(kScoreSyncBytes == DUSTIN_SCORE_SYNC_BYTES && 2 * kScoreSyncMaxBatch * 4 == DUSTIN_SCORE_SYNC_FLAG_OFFSET,
+              "the workspace layout the header documents");
 
 // Eq. 5 over the positions of a cache, or (page mode) over the pages of a page-statistics
 // array, whose rows [max | min] of length 2d meet the sign-split query [q+ | q-].
@@ -86,12 +97,22 @@ struct ScoreArgs {
   float* stats;   // [n_layers, B, n_heads, nq_max, n_chunks, 2]  (max, sum of exp2) per chunk
   int64_t ld;
   int32_t nq_max, n_chunks;
+  // single-pass form: columns 0 .. sync_np - 1 are (head slot, query) pairs on used KV head
+  // sync_col_u (KV head sync_kv[u]); sync_chunks chunks of positions per sequence
+  int32_t* sync;
+  int32_t sync_np, sync_chunks;
+  int32_t sync_local;   // 1: a sequence's chunks are consecutive among one XCD's block ids
+  int32_t sync_extent;  // bytes of K rows one buffer resource covers (a sequence, or the page pool)
+  int32_t sync_kv[4];
+  uint8_t sync_col_slot[16], sync_col_query[16], sync_col_u[16];
 };
 static_assert(sizeof(ScoreArgs) <= 4096, "kernel arguments stay within 4 KiB");
 
 // n_groups pass-1 workgroups along x (tile_first / tile_count), max_group the largest
 // tile count; row_dim: length of a K row (head_dim, or 2 * head_dim for page statistics)
 hipError_t launch_score(const ScoreArgs& a, int B, int n_groups, int max_group, int row_dim, hipStream_t stream);
+// the single-pass form: nu used KV heads (1..4), tw tiles of 16 positions per wave (2 or 8)
+hipError_t launch_score_sync(const ScoreArgs& a, int head_dim, int nu, int tw, hipStream_t stream);
 
 // ---- attention recovery rate (arr.hip) ----
 struct ArrArgs {

@@ -15,6 +15,7 @@
 namespace dustin {
 hipError_t launch_verify_attn(const AttnArgs&, int, bool, bool, hipStream_t) { return hipErrorInvalidValue; }
 hipError_t launch_score(const ScoreArgs&, int, int, int, int, hipStream_t) { return hipErrorInvalidValue; }
+hipError_t launch_score_sync(const ScoreArgs&, int, int, int, hipStream_t) { return hipErrorInvalidValue; }
 hipError_t launch_arr(const ArrArgs&, int, hipStream_t) { return hipErrorInvalidValue; }
 hipError_t launch_page_meta(const PageMetaArgs&, int, int, hipStream_t) { return hipErrorInvalidValue; }
 hipError_t launch_topk(const TopkArgs&, int, hipStream_t) { return hipErrorInvalidValue; }

@@ -48,12 +48,21 @@ def test_workspace_sizes(L):
     assert t >= 16 * 2 * 1024 * 4 and t % 256 == 0
     assert L.dustin_topk_workspace(0, 1, 32768) == 0
     s = L.dustin_score_workspace(16, 32768, 4, 4)
-    assert s >= 16 * 4 * 4 * 32768 * 4 and s % 256 == 0
+    assert s >= D.SCORE_SYNC_BYTES + 16 * 4 * 4 * 32768 * 4 and s % 256 == 0
     assert L.dustin_score_workspace(0, 10, 1, 1) == 0
     # attention: a split-K workspace once the batch leaves compute units idle
     w = L.dustin_attn_workspace(16, 64, 8, 5, 2048, 1)
     assert w == 0 or w > 4096
     assert L.dustin_attn_workspace(0, 64, 8, 5, 2048, 1) == 0
+
+
+def test_score_sync_layout_matches_the_header():
+    """The binding's copy of the score workspace's counter region and flag offset."""
+    text = open(HEADER).read()
+    got = {k: int(v) for k, v in re.findall(r"#define (DUSTIN_SCORE_SYNC_\w+) (\d+)u", text)}
+    assert got == {"DUSTIN_SCORE_SYNC_BYTES": D.SCORE_SYNC_BYTES,
+                   "DUSTIN_SCORE_SYNC_FLAG_OFFSET": D.SCORE_SYNC_FLAG_OFFSET}
+    assert D.SCORE_SYNC_FLAG_OFFSET + 4 <= D.SCORE_SYNC_BYTES and D.SCORE_SYNC_BYTES % 256 == 0
 
 
 def _batch(B=2, max_len=100, nq=4, k_max=40, m=10):
