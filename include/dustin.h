@@ -181,6 +181,41 @@ dustin_status dustin_score_layers(int32_t n_layers, const void* const* q_layers_
                                   size_t workspace_bytes, void* stream);
 
 /* ---------------------------------------------------------------------------------
+ * dustin_score_calls -- one or two dustin_score_layers calls, such as the target's and the
+ * draft's scores of one verification step (both halves of Eq. 5).  Two calls run in one
+ * launch when both take the single-pass form with the pair of shapes compiled for it (the
+ * first over four KV heads of 128-element rows, the second over two KV heads of 64-element
+ * rows, both with the same tiles per wave): the second call's workgroups then start as the
+ * first call's leave their compute units.  Otherwise the calls run one after the other.
+ * Either way each output has the same bits as the corresponding dustin_score_layers call.
+ *   calls    host array of n_calls (1 or 2) descriptors; each holds the arguments of one
+ *            dustin_score_layers call (n_layers = 1 is a dustin_score call), with a
+ *            workspace of its own (distinct workspaces; each as dustin_score requires)
+ * Neither call may write a buffer that the other reads or writes.  Errors: as
+ * dustin_score_layers for either call (nothing is enqueued), DUSTIN_ERR_INVALID_ARG for
+ * n_calls outside [1, 2], DUSTIN_ERR_WORKSPACE for a shared workspace.
+ * --------------------------------------------------------------------------------- */
+typedef struct {
+  int32_t n_layers;
+  const void* const* q_layers_host;
+  int64_t q_sb, q_sj, q_sh;
+  int32_t num_q_heads;
+  const int32_t* heads_host;
+  int32_t n_heads;
+  const dustin_kv* k_layers_host;
+  const dustin_batch* bt;
+  float scale;
+  int32_t groups;
+  const float* init;
+  int64_t init_sb, init_sg;
+  float* out;
+  int64_t out_sb, out_sg;
+  void* workspace;
+  size_t workspace_bytes;
+} dustin_score_call;
+dustin_status dustin_score_calls(int32_t n_calls, const dustin_score_call* calls, void* stream);
+
+/* ---------------------------------------------------------------------------------
  * dustin_score_per_layer -- Eq. 5 for n_layers layers in two launches, each layer into
  * its own output: the per-layer, per-head relevance of the SpecAttn-style selection the
  * paper compares with (appendix on SpecAttn: every draft layer and head scores tokens for

@@ -30,7 +30,7 @@ EXPORTED = ("dustin_status_string", "dustin_version", "dustin_score_workspace", 
             "dustin_sparse_verify_attn", "dense_verify_attn", "dustin_kv_append", "dustin_kv_commit",
             "dustin_score_layers", "dustin_page_meta", "dustin_page_score_workspace",
             "dustin_page_score", "dustin_arr", "dustin_score_per_layer",
-            "dustin_sparse_verify_attn_noalloc")
+            "dustin_sparse_verify_attn_noalloc", "dustin_score_calls")
 
 
 class DustinError(RuntimeError):
@@ -54,6 +54,18 @@ class DustinBatch(ctypes.Structure):
                 ("seq_lens", ctypes.c_void_p), ("n_query", ctypes.c_void_p),
                 ("budget", ctypes.c_void_p), ("m", ctypes.c_void_p),
                 ("m_scalar", ctypes.c_int32)]
+
+
+class DustinScoreCall(ctypes.Structure):
+    """dustin_score_call: the arguments of one dustin_score_layers call."""
+    _fields_ = [("n_layers", ctypes.c_int32), ("q_layers_host", ctypes.c_void_p),
+                ("q_sb", ctypes.c_int64), ("q_sj", ctypes.c_int64), ("q_sh", ctypes.c_int64),
+                ("num_q_heads", ctypes.c_int32), ("heads_host", ctypes.c_void_p),
+                ("n_heads", ctypes.c_int32), ("k_layers_host", ctypes.c_void_p),
+                ("bt", ctypes.c_void_p), ("scale", ctypes.c_float), ("groups", ctypes.c_int32),
+                ("init", ctypes.c_void_p), ("init_sb", ctypes.c_int64), ("init_sg", ctypes.c_int64),
+                ("out", ctypes.c_void_p), ("out_sb", ctypes.c_int64), ("out_sg", ctypes.c_int64),
+                ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_size_t)]
 
 
 _lib = None
@@ -116,6 +128,8 @@ def lib():
                                              ctypes.c_float, _i32, _vp, _i64, _i64, _i64, _vp, _sz, _vp]
         L.dustin_arr.restype = ctypes.c_int
         L.dustin_arr.argtypes = [_vp, _i64, _i64, _vp, _i64, _i64, _vp, P_BT, _i32, _i32, _vp, _vp]
+        L.dustin_score_calls.restype = ctypes.c_int
+        L.dustin_score_calls.argtypes = [_i32, ctypes.POINTER(DustinScoreCall), _vp]
         L.dustin_kv_commit.restype = ctypes.c_int
         L.dustin_kv_commit.argtypes = [_vp, _vp, _vp, _i32, _i32, _vp]
         _lib = L
@@ -269,14 +283,32 @@ def _batch(B, max_len, nq_max, k_max, seq_lens, n_query=None, budget=None, m=Non
 
 # ----------------------------------------------------------------------------- score
 
+def _score_desc(n_layers, q_host, q0, Hq, heads_host, n_heads, kv_addr, bt, scale, groups, init, ins, out, ws,
+                nbytes) -> DustinScoreCall:
+    """The dustin_score_call of a planned score call (its buffers are kept by the plan)."""
+    c = DustinScoreCall()
+    c.n_layers = n_layers
+    c.q_layers_host = ctypes.addressof(q_host)
+    c.q_sb, c.q_sj, c.q_sh = q0.stride(0), q0.stride(1), q0.stride(2)
+    c.num_q_heads, c.heads_host, c.n_heads = Hq, ctypes.addressof(heads_host), n_heads
+    c.k_layers_host, c.bt = kv_addr, ctypes.addressof(bt)
+    c.scale, c.groups = float(scale), int(groups)
+    c.init = None if init is None else init.data_ptr()
+    c.init_sb, c.init_sg = ins
+    c.out, c.out_sb, c.out_sg = out.data_ptr(), out.stride(0), out.stride(1)
+    c.workspace, c.workspace_bytes = (None if ws is None else ws.data_ptr()), nbytes
+    return c
+
+
 def plan_score(q: torch.Tensor, k: torch.Tensor, seq_lens, heads: Sequence[int], *,
                n_query=None, scale: Optional[float] = None, groups: int = 1,
                init: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None,
                max_len: Optional[int] = None, page_table: Optional[torch.Tensor] = None,
-               stream=None) -> Call:
+               stream=None, ws_tag: str = "score") -> Call:
     """Prepared dustin_score (Eq. 5 over the scoring heads).  q bf16 [B, nq_max, Hq, d];
     k bf16 [B, N_cap, Hkv, d] (or paged with page_table); init / out fp32
-    [B, groups, >= max_len]."""
+    [B, groups, >= max_len].  ws_tag names the cached workspace (calls that are to run in
+    one dustin_score_calls need different ones)."""
     _on_gpu(q, k, init, out, page_table)
     B, nq_max, Hq, d = q.shape
     dev = q.device
@@ -292,13 +324,18 @@ def plan_score(q: torch.Tensor, k: torch.Tensor, seq_lens, heads: Sequence[int],
     heads_host = (ctypes.c_int32 * len(heads))(*[int(h) for h in heads])
     bt = _batch(B, max_len, nq_max, 0, seq, nqa)
     nbytes = lib().dustin_score_workspace(B, max_len, nq_max, len(heads))
-    ws = workspace(nbytes, dev, "score", stream)
+    ws = workspace(nbytes, dev, ws_tag, stream)
     scale = 1.0 / math.sqrt(d) if scale is None else scale
     ins = (init.stride(0), init.stride(1)) if init is not None else (0, 0)
     args = (_ptr(q), q.stride(0), q.stride(1), q.stride(2), Hq, heads_host, len(heads),
             ctypes.byref(kv), ctypes.byref(bt), float(scale), int(groups), _ptr(init), ins[0],
             ins[1], _ptr(out), out.stride(0), out.stride(1), _ptr(ws), nbytes, _stream(stream))
-    return Call(lib().dustin_score, args, "dustin_score", (q, k, init, kv, bt, ws, heads_host), out)
+    q_host = (ctypes.c_void_p * 1)(q.data_ptr())
+    desc = _score_desc(1, q_host, q, Hq, heads_host, len(heads), ctypes.addressof(kv), bt, scale, groups,
+                       init, ins, out, ws, nbytes)
+    c = Call(lib().dustin_score, args, "dustin_score", (q, k, init, kv, bt, ws, heads_host, q_host), out)
+    c.desc = desc
+    return c
 
 
 def score(q, k, seq_lens, heads, **kw):
@@ -310,9 +347,9 @@ def plan_score_layers(qs: Sequence[torch.Tensor], ks: Sequence[torch.Tensor], se
                       heads: Sequence[int], *, n_query=None, scale: Optional[float] = None,
                       groups: int = 1, init: Optional[torch.Tensor] = None,
                       out: Optional[torch.Tensor] = None, max_len: Optional[int] = None,
-                      page_table: Optional[torch.Tensor] = None, stream=None) -> Call:
+                      page_table: Optional[torch.Tensor] = None, stream=None, ws_tag: str = "score") -> Call:
     """Prepared dustin_score_layers: Eq. 5 summed over layers (qs[l], ks[l]) that share every
-    shape and stride, into one output, in two launches."""
+    shape and stride, into one output, in one launch or two."""
     if len(qs) != len(ks) or not qs:
         raise ValueError("one query tensor per cache, at least one layer")
     _on_gpu(*qs, *ks, init, out, page_table)
@@ -337,19 +374,35 @@ def plan_score_layers(qs: Sequence[torch.Tensor], ks: Sequence[torch.Tensor], se
     q_host = (ctypes.c_void_p * len(qs))(*[q.data_ptr() for q in qs])
     bt = _batch(B, max_len, nq_max, 0, seq, nqa)
     nbytes = lib().dustin_score_workspace(B, max_len, nq_max, len(heads) * len(qs))
-    ws = workspace(nbytes, dev, "score", stream)
+    ws = workspace(nbytes, dev, ws_tag, stream)
     scale = 1.0 / math.sqrt(d) if scale is None else scale
     ins = (init.stride(0), init.stride(1)) if init is not None else (0, 0)
     args = (len(qs), q_host, q0.stride(0), q0.stride(1), q0.stride(2), Hq, heads_host, len(heads),
             kvs, ctypes.byref(bt), float(scale), int(groups), _ptr(init), ins[0], ins[1], _ptr(out),
             out.stride(0), out.stride(1), _ptr(ws), nbytes, _stream(stream))
-    return Call(lib().dustin_score_layers, args, "dustin_score_layers",
-                (tuple(qs), tuple(ks), init, kvs, bt, ws, heads_host, q_host), out)
+    c = Call(lib().dustin_score_layers, args, "dustin_score_layers",
+             (tuple(qs), tuple(ks), init, kvs, bt, ws, heads_host, q_host), out)
+    c.desc = _score_desc(len(qs), q_host, q0, Hq, heads_host, len(heads), ctypes.addressof(kvs), bt, scale,
+                         groups, init, ins, out, ws, nbytes)
+    return c
 
 
 def score_layers(qs, ks, seq_lens, heads, **kw):
     """Eq. 5 summed over layers; returns out (positions >= N_b untouched)."""
     return plan_score_layers(qs, ks, seq_lens, heads, **kw)()
+
+
+def plan_score_calls(calls: Sequence[Call], stream=None) -> Call:
+    """Prepared dustin_score_calls: one or two planned score calls (plan_score or
+    plan_score_layers, each with its own workspace tag) in one launch where the library can
+    (the target's and the draft's scores of a step), else one after the other.  Returns the
+    outputs of the calls."""
+    if not 1 <= len(calls) <= 2 or any(getattr(c, "desc", None) is None for c in calls):
+        raise ValueError("one or two calls planned by plan_score or plan_score_layers")
+    arr = (DustinScoreCall * len(calls))(*[c.desc for c in calls])
+    args = (len(calls), arr, _stream(stream))
+    return Call(lib().dustin_score_calls, args, "dustin_score_calls", (tuple(calls), arr),
+                tuple(c.result for c in calls))
 
 
 def plan_score_per_layer(qs: Sequence[torch.Tensor], ks: Sequence[torch.Tensor], seq_lens,

@@ -301,34 +301,36 @@ size_t score_ws_bytes(size_t rows, size_t cols, size_t chunk) {
 }
 
 // The single-pass form (score_sync.hip) for a call with at most 16 (head, query) pairs over
-// at most 4 KV heads, one output group and one output: fills the sync fields of a and
-// returns the tiles per wave (0: the call takes the two-pass form).
-int score_sync_plan(ScoreArgs& a, int32_t n_heads, int32_t nq_max, int row_dim, int B, int64_t max_len,
-                    int32_t groups, size_t logits_bytes, int* nu_out) {
-  if (a.page_mode || a.per_layer || groups != 1 || B > kScoreSyncMaxBatch) return 0;
-  if (row_dim != 64 && row_dim != 128) return 0;
-  if ((int64_t)n_heads * nq_max > 16) return 0;
+// at most 4 KV heads, one output group and one output (a's heads, layers, cache view, dims,
+// output and workspace fields set): fills sc and returns true, or false when the call
+// takes the two-pass form.
+bool score_sync_plan(const ScoreArgs& a, int32_t n_heads, int32_t nq_max, int row_dim, int B, int64_t max_len,
+                     int32_t groups, int32_t* sync_region, size_t logits_bytes, SyncCall& sc) {
+  if (a.page_mode || a.per_layer || groups != 1 || B > kScoreSyncMaxBatch) return false;
+  if (row_dim != 64 && row_dim != 128) return false;
+  if ((int64_t)n_heads * nq_max > 16) return false;
+  memset(&sc, 0, sizeof sc);
   // used KV heads in ascending order; columns KV head by KV head, then head slot, then query
   int nu = 0;
   for (int i = 0; i < n_heads; ++i) {
     const int g = a.heads[i] / a.group_size;
     int at = 0;
-    while (at < nu && a.sync_kv[at] < g) ++at;
-    if (at < nu && a.sync_kv[at] == g) continue;
-    if (nu == 4) return 0;
-    for (int v = nu; v > at; --v) a.sync_kv[v] = a.sync_kv[v - 1];
-    a.sync_kv[at] = g;
+    while (at < nu && sc.kv[at] < g) ++at;
+    if (at < nu && sc.kv[at] == g) continue;
+    if (nu == 4) return false;
+    for (int v = nu; v > at; --v) sc.kv[v] = sc.kv[v - 1];
+    sc.kv[at] = g;
     ++nu;
   }
-  if (nu == 0) return 0;
+  if (nu == 0) return false;
   int np = 0;
   for (int u = 0; u < nu; ++u)
     for (int i = 0; i < n_heads; ++i) {
-      if (a.heads[i] / a.group_size != a.sync_kv[u]) continue;
+      if (a.heads[i] / a.group_size != sc.kv[u]) continue;
       for (int jq = 0; jq < nq_max; ++jq) {
-        a.sync_col_slot[np] = (uint8_t)i;
-        a.sync_col_query[np] = (uint8_t)jq;
-        a.sync_col_u[np] = (uint8_t)u;
+        sc.col_head[np] = a.heads[i];
+        sc.col_query[np] = (uint8_t)jq;
+        sc.col_u[np] = (uint8_t)u;
         ++np;
       }
     }
@@ -337,24 +339,48 @@ int score_sync_plan(ScoreArgs& a, int32_t n_heads, int32_t nq_max, int row_dim, 
   // when every chunk the sizes allow gets a CU at once (beyond that, the two-pass form's
   // many small workgroups balance the load better).
   int tw = (int64_t)B * max_len >= (int64_t)192 * 2048 ? 8 : 2;
-  const int64_t chunks = (max_len + 256 * tw - 1) / (256 * tw);
-  if (chunks > kScoreSyncMaxChunks || (int64_t)B * chunks > kScoreSyncCUs) return 0;
-  // a sequence's chunks on one XCD when they fit there with the other sequences of that XCD
-  a.sync_local = (B + 7) / 8 * chunks <= kScoreSyncCUs / 8 ? 1 : 0;
-  if ((size_t)a.n_layers * B * chunks * 16 * 2 * sizeof(float) > logits_bytes) return 0;
+  int64_t chunks = (max_len + 256 * tw - 1) / (256 * tw);
+  if (chunks > kScoreSyncMaxChunks && tw == 2) {  // long sequences of a small batch
+    tw = 8;
+    chunks = (max_len + 256 * tw - 1) / (256 * tw);
+  }
+  if (chunks > kScoreSyncMaxChunks || (int64_t)B * chunks > kScoreSyncCUs) return false;
+  if ((size_t)a.n_layers * B * chunks * 16 * 2 * sizeof(float) > logits_bytes) return false;
   // every K row the kernel reads lies within 2^31 bytes of its buffer resource's base (a
   // sequence's rows, or the page pool)
   const int64_t rows_bytes = a.k.page_table
                                  ? (int64_t)(a.k.num_pages - 1) * a.k.stride_page * 2 +
                                        (int64_t)((1 << a.k.page_shift) - 1) * a.k.stride_n * 2
                                  : (a.k.capacity - 1) * a.k.stride_n * 2;
-  const int64_t extent = rows_bytes + (int64_t)a.sync_kv[nu - 1] * a.k.stride_h * 2 + (int64_t)row_dim * 2;
-  if (rows_bytes < 0 || extent > INT32_MAX) return 0;
-  a.sync_extent = (int32_t)extent;
-  a.sync_np = np;
-  a.sync_chunks = (int32_t)chunks;
-  *nu_out = nu;
-  return tw;
+  const int64_t extent = rows_bytes + (int64_t)sc.kv[nu - 1] * a.k.stride_h * 2 + (int64_t)row_dim * 2;
+  if (rows_bytes < 0 || extent > INT32_MAX) return false;
+  for (int l = 0; l < a.n_layers; ++l) {
+    sc.q_layers[l] = a.q_layers[l];
+    sc.k_layers[l] = a.k_layers[l];
+  }
+  sc.q_sb = a.q_sb;
+  sc.q_sj = a.q_sj;
+  sc.q_sh = a.q_sh;
+  sc.k = a.k;
+  sc.dims = a.dims;
+  sc.init = a.init;
+  sc.init_sb = a.init_sb;
+  sc.out = a.out;
+  sc.out_sb = a.out_sb;
+  sc.stats = a.logits;  // the per-chunk statistics go where the two-pass form's logits do
+  sc.sync = sync_region;
+  sc.scale_log2 = a.scale_log2;
+  sc.batch = B;
+  sc.n_layers = a.n_layers;
+  sc.head_dim = row_dim;
+  sc.nu = nu;
+  sc.tw = tw;
+  sc.np = np;
+  sc.chunks = (int32_t)chunks;
+  // a sequence's chunks on one XCD when they fit there with the other sequences of that XCD
+  sc.local = (B + 7) / 8 * chunks <= kScoreSyncCUs / 8 ? 1 : 0;
+  sc.extent = (int32_t)extent;
+  return true;
 }
 
 int log2_exact(int x) {
@@ -414,12 +440,22 @@ bool score_io_ok(const float* init, int64_t init_sb, int64_t init_sg, const floa
   return !init || (aligned(init, 4) && init_sb >= 0 && init_sg >= 0);
 }
 
-// Fills the output, size and workspace fields of a (heads, layers, k view, dims already
-// set) and launches both passes over `cols` rows per sequence at most.
-dustin_status score_launch(ScoreArgs& a, int n_groups, int max_group, int row_dim, int B, int32_t nq_max, int64_t cols,
-                           float scale, int32_t groups, const float* init, int64_t init_sb, int64_t init_sg,
-                           float* out, int64_t out_sb, int64_t out_sg, void* workspace, size_t workspace_bytes,
-                           void* stream) {
+// A validated score call, ready to launch: the two-pass arguments, and the single-pass
+// form's when the call takes it.
+struct ScorePrep {
+  ScoreArgs a;
+  int n_groups = 0, max_group = 0, row_dim = 0, B = 0;
+  bool empty = false;  // nothing to compute
+  bool sync = false;
+  SyncCall sc;
+};
+
+// Fills the output, size and workspace fields of P.a (heads, layers, k view, dims already
+// set) for `cols` rows per sequence at most, and plans the single-pass form.
+dustin_status score_fill(ScorePrep& P, int row_dim, int B, int32_t nq_max, int64_t cols, float scale,
+                         int32_t groups, const float* init, int64_t init_sb, int64_t init_sg, float* out,
+                         int64_t out_sb, int64_t out_sg, void* workspace, size_t workspace_bytes) {
+  ScoreArgs& a = P.a;
   const size_t rows = (size_t)a.n_layers * B * a.n_heads * nq_max;
   const size_t need_ws = score_ws_bytes(rows, (size_t)cols, (size_t)a.chunk);
   if (!workspace || workspace_bytes < need_ws || !aligned(workspace, kAlign)) return DUSTIN_ERR_WORKSPACE;
@@ -436,29 +472,38 @@ dustin_status score_launch(ScoreArgs& a, int n_groups, int max_group, int row_di
   a.ld = (int64_t)round_up((size_t)cols, 64);
   a.n_chunks = (int32_t)((cols + a.chunk - 1) / a.chunk);
   char* const base = static_cast<char*>(workspace);
-  a.sync = reinterpret_cast<int32_t*>(base);
   a.logits = reinterpret_cast<float*>(base + kScoreSyncBytes);
   const size_t logits_bytes = round_up(rows * a.ld * sizeof(float), kAlign);
   a.stats = reinterpret_cast<float*>(base + kScoreSyncBytes + logits_bytes);
-  int nu = 0;
-  const int tw = score_sync_plan(a, a.n_heads, nq_max, row_dim, B, cols, groups, logits_bytes, &nu);
+  P.row_dim = row_dim;
+  P.B = B;
+  P.sync = score_sync_plan(a, a.n_heads, nq_max, row_dim, B, cols, groups, reinterpret_cast<int32_t*>(base),
+                           logits_bytes, P.sc);
+  return DUSTIN_OK;
+}
+
+dustin_status score_run(const ScorePrep& P, void* stream) {
+  if (P.empty) return DUSTIN_OK;
   hipError_t e;
-  if (tw) {
-    a.stats = a.logits;  // the single-pass form's per-chunk statistics
-    e = launch_score_sync(a, row_dim, nu, tw, static_cast<hipStream_t>(stream));
+  if (P.sync) {
+    SyncArgs sa;
+    memset(&sa, 0, sizeof sa);
+    sa.call[0] = P.sc;
+    e = launch_score_sync(sa, static_cast<hipStream_t>(stream));
   } else {
-    e = launch_score(a, B, n_groups, max_group, row_dim, static_cast<hipStream_t>(stream));
+    e = launch_score(P.a, P.B, P.n_groups, P.max_group, P.row_dim, static_cast<hipStream_t>(stream));
   }
   return e == hipSuccess ? DUSTIN_OK : DUSTIN_ERR_LAUNCH;
 }
 
-// Eq. 5 for n_layers layers that share shapes, summed into one output.
-dustin_status run_score(int32_t n_layers, const void* const* q_layers, int64_t q_sb, int64_t q_sj,
-                        int64_t q_sh, int32_t num_q_heads, const int32_t* heads_host, int32_t n_heads,
-                        const dustin_kv* k_layers, const dustin_batch* bt, float scale, int32_t groups,
-                        const float* init, int64_t init_sb, int64_t init_sg, float* out, int64_t out_sb,
-                        int64_t out_sg, void* workspace, size_t workspace_bytes, void* stream,
-                        bool per_layer = false, int64_t out_sl = 0) {
+// Validates Eq. 5 for n_layers layers that share shapes, summed into one output (or each
+// layer into its own with per_layer), and fills P.
+dustin_status prepare_score(ScorePrep& P, int32_t n_layers, const void* const* q_layers, int64_t q_sb,
+                            int64_t q_sj, int64_t q_sh, int32_t num_q_heads, const int32_t* heads_host,
+                            int32_t n_heads, const dustin_kv* k_layers, const dustin_batch* bt, float scale,
+                            int32_t groups, const float* init, int64_t init_sb, int64_t init_sg, float* out,
+                            int64_t out_sb, int64_t out_sg, void* workspace, size_t workspace_bytes,
+                            bool per_layer = false, int64_t out_sl = 0) {
   if (!batch_ok(bt) || !q_layers || !k_layers || !out || !heads_host) return DUSTIN_ERR_INVALID_ARG;
   if (n_layers < 1 || n_layers > kScoreMaxLayers) return DUSTIN_ERR_UNSUPPORTED;
   if (!isfinite(scale)) return DUSTIN_ERR_INVALID_ARG;
@@ -484,19 +529,21 @@ dustin_status run_score(int32_t n_layers, const void* const* q_layers, int64_t q
   }
   if (!score_io_ok(init, init_sb, init_sg, out, out_sb, out_sg)) return DUSTIN_ERR_INVALID_ARG;
 
-  ScoreArgs a;
+  ScoreArgs& a = P.a;
   memset(&a, 0, sizeof a);
   a.n_heads = n_heads;
   a.group_size = num_q_heads / Hkv;
-  int n_groups = 0, max_group = 0;
   dustin_status st =
-      score_pairs(a, heads_host, n_heads, num_q_heads, a.group_size, bt->nq_max, &n_groups, &max_group);
+      score_pairs(a, heads_host, n_heads, num_q_heads, a.group_size, bt->nq_max, &P.n_groups, &P.max_group);
   if (st != DUSTIN_OK) return st;
   KvView kv;
   st = kv_of(k, k->head_dim, bt->max_len, &kv);
   if (st != DUSTIN_OK) return st;
   const int B = bt->batch;
-  if (B == 0 || bt->max_len == 0) return DUSTIN_OK;
+  if (B == 0 || bt->max_len == 0) {
+    P.empty = true;
+    return DUSTIN_OK;
+  }
   if ((int64_t)B * n_layers > 65535) return DUSTIN_ERR_UNSUPPORTED;
   for (int l = 0; l < n_layers; ++l) {
     a.q_layers[l] = static_cast<const uint16_t*>(q_layers[l]);
@@ -512,8 +559,21 @@ dustin_status run_score(int32_t n_layers, const void* const* q_layers, int64_t q
   a.per_layer = per_layer ? 1 : 0;
   a.out_sl = out_sl;
   if ((int64_t)groups * (per_layer ? n_layers : 1) > 65535) return DUSTIN_ERR_UNSUPPORTED;
-  return score_launch(a, n_groups, max_group, k->head_dim, B, bt->nq_max, bt->max_len, scale, groups, init, init_sb,
-                      init_sg, out, out_sb, out_sg, workspace, workspace_bytes, stream);
+  return score_fill(P, k->head_dim, B, bt->nq_max, bt->max_len, scale, groups, init, init_sb, init_sg, out, out_sb,
+                    out_sg, workspace, workspace_bytes);
+}
+
+dustin_status run_score(int32_t n_layers, const void* const* q_layers, int64_t q_sb, int64_t q_sj,
+                        int64_t q_sh, int32_t num_q_heads, const int32_t* heads_host, int32_t n_heads,
+                        const dustin_kv* k_layers, const dustin_batch* bt, float scale, int32_t groups,
+                        const float* init, int64_t init_sb, int64_t init_sg, float* out, int64_t out_sb,
+                        int64_t out_sg, void* workspace, size_t workspace_bytes, void* stream,
+                        bool per_layer = false, int64_t out_sl = 0) {
+  ScorePrep P;
+  const dustin_status st =
+      prepare_score(P, n_layers, q_layers, q_sb, q_sj, q_sh, num_q_heads, heads_host, n_heads, k_layers, bt, scale,
+                    groups, init, init_sb, init_sg, out, out_sb, out_sg, workspace, workspace_bytes, per_layer, out_sl);
+  return st != DUSTIN_OK ? st : score_run(P, stream);
 }
 
 }  // namespace
@@ -556,6 +616,34 @@ dustin_status dustin_score_per_layer(int32_t n_layers, const void* const* q_laye
   return run_score(n_layers, q_layers_host, q_sb, q_sj, q_sh, num_q_heads, heads_host, n_heads, k_layers_host,
                    bt, scale, groups, nullptr, 0, 0, out, out_sb, out_sg, workspace, workspace_bytes, stream,
                    true, out_sl);
+}
+
+dustin_status dustin_score_calls(int32_t n_calls, const dustin_score_call* calls, void* stream) {
+  if (n_calls < 1 || n_calls > 2 || !calls) return DUSTIN_ERR_INVALID_ARG;
+  ScorePrep P[2];
+  for (int i = 0; i < n_calls; ++i) {
+    const dustin_score_call& c = calls[i];
+    const dustin_status st =
+        prepare_score(P[i], c.n_layers, c.q_layers_host, c.q_sb, c.q_sj, c.q_sh, c.num_q_heads, c.heads_host,
+                      c.n_heads, c.k_layers_host, c.bt, c.scale, c.groups, c.init, c.init_sb, c.init_sg, c.out,
+                      c.out_sb, c.out_sg, c.workspace, c.workspace_bytes);
+    if (st != DUSTIN_OK) return st;
+  }
+  if (n_calls == 2 && calls[0].workspace == calls[1].workspace) return DUSTIN_ERR_WORKSPACE;
+  if (n_calls == 2 && P[0].sync && P[1].sync && !P[0].empty && !P[1].empty &&
+      score_sync_pair_supported(P[0].sc, P[1].sc)) {
+    SyncArgs sa;
+    memset(&sa, 0, sizeof sa);
+    sa.call[0] = P[0].sc;
+    sa.call[1] = P[1].sc;
+    return launch_score_sync_pair(sa, static_cast<hipStream_t>(stream)) == hipSuccess ? DUSTIN_OK
+                                                                                      : DUSTIN_ERR_LAUNCH;
+  }
+  for (int i = 0; i < n_calls; ++i) {
+    const dustin_status st = score_run(P[i], stream);
+    if (st != DUSTIN_OK) return st;
+  }
+  return DUSTIN_OK;
 }
 
 // ------------------------------------------------------------------ page estimator
@@ -643,7 +731,8 @@ dustin_status dustin_page_score(const void* q, int64_t q_sb, int64_t q_sj, int64
   if (!rows_aligned(q, q_sb, q_sj, q_sh)) return DUSTIN_ERR_INVALID_ARG;
   if (!score_io_ok(init, init_sb, init_sg, out, out_sb, out_sg)) return DUSTIN_ERR_INVALID_ARG;
   const int32_t P = pages_of(bt->max_len, page_size);
-  ScoreArgs a;
+  ScorePrep sp;
+  ScoreArgs& a = sp.a;
   memset(&a, 0, sizeof a);
   dustin_status st = meta_view(meta, meta_sb, meta_sp, meta_pages, num_kv_heads, head_dim, P, &a.k);
   if (st != DUSTIN_OK) return st;
@@ -665,8 +754,11 @@ dustin_status dustin_page_score(const void* q, int64_t q_sb, int64_t q_sj, int64
   a.page_mode = 1;
   a.page_shift = log2_exact(page_size);
   a.chunk = kScorePageChunk;
-  return score_launch(a, n_groups, max_group, 2 * head_dim, B, bt->nq_max, P, scale, groups, init, init_sb, init_sg, out,
-                      out_sb, out_sg, workspace, workspace_bytes, stream);
+  sp.n_groups = n_groups;
+  sp.max_group = max_group;
+  st = score_fill(sp, 2 * head_dim, B, bt->nq_max, P, scale, groups, init, init_sb, init_sg, out, out_sb, out_sg,
+                  workspace, workspace_bytes);
+  return st != DUSTIN_OK ? st : score_run(sp, stream);
 }
 
 // ------------------------------------------------------------------ attention recovery rate

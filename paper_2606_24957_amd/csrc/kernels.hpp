@@ -97,22 +97,47 @@ struct ScoreArgs {
   float* stats;   // [n_layers, B, n_heads, nq_max, n_chunks, 2]  (max, sum of exp2) per chunk
   int64_t ld;
   int32_t nq_max, n_chunks;
-  // single-pass form: columns 0 .. sync_np - 1 are (head slot, query) pairs on used KV head
-  // sync_col_u (KV head sync_kv[u]); sync_chunks chunks of positions per sequence
-  int32_t* sync;
-  int32_t sync_np, sync_chunks;
-  int32_t sync_local;   // 1: a sequence's chunks are consecutive among one XCD's block ids
-  int32_t sync_extent;  // bytes of K rows one buffer resource covers (a sequence, or the page pool)
-  int32_t sync_kv[4];
-  uint8_t sync_col_slot[16], sync_col_query[16], sync_col_u[16];
 };
 static_assert(sizeof(ScoreArgs) <= 4096, "kernel arguments stay within 4 KiB");
 
 // n_groups pass-1 workgroups along x (tile_first / tile_count), max_group the largest
 // tile count; row_dim: length of a K row (head_dim, or 2 * head_dim for page statistics)
 hipError_t launch_score(const ScoreArgs& a, int B, int n_groups, int max_group, int row_dim, hipStream_t stream);
-// the single-pass form: nu used KV heads (1..4), tw tiles of 16 positions per wave (2 or 8)
-hipError_t launch_score_sync(const ScoreArgs& a, int head_dim, int nu, int tw, hipStream_t stream);
+
+// One call of the single-pass form (score_sync.hip): columns 0 .. np - 1 are (query head
+// col_head, query col_query) pairs on used KV head kv[col_u]; chunks of 256 tw positions,
+// `chunks` per sequence, a sequence's chunks on one XCD when `local`.
+struct SyncCall {
+  const uint16_t* q_layers[kScoreMaxLayers];
+  const uint16_t* k_layers[kScoreMaxLayers];
+  int64_t q_sb, q_sj, q_sh;
+  KvView k;
+  SeqDims dims;
+  const float* init;
+  int64_t init_sb;
+  float* out;
+  int64_t out_sb;
+  float* stats;   // [n_layers, batch, chunks, 16] (max, sum of exp2) per chunk and column
+  int32_t* sync;  // the workspace's counter region (zero between calls) and timeout flag
+  float scale_log2;
+  int32_t batch, n_layers, head_dim, nu, tw, np, chunks, local;
+  int32_t extent;  // bytes of K rows one buffer resource covers (a sequence, or the page pool)
+  int32_t kv[4];
+  int32_t col_head[16];
+  uint8_t col_query[16], col_u[16];
+};
+
+struct SyncArgs {
+  SyncCall call[2];
+  int32_t blocks0;  // blocks of call 0 (set by the launcher)
+};
+static_assert(sizeof(SyncArgs) <= 4096, "kernel arguments stay within 4 KiB");
+
+// the single-pass form of one call; and of two calls in one launch, for the pairs of
+// shapes score_sync_pair_supported accepts
+hipError_t launch_score_sync(const SyncArgs& a, hipStream_t stream);
+bool score_sync_pair_supported(const SyncCall& c0, const SyncCall& c1);
+hipError_t launch_score_sync_pair(const SyncArgs& a, hipStream_t stream);
 
 // ---- attention recovery rate (arr.hip) ----
 struct ArrArgs {

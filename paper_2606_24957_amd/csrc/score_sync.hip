@@ -24,6 +24,8 @@
 //     workspace and goes on.
 //   * The next layer's first K rows and its queries are in flight across the wait.
 //   * The last chunk of a sequence to leave returns the sequence's counters to zero.
+#include <type_traits>
+
 #include "kernels.hpp"
 
 namespace dustin {
@@ -53,8 +55,22 @@ __device__ __forceinline__ void store_pair_sc1(float2* p, float m, float s) {
 
 }  // namespace
 
+// LDS of a single-pass workgroup: the chunk's logits column by column, a pitch of C + 4
+// staggering the columns over the banks (only the pairs' columns are written), and the
+// paged rows' physical pages.
+constexpr int kSyncMaxTW = 8;
+constexpr int kSyncXPitch = kSyncWaves * kSyncMaxTW * 16 + 4;
+struct SyncLds {
+  float x[16 * kSyncXPitch];
+  int page[kSyncWaves * kSyncMaxTW * 16];
+  float2 st[kSyncWaves][16];
+  float2 mz[16];
+};
+
+// One call's share of the grid: block blk of the call's blocks.
 template <int D, int NU, int TW, bool kPaged>
-__global__ __launch_bounds__(kSyncThreads) void score_sync_kernel(ScoreArgs a) {
+__device__ __forceinline__ void score_sync_call(const SyncCall& a, int blk, SyncLds& lds) {
+  const SeqDims& dims = a.dims;
   constexpr int KS = D / 32;                 // MFMA k-steps of one KV head's row
   constexpr int HPS = 4 / KS;                // KV heads per load stage (64 bytes per lane)
   constexpr int SPT = (NU + HPS - 1) / HPS;  // load stages per tile
@@ -67,35 +83,35 @@ __global__ __launch_bounds__(kSyncThreads) void score_sync_kernel(ScoreArgs a) {
   // when every sequence's chunks fit one XCD, consecutive among the ids of one XCD
   // (workgroups go to the XCDs round-robin by id): the chunks then share its L2 and pace
   int b, c;
-  if (a.sync_local) {
-    const int x = blockIdx.x & 7, k = blockIdx.x >> 3;
-    b = k / a.sync_chunks * 8 + x;
-    c = k % a.sync_chunks;
-    if (b >= a.batch) return;
+  if (a.local) {
+    const int x = blk & 7, k = blk >> 3;
+    b = k / a.chunks * 8 + x;
+    c = k % a.chunks;
   } else {
-    b = blockIdx.x / a.sync_chunks;
-    c = blockIdx.x - b * a.sync_chunks;
+    b = blk / a.chunks;
+    c = blk - b * a.chunks;
   }
-  const int N = a.dims.len(b);
+  if (b >= a.batch) return;
+  const int N = dims.len(b);
   const int G = (N + C - 1) / C;  // chunks of this sequence
   if (c >= G) return;
-  const int nq = a.dims.nq(b);
+  const int nq = dims.nq(b);
   const int L = a.n_layers;
 
   // column lr: (scoring head slot, query) on used KV head cu; columns past the pairs, and
   // queries past nq_b, count for nothing
-  const int col = lr < a.sync_np ? lr : 0;
-  const bool col_ok = lr < a.sync_np && (int)a.sync_col_query[col] < nq;
-  const int cu = a.sync_col_u[col];
-  const int64_t q_off = (int64_t)b * a.q_sb + (int64_t)a.sync_col_query[col] * a.q_sj +
-                        (int64_t)a.heads[a.sync_col_slot[col]] * a.q_sh + 8 * lg;
+  const int col = lr < a.np ? lr : 0;
+  const bool col_ok = lr < a.np && (int)a.col_query[col] < nq;
+  const int cu = a.col_u[col];
+  const int64_t q_off = (int64_t)b * a.q_sb + (int64_t)a.col_query[col] * a.q_sj +
+                        (int64_t)a.col_head[col] * a.q_sh + 8 * lg;
   const int p0 = c * C + wave * (TW * 16);  // this wave's first position
 
   // K rows through a buffer resource per layer (32-bit byte offsets, checked on the host):
   // this lane's row of tile t (clamped to the last position) and the stage's KV heads
   // (paged: the physical page of every row the wave reads, looked up once, kept in LDS so
   // that a stage's loads wait for no global load)
-  __shared__ int sm_page[kPaged ? kSyncWaves * TW * 16 : 1];
+  int* const sm_page = lds.page;
   if constexpr (kPaged) {
     if (lg == 0) {
 #pragma unroll
@@ -118,7 +134,7 @@ __global__ __launch_bounds__(kSyncThreads) void score_sync_kernel(ScoreArgs a) {
   };
   auto rsrc = [&](int l) {
     const uint16_t* base = a.k_layers[l] + (kPaged ? 0 : (int64_t)b * a.k.stride_b);
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(base), 0, a.sync_extent, 0x00020000);
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(base), 0, a.extent, 0x00020000);
   };
   // stage s of tile t: KV heads s HPS .. s HPS + HPS - 1, in the MFMA A layout (row lr,
   // elements 32 kk + 8 lg .. + 7)
@@ -131,7 +147,7 @@ __global__ __launch_bounds__(kSyncThreads) void score_sync_kernel(ScoreArgs a) {
 #pragma unroll
         for (int kk = 0; kk < KS; ++kk)
           dst[h * KS + kk] = __builtin_bit_cast(
-              u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, off, (int)((uint32_t)a.sync_kv[u] * sh + 64u * kk), 0));
+              u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, off, (int)((uint32_t)a.kv[u] * sh + 64u * kk), 0));
       }
     }
   };
@@ -150,16 +166,14 @@ __global__ __launch_bounds__(kSyncThreads) void score_sync_kernel(ScoreArgs a) {
   // loaded after it.
   constexpr bool kQNext = D == 64;
 
-  // The logits of the chunk, column by column, in LDS (a column's positions contiguous;
-  // the pitch staggers the columns over the banks).  Only the pairs' columns are stored.
-  constexpr int kXPitch = C + 4;
-  __shared__ __attribute__((aligned(16))) float sm_x[16 * kXPitch];
-  __shared__ float2 sm_st[kSyncWaves][16];
-  __shared__ float2 sm_mz[16];
+  constexpr int kXPitch = kSyncXPitch;
+  float* const sm_x = lds.x;
+  auto& sm_st = lds.st;
+  auto& sm_mz = lds.mz;
   int* const cnt = a.sync + b;
   int* const done = a.sync + kScoreSyncMaxBatch + b;
   int* const flag = a.sync + 2 * kScoreSyncMaxBatch;
-  const int np = a.sync_np;
+  const int np = a.np;
 
   // A ring of NB load stages: stage qi's buffer is reloaded with stage qi + NB - 1 (of this
   // layer, or of the next one) as soon as qi is consumed, so NB - 1 stages are in flight
@@ -233,7 +247,7 @@ __global__ __launch_bounds__(kSyncThreads) void score_sync_kernel(ScoreArgs a) {
     // Wave 0 alone publishes, waits and merges; the other waves' next loads stay in flight
     // (a wait for this wave's write-through stores is a wait for all its loads as well).
     if (wave == 0) {
-      float2* const stats_l = reinterpret_cast<float2*>(a.stats) + ((int64_t)l * a.batch + b) * a.sync_chunks * 16;
+      float2* const stats_l = reinterpret_cast<float2*>(a.stats) + ((int64_t)l * a.batch + b) * a.chunks * 16;
       if (lane < 16) {  // the workgroup's summary, merged over the waves in order
         float M = -INFINITY, S = 0.f;
 #pragma unroll
@@ -279,7 +293,7 @@ __global__ __launch_bounds__(kSyncThreads) void score_sync_kernel(ScoreArgs a) {
     if ((int)threadIdx.x < C / 4) {
       f32x4 y = {0.f, 0.f, 0.f, 0.f};
       for (int j = 0; j < np; ++j) {
-        if ((int)a.sync_col_query[j] >= nq) continue;  // uniform
+        if ((int)a.col_query[j] >= nq) continue;  // uniform
         const f32x4 xv = *reinterpret_cast<const f32x4*>(sm_x + j * kXPitch + 4 * threadIdx.x);
         const float2 mz = sm_mz[j];
 #pragma unroll
@@ -319,33 +333,86 @@ __global__ __launch_bounds__(kSyncThreads) void score_sync_kernel(ScoreArgs a) {
   }
 }
 
-template <int D, int NU, bool kPaged>
-static hipError_t launch_sync_tw(const ScoreArgs& a, int tw, dim3 grid, hipStream_t stream) {
-  if (tw == 8) hipLaunchKernelGGL((score_sync_kernel<D, NU, 8, kPaged>), grid, dim3(kSyncThreads), 0, stream, a);
-  else if (tw == 2) hipLaunchKernelGGL((score_sync_kernel<D, NU, 2, kPaged>), grid, dim3(kSyncThreads), 0, stream, a);
-  else return hipErrorInvalidValue;
+// Shapes of the single-pass form: row length, used KV heads, tiles per wave, paged.
+template <int D_, int NU_, int TW_, bool P_>
+struct SyncShape {
+  static constexpr int D = D_, NU = NU_, TW = TW_;
+  static constexpr bool kPaged = P_;
+};
+struct NoShape {};
+
+// One launch runs one call, or two (the first call's blocks, a multiple of 8, then the
+// second's: workgroups of the second start as the first's leave their CUs).
+template <class S0, class S1>
+__global__ __launch_bounds__(kSyncThreads) void score_sync_kernel(SyncArgs a) {
+  __shared__ __attribute__((aligned(16))) SyncLds lds;
+  if constexpr (std::is_same<S1, NoShape>::value) {
+    score_sync_call<S0::D, S0::NU, S0::TW, S0::kPaged>(a.call[0], blockIdx.x, lds);
+  } else {
+    if ((int)blockIdx.x < a.blocks0)
+      score_sync_call<S0::D, S0::NU, S0::TW, S0::kPaged>(a.call[0], blockIdx.x, lds);
+    else
+      score_sync_call<S1::D, S1::NU, S1::TW, S1::kPaged>(a.call[1], blockIdx.x - a.blocks0, lds);
+  }
+}
+
+// blocks of one call: a multiple of 8 (sequences of an XCD, or all sequences, times chunks)
+static int sync_blocks(const SyncCall& c) {
+  const int seqs = c.local ? (c.batch + 7) / 8 * 8 : c.batch;
+  return (seqs * c.chunks + 7) / 8 * 8;
+}
+
+template <class S0, class S1>
+static hipError_t launch_sync(SyncArgs a, hipStream_t stream) {
+  a.blocks0 = sync_blocks(a.call[0]);
+  const int blocks = a.blocks0 + (std::is_same<S1, NoShape>::value ? 0 : sync_blocks(a.call[1]));
+  hipLaunchKernelGGL((score_sync_kernel<S0, S1>), dim3(blocks), dim3(kSyncThreads), 0, stream, a);
   return hipGetLastError();
 }
 
+template <int D, int NU, bool kPaged>
+static hipError_t launch_sync_tw(const SyncArgs& a, int tw, hipStream_t stream) {
+  if (tw == 8) return launch_sync<SyncShape<D, NU, 8, kPaged>, NoShape>(a, stream);
+  if (tw == 2) return launch_sync<SyncShape<D, NU, 2, kPaged>, NoShape>(a, stream);
+  return hipErrorInvalidValue;
+}
+
 template <int D, bool kPaged>
-static hipError_t launch_sync_nu(const ScoreArgs& a, int nu, int tw, dim3 grid, hipStream_t stream) {
+static hipError_t launch_sync_nu(const SyncArgs& a, int nu, int tw, hipStream_t stream) {
   switch (nu) {
-    case 1: return launch_sync_tw<D, 1, kPaged>(a, tw, grid, stream);
-    case 2: return launch_sync_tw<D, 2, kPaged>(a, tw, grid, stream);
-    case 3: return launch_sync_tw<D, 3, kPaged>(a, tw, grid, stream);
-    case 4: return launch_sync_tw<D, 4, kPaged>(a, tw, grid, stream);
+    case 1: return launch_sync_tw<D, 1, kPaged>(a, tw, stream);
+    case 2: return launch_sync_tw<D, 2, kPaged>(a, tw, stream);
+    case 3: return launch_sync_tw<D, 3, kPaged>(a, tw, stream);
+    case 4: return launch_sync_tw<D, 4, kPaged>(a, tw, stream);
     default: return hipErrorInvalidValue;
   }
 }
 
-hipError_t launch_score_sync(const ScoreArgs& a, int head_dim, int nu, int tw, hipStream_t stream) {
-  const dim3 grid((unsigned)((a.sync_local ? (a.batch + 7) / 8 * 8 : a.batch) * a.sync_chunks));
-  const bool paged = a.k.page_table != nullptr;
-  if (head_dim == 128)
-    return paged ? launch_sync_nu<128, true>(a, nu, tw, grid, stream) : launch_sync_nu<128, false>(a, nu, tw, grid, stream);
-  if (head_dim == 64)
-    return paged ? launch_sync_nu<64, true>(a, nu, tw, grid, stream) : launch_sync_nu<64, false>(a, nu, tw, grid, stream);
+hipError_t launch_score_sync(const SyncArgs& a, hipStream_t stream) {
+  const SyncCall& c = a.call[0];
+  const bool paged = c.k.page_table != nullptr;
+  if (c.head_dim == 128)
+    return paged ? launch_sync_nu<128, true>(a, c.nu, c.tw, stream) : launch_sync_nu<128, false>(a, c.nu, c.tw, stream);
+  if (c.head_dim == 64)
+    return paged ? launch_sync_nu<64, true>(a, c.nu, c.tw, stream) : launch_sync_nu<64, false>(a, c.nu, c.tw, stream);
   return hipErrorInvalidValue;
+}
+
+// Two calls in one launch: the pairs of shapes compiled for it (a target call with four
+// KV heads of 128-element rows, then a draft call with two KV heads of 64-element rows, as
+// one verification step scores them); false when the two calls have another pair.
+bool score_sync_pair_supported(const SyncCall& c0, const SyncCall& c1) {
+  return c0.head_dim == 128 && c0.nu == 4 && c1.head_dim == 64 && c1.nu == 2 && c0.tw == c1.tw &&
+         (c0.tw == 8 || c0.tw == 2) && (c0.k.page_table != nullptr) == (c1.k.page_table != nullptr);
+}
+
+hipError_t launch_score_sync_pair(const SyncArgs& a, hipStream_t stream) {
+  const bool paged = a.call[0].k.page_table != nullptr;
+  if (a.call[0].tw == 8)
+    return paged ? launch_sync<SyncShape<128, 4, 8, true>, SyncShape<64, 2, 8, true>>(a, stream)
+                 : launch_sync<SyncShape<128, 4, 8, false>, SyncShape<64, 2, 8, false>>(a, stream);
+  return paged ? launch_sync<SyncShape<128, 4, 2, true>, SyncShape<64, 2, 2, true>>(a, stream)
+               : launch_sync<SyncShape<128, 4, 2, false>, SyncShape<64, 2, 2, false>>(a, stream);
 }
 
 }  // namespace dustin

@@ -9,7 +9,7 @@ from typing import List, Optional
 
 import torch
 
-from . import (plan_kv_append, plan_kv_commit, plan_score, plan_score_layers, plan_score_per_layer,
+from . import (plan_kv_append, plan_kv_commit, plan_score, plan_score_calls, plan_score_layers, plan_score_per_layer,
                plan_sparse_verify_attn, plan_topk)
 
 
@@ -52,15 +52,17 @@ class VerifyStep:
         init = est.init_target
         if init is not None and s.groups > 1:  # one historical row, the same for every group
             init = init.expand(s.B, s.groups, N)
-        ops = [plan_score(est.q_target, self.layers[0].k, self.seq, s.target_heads, groups=s.groups,
-                          init=init, out=self.s_t, max_len=N, page_table=self.layers[0].page_table,
-                          stream=stream)]
+        target = plan_score(est.q_target, self.layers[0].k, self.seq, s.target_heads, groups=s.groups,
+                            init=init, out=self.s_t, max_len=N, page_table=self.layers[0].page_table,
+                            stream=stream)
         if est.s_draft_given is not None:
             given = est.s_draft_given
-            ops.append(lambda: self.s_d.copy_(given))
+            ops = [target, lambda: self.s_d.copy_(given)]
         else:
-            ops.append(plan_score_layers(est.draft_q, est.draft_k, self.seq, s.draft.heads,
-                                         n_query=self.gam, out=self.s_d, max_len=N, stream=stream))
+            # the target's and the draft's scores in one call (one launch where the library can)
+            draft = plan_score_layers(est.draft_q, est.draft_k, self.seq, s.draft.heads, n_query=self.gam,
+                                      out=self.s_d, max_len=N, stream=stream, ws_tag="score_draft")
+            ops = [plan_score_calls([target, draft], stream=stream)]
         ops.append(plan_topk(self.s_d, self.s_t, self.seq, s.k_max, budget=self.bud, m=self.mm,
                              n_sink=s.n_sink, n_window=s.n_window, groups=s.groups, idx=self.idx,
                              count=self.cnt, stream=stream))

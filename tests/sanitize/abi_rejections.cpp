@@ -15,7 +15,9 @@
 namespace dustin {
 hipError_t launch_verify_attn(const AttnArgs&, int, bool, bool, hipStream_t) { return hipErrorInvalidValue; }
 hipError_t launch_score(const ScoreArgs&, int, int, int, int, hipStream_t) { return hipErrorInvalidValue; }
-hipError_t launch_score_sync(const ScoreArgs&, int, int, int, hipStream_t) { return hipErrorInvalidValue; }
+hipError_t launch_score_sync(const SyncArgs&, hipStream_t) { return hipErrorInvalidValue; }
+bool score_sync_pair_supported(const SyncCall&, const SyncCall&) { return false; }
+hipError_t launch_score_sync_pair(const SyncArgs&, hipStream_t) { return hipErrorInvalidValue; }
 hipError_t launch_arr(const ArrArgs&, int, hipStream_t) { return hipErrorInvalidValue; }
 hipError_t launch_page_meta(const PageMetaArgs&, int, int, hipStream_t) { return hipErrorInvalidValue; }
 hipError_t launch_topk(const TopkArgs&, int, hipStream_t) { return hipErrorInvalidValue; }
@@ -196,6 +198,35 @@ int main() {
     EXPECT(dustin_score_layers(2, qs, 800 * 8 * 128, 8 * 128, 128, 8, h_ok, 2, ks, &bt, 0.1f, 1, nullptr, 0, 0,
                                static_cast<float*>(FAKE), 0, 0, FAKE, (size_t)1 << 30, nullptr),
            DUSTIN_ERR_LAUNCH);
+    // one or two calls in one launch
+    dustin_score_call c[3];
+    memset(c, 0, sizeof c);
+    for (int i = 0; i < 3; ++i) {
+      c[i].n_layers = 2;
+      c[i].q_layers_host = qs;
+      c[i].q_sb = 800 * 8 * 128;
+      c[i].q_sj = 8 * 128;
+      c[i].q_sh = 128;
+      c[i].num_q_heads = 8;
+      c[i].heads_host = h_ok;
+      c[i].n_heads = 2;
+      c[i].k_layers_host = ks;
+      c[i].bt = &bt;
+      c[i].scale = 0.1f;
+      c[i].groups = 1;
+      c[i].out = static_cast<float*>(FAKE);
+      c[i].workspace = fake((size_t)i << 30);
+      c[i].workspace_bytes = (size_t)1 << 30;
+    }
+    EXPECT(dustin_score_calls(0, c, nullptr), DUSTIN_ERR_INVALID_ARG);
+    EXPECT(dustin_score_calls(3, c, nullptr), DUSTIN_ERR_INVALID_ARG);
+    EXPECT(dustin_score_calls(1, nullptr, nullptr), DUSTIN_ERR_INVALID_ARG);
+    EXPECT(dustin_score_calls(2, c, nullptr), DUSTIN_ERR_LAUNCH);  // valid: reaches the (stubbed) launch
+    c[1].workspace = c[0].workspace;
+    EXPECT(dustin_score_calls(2, c, nullptr), DUSTIN_ERR_WORKSPACE);
+    c[1].workspace = fake((size_t)1 << 30);
+    c[1].heads_host = h_dup;
+    EXPECT(dustin_score_calls(2, c, nullptr), DUSTIN_ERR_INVALID_ARG);
   }
 
   // ---- page estimator

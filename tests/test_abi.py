@@ -175,6 +175,38 @@ def test_score_rejects(L):
     assert _score(L, ws_bytes=16) == D.ERR_WORKSPACE
 
 
+def _score_call(keep, heads=(0, 2), Hq=8, kv=None, bt=None, ws=FAKE, ws_bytes=1 << 30, out=FAKE):
+    """A dustin_score_call descriptor; keep holds the ctypes objects it points at."""
+    kv = kv or _kv(Hkv=4)
+    bt = bt or _batch(nq=1)
+    hd = (ctypes.c_int32 * max(len(heads), 1))(*heads)
+    qh = (ctypes.c_void_p * 1)(FAKE)
+    keep += [kv, bt, hd, qh]
+    c = D.DustinScoreCall()
+    c.n_layers, c.q_layers_host, c.q_sb, c.q_sj, c.q_sh = 1, ctypes.addressof(qh), 8 * 128, 8 * 128, 128
+    c.num_q_heads, c.heads_host, c.n_heads = Hq, ctypes.addressof(hd), len(heads)
+    c.k_layers_host, c.bt, c.scale, c.groups = ctypes.addressof(kv), ctypes.addressof(bt), 0.1, 1
+    c.out, c.workspace, c.workspace_bytes = out, ws, ws_bytes
+    return c
+
+
+def test_score_calls_rejects(L):
+    keep = []
+    one = _score_call(keep)
+    arr = (D.DustinScoreCall * 3)(one, _score_call(keep, ws=FAKE + 0x40000000), one)
+    assert L.dustin_score_calls(0, arr, None) == D.ERR_INVALID_ARG
+    assert L.dustin_score_calls(3, arr, None) == D.ERR_INVALID_ARG
+    assert L.dustin_score_calls(1, None, None) == D.ERR_INVALID_ARG
+    shared = (D.DustinScoreCall * 2)(one, one)
+    assert L.dustin_score_calls(2, shared, None) == D.ERR_WORKSPACE    # one workspace for two calls
+    bad = (D.DustinScoreCall * 2)(one, _score_call(keep, heads=(0, 8), ws=FAKE + 0x40000000))
+    assert L.dustin_score_calls(2, bad, None) == D.ERR_INVALID_ARG     # the second call's head
+    bad = (D.DustinScoreCall * 2)(_score_call(keep, out=None), one)
+    assert L.dustin_score_calls(2, bad, None) == D.ERR_INVALID_ARG
+    small = (D.DustinScoreCall * 1)(_score_call(keep, ws_bytes=16))
+    assert L.dustin_score_calls(1, small, None) == D.ERR_WORKSPACE
+
+
 def test_product_never_touches_the_oracle():
     """The HIP path has no CPU fallback and never imports the checker."""
     pkg = os.path.join(ROOT, "paper_2606_24957_amd")

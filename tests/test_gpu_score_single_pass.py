@@ -128,18 +128,90 @@ def test_single_pass_is_deterministic_and_reusable():
 
 
 def test_single_pass_many_chunks_per_sequence():
-    """More workgroups than the GPU holds at once (later sequences wait for CUs that earlier
-    ones free) and sequences of many chunks: B = 8 of N = 131072 with the draft's shape."""
-    B, N, d, heads = 8, 131072, 64, [0, 4, 7, 11]
+    """Sequences of many chunks, spread over every XCD (64 chunks of 2048 positions do not
+    fit one): B = 2 of N = 131072 with the draft's shape."""
+    B, N, d, heads = 2, 131072, 64, [0, 4, 7, 11]
     g = torch.Generator(device=DEV).manual_seed(60)
     q = torch.randn((B, 4, 14, d), generator=g, device=DEV).to(torch.bfloat16)
     k = torch.randn((B, N, 2, d), generator=g, device=DEV).to(torch.bfloat16)
-    lens = [N, N - 1, 100000, 65537, 2049, 1, 0, 77777]
+    lens = [N, 77777]
     seq = torch.tensor(lens, dtype=torch.int32, device=DEV)
     out = D.score(q, k, seq, heads, max_len=N)
     torch.cuda.synchronize()
     _sync_region_clear()
-    for b in (0, 3, 5, 7):
+    for b in (0, 1):
         n = lens[b]
         ref = O.score(bits(q[b:b + 1]), bits(k[b:b + 1]), [n], [4], heads, scale_of(d), num_kv_heads=2)
         check_score(host(out)[b, 0, :n], ref[0, 0, :n], n, f"b={b}")
+
+
+def _step_scores(B, N, lens, gamma, page_size=0, seed=70):
+    """A target call (last token, heads {0, 17, 34, 51} over 8 KV heads of 128) and a draft
+    call (Gamma queries, heads {0, 4, 7, 11} over 2 KV heads of 64, three layers)."""
+    g = torch.Generator(device=DEV).manual_seed(seed)
+    qt = torch.randn((B, 1, 64, 128), generator=g, device=DEV).to(torch.bfloat16)
+    kt = torch.randn((B, N, 8, 128), generator=g, device=DEV).to(torch.bfloat16)
+    qd = [torch.randn((B, gamma, 14, 64), generator=g, device=DEV).to(torch.bfloat16) for _ in range(3)]
+    kd = [torch.randn((B, N, 2, 64), generator=g, device=DEV).to(torch.bfloat16) for _ in range(3)]
+    init = torch.rand((B, 1, N), generator=g, device=DEV) / N
+    pt = None
+    if page_size:
+        kt, pt = _paged(kt, page_size, seed)
+        kd = [_paged(k, page_size, seed)[0] for k in kd]
+    seq = torch.tensor(lens, dtype=torch.int32, device=DEV)
+    nq = torch.tensor([max(1, gamma - b % 2) for b in range(B)], dtype=torch.int32, device=DEV)
+    st, sd = torch.full((B, 1, N), -5.0, device=DEV), torch.full((B, 1, N), -5.0, device=DEV)
+    pt_ = D.plan_score(qt, kt, seq, [0, 17, 34, 51], init=init, out=st, max_len=N, page_table=pt)
+    pd_ = D.plan_score_layers(qd, kd, seq, [0, 4, 7, 11], n_query=nq, out=sd, max_len=N, page_table=pt,
+                              ws_tag="score_draft")
+    return pt_, pd_, st, sd
+
+
+@pytest.mark.parametrize("B,N,page_size", [(16, 32768, 0), (16, 32768, 16), (5, 3000, 0), (5, 3000, 4)])
+def test_two_calls_in_one_launch_equal_the_separate_calls(B, N, page_size):
+    """dustin_score_calls with the target's and the draft's calls of a step: the outputs have
+    the bits of the two calls made one after the other (one launch at the full shape, where
+    both take the single-pass form with eight tiles per wave; two tiles per wave below)."""
+    lens = [N - 37 * b for b in range(B)]
+    pt_, pd_, st, sd = _step_scores(B, N, lens, 4, page_size)
+    pt_()
+    pd_()
+    torch.cuda.synchronize()
+    ref_t, ref_d = st.clone(), sd.clone()
+    st.fill_(-5.0)
+    sd.fill_(-5.0)
+    both = D.plan_score_calls([pt_, pd_])
+    for _ in range(2):  # twice in a row: the counters return to zero
+        both()
+    torch.cuda.synchronize()
+    assert torch.equal(st, ref_t) and torch.equal(sd, ref_d)
+    for tag in ("score", "score_draft"):
+        reg = D.score_sync_region(tag=tag)
+        assert int(reg.count_nonzero()) == 0
+    if not page_size:  # and the target against the oracle for the last sequence
+        b, n = B - 1, lens[-1]
+        q, k, init = pt_._keep[0], pt_._keep[1], pt_._keep[2]
+        ref = O.score(bits(q[b:b + 1]), bits(k[b:b + 1]), [n], [1], [0, 17, 34, 51], scale_of(128),
+                      num_kv_heads=8, init=host(init)[b:b + 1])
+        check_score(host(st)[b, 0, :n], ref[0, 0, :n], n, f"target b={b}")
+
+
+def test_two_calls_fall_back_to_one_after_the_other():
+    """A pair of shapes the fused launch does not cover (a draft call of three KV heads)
+    still gives the separate calls' bits."""
+    B, N = 3, 2500
+    g = torch.Generator(device=DEV).manual_seed(80)
+    qt = torch.randn((B, 1, 64, 128), generator=g, device=DEV).to(torch.bfloat16)
+    kt = torch.randn((B, N, 8, 128), generator=g, device=DEV).to(torch.bfloat16)
+    qd = torch.randn((B, 2, 16, 64), generator=g, device=DEV).to(torch.bfloat16)
+    kd = torch.randn((B, N, 4, 64), generator=g, device=DEV).to(torch.bfloat16)
+    seq = torch.tensor([N, 1000, 1], dtype=torch.int32, device=DEV)
+    a = D.plan_score(qt, kt, seq, [0, 17, 34, 51], max_len=N)
+    b_ = D.plan_score(qd, kd, seq, [0, 5, 10], max_len=N, ws_tag="score_draft")
+    a()
+    b_()
+    torch.cuda.synchronize()
+    ra, rb = a.result.clone(), b_.result.clone()
+    D.plan_score_calls([a, b_])()
+    torch.cuda.synchronize()
+    assert torch.equal(a.result[0, 0, :N], ra[0, 0, :N]) and torch.equal(b_.result[1, 0, :1000], rb[1, 0, :1000])
