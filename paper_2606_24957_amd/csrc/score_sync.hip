@@ -194,8 +194,7 @@ __device__ __forceinline__ void score_sync_call(const SyncCall& a, int blk, Sync
     } else {
       if (l > 0) load_q(l, bq);
     }
-    // the next layer's rows (the last layer loads its own first stages again: every stage
-    // is then followed by the same number of loads)
+    // the next layer's rows
     const auto rs_next = rsrc(l + 1 < L ? l + 1 : l);
     float m = -INFINITY, ssum = 0.f;  // running (max, sum of exp2) of column lr
     // ---- logits of the wave's TW tiles, NB stages at a time
@@ -205,9 +204,13 @@ __device__ __forceinline__ void score_sync_call(const SyncCall& a, int blk, Sync
 #pragma unroll
       for (int r = 0; r < NB; ++r) {
         const int qi = g0 + r, qn = qi + NB - 1, s = r % SPT;
-        // the stage NB - 1 ahead: of this layer, else of the next one
-        const bool next = qn >= NST;
-        issue(next ? rs_next : rs, (next ? qn - NST : qn) / SPT, (NB - 1 + r) % SPT, buf[(r + NB - 1) % NB]);
+        // the stage NB - 1 ahead: of this layer, else of the next one; past the last layer,
+        // this layer's last stage again (its rows are in flight or in L2, so these loads,
+        // which keep the number of loads behind every stage the same, cost no HBM traffic)
+        const bool next = qn >= NST, past = next && l + 1 >= L;
+        const int qs = past ? NST - 1 : (next ? qn - NST : qn);
+        issue(next && !past ? rs_next : rs, qs / SPT, past ? (NST - 1) % SPT : (NB - 1 + r) % SPT,
+              buf[(r + NB - 1) % NB]);
 #pragma unroll
         for (int h = 0; h < HPS; ++h) {
           const int u = s * HPS + h;
