@@ -337,9 +337,12 @@ dustin_status dustin_arr(const float* s, int64_t s_sb, int64_t s_sg, const int32
  *       required when both s_draft and s_target are given (else NULL, 0 will do): the two
  *       tiers of a row are selected side by side (I_D, and C_T = the k - |P| best free
  *       positions by S_T, of which I_T is the k - m - |P| best outside I_D) and hand off
- *       through it.  It holds an arrival counter per (b, go), then two bitmaps of max_len
- *       bits per (b, go).  Zero-fill it once before its first use: every call leaves the
- *       counters at zero again.  Calls sharing a workspace must not overlap.
+ *       through it.  It holds a 16 KB counter region (one arrival counter per (b, go);
+ *       B * groups <= 4096, beyond which no workspace is needed and the tiers of a row run
+ *       one after the other), then two bitmaps of max_len bits per (b, go).  Zero-fill it
+ *       once before its first use: every call leaves the counter region at zero again, so
+ *       one buffer can then serve calls of any shape.  Calls sharing a workspace must not
+ *       overlap.
  * The result is a pure function of the fp32 inputs: bit-exact and deterministic.
  * --------------------------------------------------------------------------------- */
 size_t dustin_topk_workspace(int32_t batch, int32_t groups, int32_t max_len);

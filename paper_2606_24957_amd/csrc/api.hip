@@ -794,8 +794,13 @@ dustin_status dustin_arr(const float* s, int64_t s_sb, int64_t s_sg, const int32
 
 namespace {
 
-// Top-k workspace: an arrival counter per (b, go), then two bitmaps of the row's positions
-// per (b, go) for the hand-off between its two tiers.
+// Top-k workspace: an arrival counter per (b, go) in a region of fixed size (kTopkMaxRows
+// counters, whatever the call's shape, so that a buffer that served a call of another shape
+// still reads zero there), then two bitmaps of the row's positions per (b, go) for the
+// hand-off between its two tiers.  Beyond kTopkMaxRows rows there is no hand-off (and no
+// workspace): the tiers of a row run one after the other in one workgroup.
+constexpr int64_t kTopkMaxRows = 4096;
+
 struct TopkWs {
   size_t counters, bitmaps, total;
   int32_t words;
@@ -805,8 +810,9 @@ TopkWs topk_ws_layout(int32_t batch, int32_t groups, int32_t max_len) {
   TopkWs w{0, 0, 0, 0};
   if (batch <= 0 || groups <= 0 || max_len <= 0) return w;
   const size_t rows = (size_t)batch * groups;
+  if (rows > (size_t)kTopkMaxRows) return w;
   w.words = (max_len + 31) / 32;
-  w.counters = round_up(rows * sizeof(uint32_t), kAlign);
+  w.counters = kTopkMaxRows * sizeof(uint32_t);
   w.bitmaps = round_up(rows * 2 * (size_t)w.words * sizeof(uint32_t), kAlign);
   w.total = w.counters + w.bitmaps;
   return w;

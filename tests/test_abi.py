@@ -44,9 +44,10 @@ def test_status_strings_and_version(L):
 
 
 def test_workspace_sizes(L):
-    t = L.dustin_topk_workspace(16, 1, 32768)   # counters and two bitmaps per row
-    assert t >= 16 * 2 * 1024 * 4 and t % 256 == 0
+    t = L.dustin_topk_workspace(16, 1, 32768)   # a fixed counter region, two bitmaps per row
+    assert t == 4096 * 4 + 16 * 2 * 1024 * 4 and t % 256 == 0
     assert L.dustin_topk_workspace(0, 1, 32768) == 0
+    assert L.dustin_topk_workspace(4097, 1, 1000) == 0   # no hand-off: no workspace
     s = L.dustin_score_workspace(16, 32768, 4, 4)
     assert s >= D.SCORE_SYNC_BYTES + 16 * 4 * 4 * 32768 * 4 and s % 256 == 0
     assert L.dustin_score_workspace(0, 10, 1, 1) == 0

@@ -120,3 +120,26 @@ def test_topk_calls_of_different_shapes_in_turn():
         sd = _scores("uniform", B, N, 30 + t)
         st = np.random.default_rng(40 + t).random((B, G, N)).astype(np.float32)
         _compare(sd, st, [N - b for b in range(B)], k, groups=G)
+
+
+def test_topk_workspace_reused_by_a_call_with_more_rows():
+    """A workspace that served long rows (its bitmaps written) serves a later call with
+    more rows and a smaller total size: the arrival counters of every row still start at
+    zero (they live in a region of fixed size at the start)."""
+    shapes = [(4, 1, 131072, 2048), (16, 8, 1000, 128), (4, 1, 131072, 2048), (16, 8, 1000, 128)]
+    sizes = [D.lib().dustin_topk_workspace(B, G, N) for B, G, N, _ in shapes]
+    assert sizes[1] < sizes[0]          # the second call reuses the first call's buffer
+    for t, (B, G, N, k) in enumerate(shapes):
+        sd = _scores("uniform", B, N, 80 + t)
+        st = np.random.default_rng(90 + t).random((B, G, N)).astype(np.float32)
+        _compare(sd, st, [N - b for b in range(B)], k, groups=G)
+
+
+def test_topk_many_rows_run_the_tiers_in_turn():
+    """Beyond 4096 (sequence, group) rows there is no hand-off workspace: each row's two
+    tiers run one after the other in one workgroup."""
+    B, G, N, k = 520, 8, 300, 64
+    assert D.lib().dustin_topk_workspace(B, G, N) == 0
+    sd = _scores("dirichlet", B, N, 95)
+    st = np.random.default_rng(96).random((B, G, N)).astype(np.float32)
+    _compare(sd, st, [N - (b % 50) for b in range(B)], k, groups=G)
