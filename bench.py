@@ -611,7 +611,8 @@ def main():
     sp_us, dn_us = mean(sp) * 1e3, mean(dn) * 1e3
     est_us = (mean(est_s) + mean(est_k)) * 1e3
     sb, db = sparse_bytes(s), dense_bytes(s)
-    eb = score_bytes(s, True) + (0 if est.s_draft_given is not None else score_bytes(s, False)) + topk_bytes(s)
+    est_sd_given = est.s_draft_given is not None
+    eb = score_bytes(s, True) + (0 if est_sd_given else score_bytes(s, False)) + topk_bytes(s)
     achieved = sb / (sp_us * 1e-6) / 1e9 if sp else float("nan")
     dense_gbps = db / (dn_us * 1e-6) / 1e9 if dn else float("nan")
     log(f"[bench] sparse {sp_us:.2f} us/layer (median {med(sp) * 1e3:.2f}; with an event between launches "
@@ -696,6 +697,22 @@ def main():
         copy_gbps = round(2 * (1 << 30) * 5 / (c0.elapsed_time(c1) * 1e-3) / 1e9, 1)
         del src, dst
         log(f"[bench] 1 GiB device copy: {copy_gbps} GB/s (read + write)")
+    # ... and what a plain streaming read of 2 GiB reaches (the library's read probe), the
+    # practical ceiling of the read-only kernels
+    read_gbps = None
+    if args.only == "all":
+        buf = torch.zeros(1 << 31, dtype=torch.uint8, device=dev)
+        probe = D.plan_read_probe(buf, blocks=1024)
+        probe()
+        c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        c0.record()
+        for _ in range(5):
+            probe()
+        c1.record()
+        torch.cuda.synchronize()
+        read_gbps = round((1 << 31) * 5 / (c0.elapsed_time(c1) * 1e-3) / 1e9, 1)
+        del buf, probe
+        log(f"[bench] 2 GiB streaming read: {read_gbps} GB/s")
 
     # the other workloads through the same timed step, after the headline's buffers are gone
     others = None
@@ -710,6 +727,8 @@ def main():
             others[tag] = r2
 
     traffic = measured_traffic(s.name, s.k_max)
+    sc_bytes = score_bytes(s, True) + (0 if est_sd_given else score_bytes(s, False))
+    scores_gbps = round(sc_bytes / (mean(est_s) * 1e-3) / 1e9, 1) if est_s and mean(est_s) > 0 else None
     rec = {
         "metric": "sparse verify-attention us/layer + achieved HBM GB/s, B=16 ctx=32k 72B-shape",
         "value": round(sp_us, 3),
@@ -744,13 +763,18 @@ def main():
             "overfetch": round(traffic / sb, 4) if traffic else None,
             "measured_copy_GBps": copy_gbps,
             "frac_of_measured_copy": round(achieved / copy_gbps, 4) if copy_gbps else None,
+            "measured_read_GBps": read_gbps,
+            "frac_of_measured_read": round(achieved / read_gbps, 4) if read_gbps else None,
         },
         "dense": {"us_per_layer": round(dn_us, 3), "GBps": round(dense_gbps, 1), "bytes_per_launch": db,
                   "frac": round(dense_gbps / PEAK_HBM_GBPS, 4)},
         "estimation": {"us_per_step": round(est_us, 3), "scores_one_launch_us": round(mean(est_s) * 1e3, 3),
                        "target_score_us": round(est_t * 1e3, 3), "draft_score_us": round(est_d * 1e3, 3),
                        "topk_us": round(mean(est_k) * 1e3, 3),
-                       "bytes": eb, "GBps": round(eb / (est_us * 1e-6) / 1e9, 1) if est_us == est_us else None},
+                       "bytes": eb, "GBps": round(eb / (est_us * 1e-6) / 1e9, 1) if est_us == est_us else None,
+                       "scores_GBps": scores_gbps,
+                       "scores_frac_of_measured_read": round(scores_gbps / read_gbps, 4)
+                       if scores_gbps and read_gbps else None},
         "speedup": {
             "per_layer": round(dn_us / sp_us, 3) if sp else None,
             f"per_step_L{L}": round(L * dn_us / (est_us + L * sp_us), 3) if sp else None,

@@ -457,6 +457,21 @@ dustin_status dustin_kv_append(const void* k_new, int64_t k_sb, int64_t k_st, in
 dustin_status dustin_kv_commit(int32_t* seq_lens, const int32_t* accepted, const int32_t* n_query,
                                int32_t batch, int32_t nq_max, void* stream);
 
+/* ---------------------------------------------------------------------------------
+ * dustin_read_probe -- a plain streaming read of a device buffer, for measurement only (no
+ * part of the method): the practical read rate of the GPU, against which the rates of the
+ * bandwidth-bound kernels above are reported.  Workgroup g of `blocks` reads the g-th of
+ * `blocks` equal runs of the buffer with 16-byte loads and writes the wrapping sum of the
+ * 32-bit words it read to block_sums[g] (so the sums over the workgroups add up to the
+ * wrapping sum of every word of the buffer).
+ *   data        device buffer, 16-byte aligned; bytes a multiple of 16
+ *   block_sums  device uint32 [blocks]; 1 <= blocks <= 65536, bytes / blocks < 2 GiB
+ * Returns DUSTIN_ERR_INVALID_ARG on a bad pointer, size or count, DUSTIN_ERR_UNSUPPORTED
+ * when a workgroup's run would reach 2 GiB.
+ * --------------------------------------------------------------------------------- */
+dustin_status dustin_read_probe(const void* data, size_t bytes, uint32_t* block_sums, int32_t blocks,
+                                void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -30,7 +30,7 @@ EXPORTED = ("dustin_status_string", "dustin_version", "dustin_score_workspace", 
             "dustin_sparse_verify_attn", "dense_verify_attn", "dustin_kv_append", "dustin_kv_commit",
             "dustin_score_layers", "dustin_page_meta", "dustin_page_score_workspace",
             "dustin_page_score", "dustin_arr", "dustin_score_per_layer",
-            "dustin_sparse_verify_attn_noalloc", "dustin_score_calls")
+            "dustin_sparse_verify_attn_noalloc", "dustin_score_calls", "dustin_read_probe")
 
 
 class DustinError(RuntimeError):
@@ -132,6 +132,8 @@ def lib():
         L.dustin_score_calls.argtypes = [_i32, ctypes.POINTER(DustinScoreCall), _vp]
         L.dustin_kv_commit.restype = ctypes.c_int
         L.dustin_kv_commit.argtypes = [_vp, _vp, _vp, _i32, _i32, _vp]
+        L.dustin_read_probe.restype = ctypes.c_int
+        L.dustin_read_probe.argtypes = [_vp, _sz, _vp, _i32, _vp]
         _lib = L
     return _lib
 
@@ -623,6 +625,18 @@ def plan_topk(s_draft: Optional[torch.Tensor], s_target: Optional[torch.Tensor],
 def topk(s_draft, s_target, seq_lens, k_max, **kw):
     """Eq. 6; returns (idx int32 [B, groups, k_max], count int32 [B, groups])."""
     return plan_topk(s_draft, s_target, seq_lens, k_max, **kw)()
+
+
+def plan_read_probe(data: torch.Tensor, blocks: int = 1024, stream=None) -> "Call":
+    """Prepared dustin_read_probe over a contiguous device tensor (its bytes, a multiple of
+    16): a plain streaming read, for measuring the read rate.  Returns the per-workgroup
+    wrapping sums of its 32-bit words, uint32 as int32 [blocks]."""
+    if not data.is_cuda or not data.is_contiguous():
+        raise ValueError("data must be a contiguous device tensor")
+    nbytes = data.numel() * data.element_size()
+    sums = torch.empty(int(blocks), dtype=torch.int32, device=data.device)
+    args = (_ptr(data), nbytes, _ptr(sums), int(blocks), _stream(stream))
+    return Call(lib().dustin_read_probe, args, "dustin_read_probe", (data,), sums)
 
 
 

@@ -8,7 +8,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libdustin.so")
-SOURCES = ["api.hip", "attn.hip", "score.hip", "score_sync.hip", "topk.hip", "kv.hip", "page.hip", "arr.hip"]
+SOURCES = ["api.hip", "attn.hip", "score.hip", "score_sync.hip", "topk.hip", "kv.hip", "page.hip", "arr.hip",
+           "probe.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 

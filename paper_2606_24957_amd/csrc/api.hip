@@ -9,6 +9,7 @@
 #include <mutex>
 
 #include "kernels.hpp"
+#include "probe.hpp"
 
 using namespace dustin;
 
@@ -1014,3 +1015,15 @@ extern "C" dustin_status dustin_sparse_verify_attn_noalloc(
   }
   return launch_attention(call, true, ws, stream);
 }
+
+// ------------------------------------------------------------------ streaming-read probe
+
+dustin_status dustin_read_probe(const void* data, size_t bytes, uint32_t* block_sums, int32_t blocks,
+                                void* stream) {
+  if (!data || !block_sums || blocks < 1 || blocks > 65536) return DUSTIN_ERR_INVALID_ARG;
+  if (!aligned(data, 16) || !aligned(block_sums, 4) || bytes % 16) return DUSTIN_ERR_INVALID_ARG;
+  if (bytes / 16 / (size_t)blocks + 1 >= ((size_t)1 << 31) / 16) return DUSTIN_ERR_UNSUPPORTED;
+  const hipError_t e = launch_read_probe(data, bytes, block_sums, blocks, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? DUSTIN_OK : DUSTIN_ERR_LAUNCH;
+}
+

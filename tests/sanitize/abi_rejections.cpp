@@ -25,6 +25,7 @@ hipError_t launch_kv_append(const KvAppendArgs&, hipStream_t) { return hipErrorI
 hipError_t launch_kv_commit(int32_t*, const int32_t*, const int32_t*, int, int, hipStream_t) {
   return hipErrorInvalidValue;
 }
+hipError_t launch_read_probe(const void*, uint64_t, uint32_t*, int, hipStream_t) { return hipErrorInvalidValue; }
 }  // namespace dustin
 
 static int failures = 0;
@@ -266,6 +267,17 @@ int main() {
     EXPECT(dustin_kv_commit(static_cast<int32_t*>(FAKE), nullptr, nullptr, 2, 4, nullptr), DUSTIN_ERR_INVALID_ARG);
     EXPECT(dustin_kv_commit(static_cast<int32_t*>(FAKE), static_cast<const int32_t*>(FAKE), nullptr, -1, 4, nullptr),
            DUSTIN_ERR_INVALID_ARG);
+  }
+  {  // the streaming-read probe
+    uint32_t* sums = static_cast<uint32_t*>(FAKE);
+    EXPECT(dustin_read_probe(nullptr, 4096, sums, 4, nullptr), DUSTIN_ERR_INVALID_ARG);
+    EXPECT(dustin_read_probe(FAKE, 4096, nullptr, 4, nullptr), DUSTIN_ERR_INVALID_ARG);
+    EXPECT(dustin_read_probe(fake(8), 4096, sums, 4, nullptr), DUSTIN_ERR_INVALID_ARG);
+    EXPECT(dustin_read_probe(FAKE, 4100, sums, 4, nullptr), DUSTIN_ERR_INVALID_ARG);
+    EXPECT(dustin_read_probe(FAKE, 4096, sums, 0, nullptr), DUSTIN_ERR_INVALID_ARG);
+    EXPECT(dustin_read_probe(FAKE, 4096, sums, 65537, nullptr), DUSTIN_ERR_INVALID_ARG);
+    EXPECT(dustin_read_probe(FAKE, (size_t)1 << 32, sums, 1, nullptr), DUSTIN_ERR_UNSUPPORTED);
+    EXPECT(dustin_read_probe(FAKE, 4096, sums, 4, nullptr), DUSTIN_ERR_LAUNCH);
   }
 
   printf("%s: %d failed expectations\n", failures ? "FAILED" : "ok", failures);

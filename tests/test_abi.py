@@ -208,6 +208,17 @@ def test_score_calls_rejects(L):
     assert L.dustin_score_calls(1, small, None) == D.ERR_WORKSPACE
 
 
+def test_read_probe_rejects(L):
+    f = ctypes.c_void_p(FAKE)
+    assert L.dustin_read_probe(None, 4096, f, 4, None) == D.ERR_INVALID_ARG
+    assert L.dustin_read_probe(f, 4096, None, 4, None) == D.ERR_INVALID_ARG
+    assert L.dustin_read_probe(ctypes.c_void_p(FAKE + 8), 4096, f, 4, None) == D.ERR_INVALID_ARG
+    assert L.dustin_read_probe(f, 4100, f, 4, None) == D.ERR_INVALID_ARG
+    assert L.dustin_read_probe(f, 4096, f, 0, None) == D.ERR_INVALID_ARG
+    assert L.dustin_read_probe(f, 4096, f, 65537, None) == D.ERR_INVALID_ARG
+    assert L.dustin_read_probe(f, 1 << 32, f, 1, None) == D.ERR_UNSUPPORTED
+
+
 def test_product_never_touches_the_oracle():
     """The HIP path has no CPU fallback and never imports the checker."""
     pkg = os.path.join(ROOT, "paper_2606_24957_amd")
