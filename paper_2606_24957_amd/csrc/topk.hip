@@ -26,6 +26,8 @@
 
 namespace dustin {
 
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
 constexpr int kTopkThreads = 1024;
 constexpr int kTopkWaves = kTopkThreads / kWave;
 constexpr int kBins1 = 4096;                            // first digit: key bits 31..20
@@ -291,87 +293,95 @@ __device__ __forceinline__ void select_tier_fast(TopkSmem& s, KeyStage& ks, uint
   if (need == 0) return;
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
   const int N = ks.N;
-  const float* row = ks.row;
-  const int ngroups = (N + kWave - 1) / kWave;  // 64-position groups; wave w takes w, w + 16, ...
-
-  // Keys of this wave's groups, kFastBatch groups at a time (a row of up to kFastBatch
-  // groups per wave is loaded once for both passes).
-  const int iters = (ngroups + kTopkWaves - 1) / kTopkWaves;
-  const bool resident = iters <= kFastBatch;
+  const int ngroups = (N + kWave - 1) / kWave;  // 64-position groups
+  // wave w takes the run of groups [w gpw, (w + 1) gpw), kFastBatch at a time; a run of up
+  // to kFastBatch groups is loaded once for both passes
+  const int gpw = (ngroups + kTopkWaves - 1) / kTopkWaves;
+  const int g_first = wave * gpw;
+  const bool resident = gpw <= kFastBatch;
+  // the row through a buffer resource: loads past its N values read 0.0, at positions the
+  // bitmap (padded with taken bits to a whole number of groups) marks taken
+  // (the row pointer comes through a small local array: made explicitly uniform, so that
+  // the resource lives in scalar registers)
+  // (readfirstlane returns a signed int: each half is taken back through uint32_t, so that
+  // the low half is not sign-extended into the high one)
+  const uint64_t rp = reinterpret_cast<uint64_t>(ks.row);
+  const uint32_t rp_hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(rp >> 32));
+  const uint32_t rp_lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)rp);
+  const uint64_t rpu = ((uint64_t)rp_hi << 32) | (uint64_t)rp_lo;
+  const auto rs = __builtin_amdgcn_make_buffer_rsrc(reinterpret_cast<void*>(rpu), 0,
+                                                    __builtin_amdgcn_readfirstlane(N * 4), 0x00020000);
+  const int lane_pos = g_first * kWave + lane;  // this lane's position in the run's first group
+  const uint32_t* const bm_lane = bm + 2 * g_first + (lane >> 5);  // its bitmap word there
+  const int bit = lane & 31;
   uint32_t kb[kFastBatch];
   auto load_batch = [&](int i0) {
     float v[kFastBatch];
+    const int off = (lane_pos + i0 * kWave) * 4;
 #pragma unroll
-    for (int u = 0; u < kFastBatch; ++u) v[u] = row[min((wave + kTopkWaves * (i0 + u)) * kWave + lane, N - 1)];
+    for (int u = 0; u < kFastBatch; ++u)
+      v[u] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, off + u * kWave * 4, 0, 0));
 #pragma unroll
     for (int u = 0; u < kFastBatch; ++u) kb[u] = order_key(v[u]);
   };
-  // keys and free flags of kScanBatch groups of the batch loaded at i0 (sub-batch j0)
-  auto fetch = [&](int i0, int j0, uint32_t* key, bool* fr) {
-    uint32_t word[kScanBatch];
+  // free flags of the batch at i0: inside this wave's run and the row, and not yet chosen
+  auto free_flags = [&](int i0, bool* fr) {
+    uint32_t word[kFastBatch];
 #pragma unroll
-    for (int u = 0; u < kScanBatch; ++u) {
-      const int n = min((wave + kTopkWaves * (i0 + j0 + u)) * kWave + lane, N - 1);
-      word[u] = bm[n >> 5];
-    }
+    for (int u = 0; u < kFastBatch; ++u) word[u] = bm_lane[2 * (i0 + u)];
 #pragma unroll
-    for (int u = 0; u < kScanBatch; ++u) {
-      const int g = wave + kTopkWaves * (i0 + j0 + u);
-      const int n = g * kWave + lane;
-      key[u] = kb[j0 + u];
-      fr[u] = g < ngroups && n < N && !((word[u] >> (n & 31)) & 1u);
-    }
+    for (int u = 0; u < kFastBatch; ++u)
+      fr[u] = i0 + u < gpw && g_first + i0 + u < ngroups && !((word[u] >> bit) & 1u);
   };
   if (resident) load_batch(0);
 
   // ---- A
   for (int i = tid; i < kBins1; i += kTopkThreads) s.hist[i] = 0u;
   __syncthreads();
-  for (int i0 = 0; i0 < iters; i0 += kFastBatch) {
+  for (int i0 = 0; i0 < gpw; i0 += kFastBatch) {
     if (!resident) load_batch(i0);
+    bool fr[kFastBatch];
+    free_flags(i0, fr);
 #pragma unroll
-    for (int j0 = 0; j0 < kFastBatch; j0 += kScanBatch) {
-      uint32_t key[kScanBatch];
-      bool fr[kScanBatch];
-      fetch(i0, j0, key, fr);
-#pragma unroll
-      for (int u = 0; u < kScanBatch; ++u) hist_add(s.hist, key[u] >> 20, fr[u]);
-    }
+    for (int u = 0; u < kFastBatch; ++u) hist_add(s.hist, kb[u] >> 20, fr[u]);
   }
   __syncthreads();
   find_digit<kBins1>(s, need);
   const uint32_t d1 = s.misc[0], r1 = s.misc[1];
 
-  // ---- B (each wave appends to its own slice of the candidate list)
+  // ---- B (each wave appends to its own slice of the candidate list; a wave whose slice
+  // would overflow stops appending, and the tier then takes the general path below)
   const int wcap = cap / kTopkWaves;
   uint32_t* const wlist = cand + 2 * wave * wcap;
   uint32_t wcount = 0;  // wave-uniform
-  for (int i0 = 0; i0 < iters; i0 += kFastBatch) {
+  for (int i0 = 0; i0 < gpw; i0 += kFastBatch) {
     if (!resident) load_batch(i0);
+    bool fr[kFastBatch];
+    free_flags(i0, fr);
+    uint64_t take[kFastBatch];
 #pragma unroll
-    for (int j0 = 0; j0 < kFastBatch; j0 += kScanBatch) {
-    uint32_t key[kScanBatch];
-    bool fr[kScanBatch];
-    fetch(i0, j0, key, fr);
-    uint64_t take[kScanBatch];
-#pragma unroll
-    for (int u = 0; u < kScanBatch; ++u) {
-      take[u] = __ballot(fr[u] && (key[u] >> 20) > d1);
-      const bool inbin = fr[u] && (key[u] >> 20) == d1;
+    for (int u = 0; u < kFastBatch; ++u) {
+      const uint32_t dig = kb[u] >> 20;
+      take[u] = __ballot(fr[u] && dig > d1);
+      const bool inbin = fr[u] && dig == d1;
       const uint64_t cm = __ballot(inbin);
-      const uint32_t at = wcount + __popcll(cm & lanemask_lt(lane));
-      if (inbin && at < (uint32_t)wcap) {
-        wlist[2 * at] = key[u];
-        wlist[2 * at + 1] = (uint32_t)((wave + kTopkWaves * (i0 + j0 + u)) * kWave + lane);
+      if (cm) {
+        const uint32_t c = (uint32_t)__popcll(cm);
+        if (wcount + c <= (uint32_t)wcap && inbin) {
+          const uint32_t at = wcount + __builtin_amdgcn_mbcnt_hi((uint32_t)(cm >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)cm, 0u));
+          *reinterpret_cast<u32x2*>(wlist + 2 * at) = u32x2{kb[u], (uint32_t)(lane_pos + (i0 + u) * kWave)};
+        }
+        wcount += c;
       }
-      wcount += __popcll(cm);
     }
-    // the two bitmap words of a group belong to the wave that owns the group
+    // the bitmap words of the batch's groups are this wave's alone: lanes 0 and 32 write the
+    // low and the high word of each group, after every read of the batch
 #pragma unroll
-    for (int u = 0; u < kScanBatch; ++u) {
-      const int g = wave + kTopkWaves * (i0 + j0 + u);
-      if (g < ngroups) mark64(bm, g * kWave, N, take[u]);
-    }
+    for (int u = 0; u < kFastBatch; ++u) {
+      if (take[u] && (lane & 31) == 0) {
+        uint32_t* const w = const_cast<uint32_t*>(bm_lane) + 2 * (i0 + u);
+        *w |= lane == 0 ? (uint32_t)take[u] : (uint32_t)(take[u] >> 32);
+      }
     }
   }
   if (lane == 0) s.wave_cnt[wave] = wcount;
@@ -440,8 +450,13 @@ __device__ __noinline__ void select_tier_fast_outlined(TopkSmem& s, KeyStage& ks
 
 // Key-segment length for rows of up to max_len positions: the LDS left beside the
 // static state and the bitmap, a multiple of kSegQuantum, at most the row rounded up.
+// Bitmap words kept for rows of up to max_len positions: two per 64-position group, plus the
+// groups past the row that the waves' runs (16 runs of whole groups, up to 15 groups past
+// the row) and a last batch (up to 7 groups past a run) may read, all initialised as taken.
+__host__ __device__ inline int topk_bitmap_words(int max_len) { return 2 * ((max_len + 63) / 64 + 24); }
+
 static int topk_segment(int max_len) {
-  const int nwords = (max_len + 31) / 32;
+  const int nwords = topk_bitmap_words(max_len);
   const int avail = (kTopkLds - (int)sizeof(TopkSmem)) / 4 - nwords;
   const int cap = avail / kSegQuantum * kSegQuantum;
   const int row = (max_len + kSegQuantum - 1) / kSegQuantum * kSegQuantum;
@@ -583,7 +598,7 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(TopkArgs a, int seg)
     const int c = x - n0;
     return c <= 0 ? 0u : (c >= 32 ? ~0u : (1u << c) - 1u);
   };
-  for (int w = tid; w < nwords; w += kTopkThreads)
+  for (int w = tid; w < topk_bitmap_words(N); w += kTopkThreads)
     bm[w] = below(a.n_sink, w * 32) | ~below(N - a.n_window, w * 32);
   // a row shorter than the segment uses a shorter one (still a multiple of kSegQuantum)
   const int rseg = min(seg, (N + kSegQuantum - 1) / kSegQuantum * kSegQuantum);
@@ -666,8 +681,7 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(TopkArgs a, int seg)
 hipError_t launch_topk(const TopkArgs& a, int B, hipStream_t stream) {
   const int seg = topk_segment(a.dims.max_len);
   if (seg < kSegQuantum) return hipErrorInvalidValue;
-  const int nwords = (a.dims.max_len + 31) / 32;
-  const size_t dyn = (size_t)(seg + nwords) * sizeof(uint32_t);
+  const size_t dyn = (size_t)(seg + topk_bitmap_words(a.dims.max_len)) * sizeof(uint32_t);
   // the dynamic-LDS limit is raised once per device (not per launch, so that launches can
   // be recorded in a graph after the first one)
   static bool lds_raised[64] = {};

@@ -143,3 +143,31 @@ def test_topk_many_rows_run_the_tiers_in_turn():
     sd = _scores("dirichlet", B, N, 95)
     st = np.random.default_rng(96).random((B, G, N)).astype(np.float32)
     _compare(sd, st, [N - (b % 50) for b in range(B)], k, groups=G)
+
+
+def test_topk_rows_whose_low_address_word_is_above_two_gib():
+    """Score rows placed where the low 32 bits of their address have bit 31 set: the kernel
+    rebuilds each row's address from two 32-bit halves, and the low half must not be
+    sign-extended into the high one."""
+    B, N, k = 2, 40000, 1024
+    sd, st = _scores("uniform", B, N, 97), _scores("dirichlet", B, N, 98)
+    span = B * N * 4
+    pool = torch.empty((1 << 32) + 2 * span + 4096, dtype=torch.uint8, device=DEV)
+    base = pool.data_ptr()
+    off = ((0x80000100 - (base & 0xFFFFFFFF)) % (1 << 32))  # low word 0x80000100, 256-byte aligned
+    assert (base + off) % 256 == 0 and ((base + off) & 0xFFFFFFFF) >= 0x80000000
+    views = []
+    for j, a in enumerate((sd, st)):
+        v = pool[off + j * span: off + (j + 1) * span].view(torch.float32).view(B, 1, N)
+        v.copy_(torch.from_numpy(a))
+        views.append(v)
+    P = 20
+    idx_ref, cnt_ref = O.select(sd, st, [N, N - 7], k, m_scalar=(k - P) // 2, n_sink=4, n_window=16)
+    idx_g, cnt_g = D.topk(views[0], views[1], torch.tensor([N, N - 7], dtype=torch.int32, device=DEV), k,
+                          m_scalar=(k - P) // 2, n_sink=4, n_window=16)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(cnt_g.cpu().numpy(), cnt_ref)
+    for b in range(B):
+        c = cnt_ref[b, 0]
+        np.testing.assert_array_equal(idx_g.cpu().numpy()[b, 0, :c], idx_ref[b, 0, :c])
+    del pool, views
