@@ -47,6 +47,9 @@ def parse():
     p.add_argument("--cpu-sample-seqs", type=int, default=16)
     p.add_argument("--no-secondary", action="store_true",
                    help="skip the other workloads (ragged, 131k, k = 512) that the headline run also times")
+    p.add_argument("--no-digit-hist", action="store_true",
+                   help="the top-k makes its own first pass over each row instead of taking the score calls' "
+                        "first-digit histograms")
     p.add_argument("--copy-probe", action="store_true",
                    help="also run one plain 1 GiB device copy (counter calibration)")
     p.add_argument("--only", choices=["all", "sparse", "dense", "estimate", "page"], default="all",
@@ -151,7 +154,7 @@ class StepTimer:
     back to back, as in a forward pass, since an event between launches adds an end-of-pipe
     wait of its own)."""
 
-    def __init__(self, s, layers, est, dev):
+    def __init__(self, s, layers, est, dev, digit_hist=True):
         import torch
         import paper_2606_24957_amd as D
         self.s, self.L = s, len(layers)
@@ -178,10 +181,15 @@ class StepTimer:
                                                     n_query=self.gam, out=self.s_d, max_len=N,
                                                     ws_tag="score_draft"))
         # the target's and the draft's scores in one dustin_score_calls (one launch where both
-        # take the single-pass form)
-        self.scores = D.plan_score_calls([self.score_t] + self.score_d)
+        # take the single-pass form); with one selection group they count their outputs by top
+        # key digit, and the top-k takes those counts in place of its first pass
+        self.hist_t = D.digit_hist(B, dev) if G == 1 and digit_hist else None
+        self.hist_d = D.digit_hist(B, dev) if G == 1 and self.score_d and digit_hist else None
+        self.scores = D.plan_score_calls([self.score_t] + self.score_d,
+                                         digit_hists=[self.hist_t] + [self.hist_d] * len(self.score_d))
         self.sel = D.plan_topk(self.s_d, self.s_t, self.seq, s.k_max, budget=self.bud, m=self.mm, n_sink=s.n_sink,
-                               n_window=s.n_window, groups=G, idx=self.idx, count=self.cnt)
+                               n_window=s.n_window, groups=G, idx=self.idx, count=self.cnt, hist_d=self.hist_d,
+                               hist_t=self.hist_t)
         self.sparse = [D.plan_sparse_verify_attn(l.q, l.k, l.v, self.idx, self.cnt, self.seq, n_query=self.nq,
                                                  page_table=l.page_table, out=o)
                        for l, o in zip(layers, self.outs)]
@@ -599,7 +607,7 @@ def main():
     torch.cuda.synchronize()
     log(f"[bench] inputs generated in {time.perf_counter() - t0:.1f}s")
 
-    T = StepTimer(s, layers, est, dev)
+    T = StepTimer(s, layers, est, dev, digit_hist=not args.no_digit_hist)
     seq, nq, bud, mm = T.seq, T.nq, T.bud, T.mm
     s_t, s_d, idx, cnt = T.s_t, T.s_d, T.idx, T.cnt
     r = T.run(args.steps, args.warmup, args.only, copy_probe=args.copy_probe)

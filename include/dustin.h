@@ -191,9 +191,16 @@ dustin_status dustin_score_layers(int32_t n_layers, const void* const* q_layers_
  *   calls    host array of n_calls (1 or 2) descriptors; each holds the arguments of one
  *            dustin_score_layers call (n_layers = 1 is a dustin_score call), with a
  *            workspace of its own (distinct workspaces; each as dustin_score requires)
+ *   digit_hist  NULL, or device uint32 [batch * groups][4096], 16-byte aligned, zero before
+ *            the call: for every written out[b, go, n] (n < N_b) the call adds one to
+ *            digit_hist[(b * groups + go) * 4096 + key >> 20], key the order-preserving
+ *            uint32 of the fp32 output (dustin_topk's ranking key).  It is the first-digit
+ *            histogram that dustin_topk can take in place of its first pass over the row
+ *            (hist_draft / hist_target), and dustin_topk returns it to zero.
  * Neither call may write a buffer that the other reads or writes.  Errors: as
  * dustin_score_layers for either call (nothing is enqueued), DUSTIN_ERR_INVALID_ARG for
- * n_calls outside [1, 2], DUSTIN_ERR_WORKSPACE for a shared workspace.
+ * n_calls outside [1, 2] or a misaligned or shared digit_hist, DUSTIN_ERR_WORKSPACE for a
+ * shared workspace.
  * --------------------------------------------------------------------------------- */
 typedef struct {
   int32_t n_layers;
@@ -212,6 +219,7 @@ typedef struct {
   int64_t out_sb, out_sg;
   void* workspace;
   size_t workspace_bytes;
+  uint32_t* digit_hist;
 } dustin_score_call;
 dustin_status dustin_score_calls(int32_t n_calls, const dustin_score_call* calls, void* stream);
 
@@ -333,6 +341,13 @@ dustin_status dustin_arr(const float* s, int64_t s_sb, int64_t s_sg, const int32
  *   bt       seq_lens, budget/k_max, m/m_scalar; 1 <= max_len <= 1 << 19
  *   groups   1 or the KV head count
  *   idx      int32 [B, groups, >= k_max] (strides idx_sb, idx_sg), count int32 [B*groups]
+ *   hist_draft / hist_target  NULL, or (groups = 1, with s_draft / s_target given) device
+ *       uint32 [B][4096], 16-byte aligned: for each sequence, the count of positions
+ *       n < N_b of its S_D / S_T row per top key digit (key >> 20), as dustin_score_calls
+ *       writes with digit_hist.  A tier that is its workgroup's first job then takes it, less
+ *       the protected positions, instead of a first pass over the row.  Every given histogram
+ *       is left at zero.  The histograms must describe the rows passed here (same values,
+ *       same N_b): the result is then the same as without them.
  *   workspace  dustin_topk_workspace(batch, groups, max_len) bytes, 256-byte aligned,
  *       required when both s_draft and s_target are given (else NULL, 0 will do): the two
  *       tiers of a row are selected side by side (I_D, and C_T = the k - |P| best free
@@ -350,8 +365,8 @@ dustin_status dustin_topk(const float* s_draft, int64_t d_sb, int64_t d_sg,
                           const float* s_target, int64_t t_sb, int64_t t_sg,
                           const dustin_batch* bt, int32_t groups, int32_t n_sink,
                           int32_t n_window, int32_t* idx, int64_t idx_sb, int64_t idx_sg,
-                          int32_t* count, void* workspace, size_t workspace_bytes,
-                          void* stream);
+                          int32_t* count, uint32_t* hist_draft, uint32_t* hist_target,
+                          void* workspace, size_t workspace_bytes, void* stream);
 
 /* ---------------------------------------------------------------------------------
  * dustin_sparse_verify_attn -- verification attention over the selected tokens only

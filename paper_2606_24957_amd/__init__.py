@@ -65,7 +65,8 @@ class DustinScoreCall(ctypes.Structure):
                 ("bt", ctypes.c_void_p), ("scale", ctypes.c_float), ("groups", ctypes.c_int32),
                 ("init", ctypes.c_void_p), ("init_sb", ctypes.c_int64), ("init_sg", ctypes.c_int64),
                 ("out", ctypes.c_void_p), ("out_sb", ctypes.c_int64), ("out_sg", ctypes.c_int64),
-                ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_size_t)]
+                ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_size_t),
+                ("digit_hist", ctypes.c_void_p)]
 
 
 _lib = None
@@ -94,7 +95,7 @@ def lib():
         L.dustin_topk_workspace.argtypes = [_i32, _i32, _i32]
         L.dustin_topk.restype = ctypes.c_int
         L.dustin_topk.argtypes = [_vp, _i64, _i64, _vp, _i64, _i64, P_BT, _i32, _i32, _i32,
-                                  _vp, _i64, _i64, _vp, _vp, _sz, _vp]
+                                  _vp, _i64, _i64, _vp, _vp, _vp, _vp, _sz, _vp]
         L.dustin_attn_workspace.restype = _sz
         L.dustin_attn_workspace.argtypes = [_i32, _i32, _i32, _i32, _i32, _i32]
         L.dustin_sparse_verify_attn.restype = ctypes.c_int
@@ -394,16 +395,39 @@ def score_layers(qs, ks, seq_lens, heads, **kw):
     return plan_score_layers(qs, ks, seq_lens, heads, **kw)()
 
 
-def plan_score_calls(calls: Sequence[Call], stream=None) -> Call:
+DIGIT_BINS = 4096
+
+
+def digit_hist(rows: int, device) -> torch.Tensor:
+    """A zeroed first-digit histogram for `rows` score rows (uint32 held as int32
+    [rows, 4096]): what dustin_score_calls fills with digit_hist and dustin_topk consumes
+    (and returns to zero)."""
+    return torch.zeros((rows, DIGIT_BINS), dtype=torch.int32, device=device)
+
+
+def plan_score_calls(calls: Sequence[Call], stream=None, digit_hists=None) -> Call:
     """Prepared dustin_score_calls: one or two planned score calls (plan_score or
     plan_score_layers, each with its own workspace tag) in one launch where the library can
     (the target's and the draft's scores of a step), else one after the other.  Returns the
-    outputs of the calls."""
+    outputs of the calls.  digit_hists: per call None or a zeroed digit_hist of the call's
+    output rows, into which the call counts its outputs by top key digit."""
     if not 1 <= len(calls) <= 2 or any(getattr(c, "desc", None) is None for c in calls):
         raise ValueError("one or two calls planned by plan_score or plan_score_layers")
-    arr = (DustinScoreCall * len(calls))(*[c.desc for c in calls])
+    hists = list(digit_hists) if digit_hists is not None else [None] * len(calls)
+    if len(hists) != len(calls):
+        raise ValueError("one histogram (or None) per call")
+    for h in hists:
+        if h is not None and (h.dtype != torch.int32 or not h.is_contiguous() or h.shape[-1] != DIGIT_BINS):
+            raise ValueError("a histogram is a contiguous int32 [rows, 4096] tensor")
+    _on_gpu(*[h for h in hists if h is not None])
+    descs = []
+    for c, h in zip(calls, hists):
+        d = DustinScoreCall.from_buffer_copy(c.desc)
+        d.digit_hist = None if h is None else h.data_ptr()
+        descs.append(d)
+    arr = (DustinScoreCall * len(calls))(*descs)
     args = (len(calls), arr, _stream(stream))
-    return Call(lib().dustin_score_calls, args, "dustin_score_calls", (tuple(calls), arr),
+    return Call(lib().dustin_score_calls, args, "dustin_score_calls", (tuple(calls), arr, tuple(hists)),
                 tuple(c.result for c in calls))
 
 
@@ -588,10 +612,16 @@ def arr(s, idx, count, seq_lens, heads_per_group, **kw):
 def plan_topk(s_draft: Optional[torch.Tensor], s_target: Optional[torch.Tensor], seq_lens,
          k_max: int, *, budget=None, m=None, m_scalar: Optional[int] = None, n_sink: int = 4,
          n_window: int = 16, groups: int = 1, idx: Optional[torch.Tensor] = None,
-         count: Optional[torch.Tensor] = None, stream=None) -> Call:
+         count: Optional[torch.Tensor] = None, hist_d: Optional[torch.Tensor] = None,
+         hist_t: Optional[torch.Tensor] = None, stream=None) -> Call:
     """Prepared dustin_topk, Eq. 6.  s_draft / s_target fp32 [B, G' (1 = broadcast), N]; returns (idx int32
-    [B, groups, k_max] ascending, only [:count] written; count int32 [B, groups])."""
-    _on_gpu(s_draft, s_target, idx, count)
+    [B, groups, k_max] ascending, only [:count] written; count int32 [B, groups]).  hist_d / hist_t: the
+    rows' first-digit histograms (digit_hist [B, 4096], groups = 1) written with the scores; taken in place
+    of a first pass and left at zero."""
+    _on_gpu(s_draft, s_target, idx, count, hist_d, hist_t)
+    for h in (hist_d, hist_t):
+        if h is not None and (h.dtype != torch.int32 or not h.is_contiguous() or h.shape[-1] != DIGIT_BINS):
+            raise ValueError("a histogram is a contiguous int32 [B, 4096] tensor")
     ref = s_target if s_target is not None else s_draft
     B, _, max_len = ref.shape
     dev = ref.device
@@ -618,8 +648,8 @@ def plan_topk(s_draft: Optional[torch.Tensor], s_target: Optional[torch.Tensor],
     ws = workspace(nbytes, dev, "topk", stream)
     args = (_ptr(s_draft), dsb, dsg, _ptr(s_target), tsb, tsg, ctypes.byref(bt), int(groups),
             int(n_sink), int(n_window), _ptr(idx), idx.stride(0), idx.stride(1), _ptr(count),
-            _ptr(ws), nbytes, _stream(stream))
-    return Call(lib().dustin_topk, args, "dustin_topk", (s_draft, s_target, bt, ws), (idx, count))
+            _ptr(hist_d), _ptr(hist_t), _ptr(ws), nbytes, _stream(stream))
+    return Call(lib().dustin_topk, args, "dustin_topk", (s_draft, s_target, bt, ws, hist_d, hist_t), (idx, count))
 
 
 def topk(s_draft, s_target, seq_lens, k_max, **kw):

@@ -629,7 +629,11 @@ dustin_status dustin_score_calls(int32_t n_calls, const dustin_score_call* calls
                       c.n_heads, c.k_layers_host, c.bt, c.scale, c.groups, c.init, c.init_sb, c.init_sg, c.out,
                       c.out_sb, c.out_sg, c.workspace, c.workspace_bytes);
     if (st != DUSTIN_OK) return st;
+    if (c.digit_hist && !aligned(c.digit_hist, 16)) return DUSTIN_ERR_INVALID_ARG;
+    P[i].a.hist = c.digit_hist;
+    P[i].sc.hist = c.digit_hist;
   }
+  if (n_calls == 2 && calls[0].digit_hist && calls[0].digit_hist == calls[1].digit_hist) return DUSTIN_ERR_INVALID_ARG;
   if (n_calls == 2 && calls[0].workspace == calls[1].workspace) return DUSTIN_ERR_WORKSPACE;
   if (n_calls == 2 && P[0].sync && P[1].sync && !P[0].empty && !P[1].empty &&
       score_sync_pair_supported(P[0].sc, P[1].sc)) {
@@ -829,9 +833,13 @@ dustin_status dustin_topk(const float* s_draft, int64_t d_sb, int64_t d_sg,
                           const float* s_target, int64_t t_sb, int64_t t_sg,
                           const dustin_batch* bt, int32_t groups, int32_t n_sink,
                           int32_t n_window, int32_t* idx, int64_t idx_sb, int64_t idx_sg,
-                          int32_t* count, void* workspace, size_t workspace_bytes,
-                          void* stream) {
+                          int32_t* count, uint32_t* hist_draft, uint32_t* hist_target, void* workspace,
+                          size_t workspace_bytes, void* stream) {
   if (!batch_ok(bt) || !idx || !count) return DUSTIN_ERR_INVALID_ARG;
+  if ((hist_draft && (!s_draft || !aligned(hist_draft, 16))) || (hist_target && (!s_target || !aligned(hist_target, 16))))
+    return DUSTIN_ERR_INVALID_ARG;
+  if ((hist_draft || hist_target) && groups != 1) return DUSTIN_ERR_INVALID_ARG;
+  if (hist_draft && hist_draft == hist_target) return DUSTIN_ERR_INVALID_ARG;
   if (!s_draft && !s_target) return DUSTIN_ERR_INVALID_ARG;
   if (groups < 1 || groups > 65535 || n_sink < 0 || n_window < 0) return DUSTIN_ERR_INVALID_ARG;
   if (bt->max_len > kTopkMaxLen) return DUSTIN_ERR_UNSUPPORTED;
@@ -873,6 +881,8 @@ dustin_status dustin_topk(const float* s_draft, int64_t d_sb, int64_t d_sg,
   a.idx_sb = idx_sb;
   a.idx_sg = idx_sg;
   a.count = count;
+  a.hist_d = hist_draft;
+  a.hist_t = hist_target;
   const hipError_t e = launch_topk(a, B, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? DUSTIN_OK : DUSTIN_ERR_LAUNCH;
 }

@@ -15,6 +15,16 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 constexpr int kWave = 64;
 constexpr float kLog2e = 1.4426950408889634f;
 
+// The order-preserving uint32 of an fp32 value (larger value, larger key; -0 and +0 alike;
+// NaNs beyond +-inf by their sign bit): the ranking key of the top-k.  Its top 12 bits are
+// the first digit of the top-k's radix selection (kDigitBins bins).
+constexpr int kDigitBins = 4096;
+__device__ __forceinline__ uint32_t order_key(float x) {
+  uint32_t u = __float_as_uint(x);
+  if (u == 0x80000000u) u = 0u;
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
 // D = A * B + C on one 16x16x32 bf16 MFMA tile.  Lane l holds A[l % 16][8 (l / 16) + e],
 // B[8 (l / 16) + e][l % 16] (e = 0..7) and D[4 (l / 16) + e][l % 16] (e = 0..3).
 __device__ __forceinline__ f32x4 mfma16x16x32(const bf16x8& a, const bf16x8& b, const f32x4& c) {

@@ -97,6 +97,9 @@ struct ScoreArgs {
   float* stats;   // [n_layers, B, n_heads, nq_max, n_chunks, 2]  (max, sum of exp2) per chunk
   int64_t ld;
   int32_t nq_max, n_chunks;
+  // optional: one count per written position added to hist[(b groups + go) kDigitBins +
+  // order_key(out) >> 20] (summed outputs only)
+  uint32_t* hist;
 };
 static_assert(sizeof(ScoreArgs) <= 4096, "kernel arguments stay within 4 KiB");
 
@@ -125,6 +128,7 @@ struct SyncCall {
   int32_t kv[4];
   int32_t col_head[16];
   uint8_t col_query[16], col_u[16];
+  uint32_t* hist;  // optional: as ScoreArgs::hist (one output row per sequence)
 };
 
 struct SyncArgs {
@@ -182,6 +186,10 @@ struct TopkArgs {
   uint32_t* counters;  // [B * groups]
   uint32_t* bitmaps;   // [B * groups][2][words]
   int32_t words;
+  // optional (groups = 1): per sequence the top-digit histogram of the whole row of S_D /
+  // S_T, which replaces the tier's first pass and is returned to zero
+  uint32_t* hist_d;
+  uint32_t* hist_t;
 };
 
 hipError_t launch_topk(const TopkArgs& a, int B, hipStream_t stream);

@@ -282,9 +282,10 @@ __global__ __launch_bounds__(kFinishThreads) void score_finish_kernel(ScoreArgs 
   // four consecutive positions per thread (the logits rows are 64-element aligned, so
   // the vector load stays inside a row even past N)
   const int n0 = p_begin + 4 * tid;
-  if (n0 >= N) return;
+  if (!a.hist && n0 >= N) return;  // (with a histogram every thread reaches its barriers)
+  const bool live = n0 < N;
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-  for (int i0 = 0; i0 < np; i0 += kFinishBatch) {
+  for (int i0 = 0; live && i0 < np; i0 += kFinishBatch) {
     f32x4 x[kFinishBatch];
 #pragma unroll
     for (int u = 0; u < kFinishBatch; ++u) {
@@ -302,13 +303,37 @@ __global__ __launch_bounds__(kFinishThreads) void score_finish_kernel(ScoreArgs 
   }
   const float* init_row = a.init ? a.init + (int64_t)b * a.init_sb + (int64_t)go * a.init_sg : nullptr;
   float* out_row = a.out + (int64_t)b * a.out_sb + (int64_t)go * a.out_sg + (int64_t)lo * a.out_sl;
-  if (n0 + 3 < N && aligned16(out_row + n0) && (!init_row || aligned16(init_row + n0))) {
-    const f32x4 in = init_row ? *reinterpret_cast<const f32x4*>(init_row + n0) : f32x4{0.f, 0.f, 0.f, 0.f};
-    *reinterpret_cast<f32x4*>(out_row + n0) = in + acc;
-  } else {
+  f32x4 val = {0.f, 0.f, 0.f, 0.f};
+  if (live) {
+    if (n0 + 3 < N && aligned16(out_row + n0) && (!init_row || aligned16(init_row + n0))) {
+      const f32x4 in = init_row ? *reinterpret_cast<const f32x4*>(init_row + n0) : f32x4{0.f, 0.f, 0.f, 0.f};
+      val = in + acc;
+      *reinterpret_cast<f32x4*>(out_row + n0) = val;
+    } else {
 #pragma unroll
-    for (int e = 0; e < 4; ++e)
-      if (n0 + e < N) out_row[n0 + e] = (init_row ? init_row[n0 + e] : 0.f) + acc[e];
+      for (int e = 0; e < 4; ++e) {
+        val[e] = (init_row && n0 + e < N ? init_row[n0 + e] : 0.f) + acc[e];
+        if (n0 + e < N) out_row[n0 + e] = val[e];
+      }
+    }
+  }
+  // the chunk's outputs counted by top key digit, then the non-zero bins added into the
+  // output row's histogram (summed outputs only: the host passes none with per-layer ones)
+  if (a.hist) {
+    __shared__ uint32_t h[kDigitBins];
+    for (int i = tid; i < kDigitBins; i += kFinishThreads) h[i] = 0u;
+    __syncthreads();
+    if (live) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (n0 + e < N) atomicAdd(&h[order_key(val[e]) >> 20], 1u);
+    }
+    __syncthreads();
+    uint32_t* const gh = a.hist + ((int64_t)b * a.groups + go) * kDigitBins;
+    for (int i = tid; i < kDigitBins; i += kFinishThreads) {
+      const uint32_t v = h[i];
+      if (v) __hip_atomic_fetch_add(gh + i, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
   }
 }
 

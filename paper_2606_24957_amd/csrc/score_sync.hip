@@ -65,6 +65,7 @@ struct SyncLds {
   int page[kSyncWaves * kSyncMaxTW * 16];
   float2 st[kSyncWaves][16];
   float2 mz[16];
+  uint32_t hist[kDigitBins];  // the chunk's outputs by top key digit (with a histogram)
 };
 
 // One call's share of the grid: block blk of the call's blocks.
@@ -97,6 +98,8 @@ __device__ __forceinline__ void score_sync_call(const SyncCall& a, int blk, Sync
   if (c >= G) return;
   const int nq = dims.nq(b);
   const int L = a.n_layers;
+  if (a.hist)  // cleared now; the layers' barriers order this before the counting at the end
+    for (int i = threadIdx.x; i < kDigitBins; i += kSyncThreads) lds.hist[i] = 0u;
 
   // column lr: (scoring head slot, query) on used KV head cu; columns past the pairs, and
   // queries past nq_b, count for nothing
@@ -319,19 +322,39 @@ __device__ __forceinline__ void score_sync_call(const SyncCall& a, int blk, Sync
   }
 
   // out = init + the sums, for positions below N_b
+  const int n0 = c * C + 4 * threadIdx.x;
+  f32x4 val = {0.f, 0.f, 0.f, 0.f};
   if ((int)threadIdx.x < C / 4) {
-    const int n0 = c * C + 4 * threadIdx.x;
     const float* init_row = a.init ? a.init + (int64_t)b * a.init_sb : nullptr;
     float* out_row = a.out + (int64_t)b * a.out_sb;
     const bool vec = n0 + 3 < N && ((uintptr_t)(out_row + n0) & 15) == 0 &&
                      (!init_row || ((uintptr_t)(init_row + n0) & 15) == 0);
     if (vec) {
       const f32x4 in = init_row ? *reinterpret_cast<const f32x4*>(init_row + n0) : f32x4{0.f, 0.f, 0.f, 0.f};
-      *reinterpret_cast<f32x4*>(out_row + n0) = in + acc_pos;
+      val = in + acc_pos;
+      *reinterpret_cast<f32x4*>(out_row + n0) = val;
     } else {
 #pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        val[e] = (init_row && n0 + e < N ? init_row[n0 + e] : 0.f) + acc_pos[e];
+        if (n0 + e < N) out_row[n0 + e] = val[e];
+      }
+    }
+  }
+  // the chunk's outputs counted by top key digit, then the non-zero bins added into the
+  // sequence's histogram
+  if (a.hist) {
+    uint32_t* const h = lds.hist;
+    if ((int)threadIdx.x < C / 4) {
+#pragma unroll
       for (int e = 0; e < 4; ++e)
-        if (n0 + e < N) out_row[n0 + e] = (init_row ? init_row[n0 + e] : 0.f) + acc_pos[e];
+        if (n0 + e < N) atomicAdd(&h[order_key(val[e]) >> 20], 1u);
+    }
+    __syncthreads();
+    uint32_t* const gh = a.hist + (int64_t)b * kDigitBins;
+    for (int i = threadIdx.x; i < kDigitBins; i += kSyncThreads) {
+      const uint32_t v = h[i];
+      if (v) __hip_atomic_fetch_add(gh + i, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
 }

@@ -30,18 +30,12 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kTopkThreads = 1024;
 constexpr int kTopkWaves = kTopkThreads / kWave;
-constexpr int kBins1 = 4096;                            // first digit: key bits 31..20
+constexpr int kBins1 = kDigitBins;                      // first digit: key bits 31..20
 constexpr int kBins = 1024;                             // later digits: 19..10, 9..0
 constexpr int kTopkLds = 160 * 1024;                    // LDS of one gfx950 workgroup
 constexpr int kLoadBatch = 16;                          // global loads in flight per thread
 constexpr int kScanBatch = 8;                           // LDS key reads in flight per lane
 constexpr int kSegQuantum = kTopkThreads * kLoadBatch;  // segments are multiples of this
-
-__device__ __forceinline__ uint32_t order_key(float x) {
-  uint32_t u = __float_as_uint(x);
-  if (u == 0x80000000u) u = 0u;
-  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-}
 
 __device__ __forceinline__ uint64_t lanemask_lt(int lane) { return (1ull << lane) - 1ull; }
 
@@ -289,8 +283,12 @@ constexpr int kMaxRankedTies = 1024;
 constexpr int kFastBatch = 8;  // 64-position groups of a wave loaded together
 
 __device__ __forceinline__ void select_tier_fast(TopkSmem& s, KeyStage& ks, uint32_t need, uint32_t* bm, uint32_t* cand,
-                                 int cap) {
-  if (need == 0) return;
+                                 int cap, uint32_t* hist = nullptr, int n_sink = 0, int n_window = 0) {
+  if (need == 0) {
+    if (hist)
+      for (int i = threadIdx.x; i < kBins1; i += kTopkThreads) hist[i] = 0u;
+    return;
+  }
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
   const int N = ks.N;
   const int ngroups = (N + kWave - 1) / kWave;  // 64-position groups
@@ -335,15 +333,28 @@ __device__ __forceinline__ void select_tier_fast(TopkSmem& s, KeyStage& ks, uint
   };
   if (resident) load_batch(0);
 
-  // ---- A
-  for (int i = tid; i < kBins1; i += kTopkThreads) s.hist[i] = 0u;
-  __syncthreads();
-  for (int i0 = 0; i0 < gpw; i0 += kFastBatch) {
-    if (!resident) load_batch(i0);
-    bool fr[kFastBatch];
-    free_flags(i0, fr);
+  // ---- A (or the row's histogram counted when the scores were written, less the protected
+  // positions, which are taken when the tier starts: the same counts over the free keys;
+  // the histogram is then returned to zero for the next call)
+  if (hist) {
+    for (int i = tid; i < kBins1; i += kTopkThreads) s.hist[i] = hist[i];
+    __syncthreads();
+    const int s0 = min(n_sink, N), w0 = max(s0, N - n_window), np = s0 + (N - w0);
+    for (int i = tid; i < np; i += kTopkThreads) {
+      const int n = i < s0 ? i : w0 + (i - s0);
+      atomicSub(&s.hist[order_key(ks.row[n]) >> 20], 1u);
+    }
+    for (int i = tid; i < kBins1; i += kTopkThreads) hist[i] = 0u;
+  } else {
+    for (int i = tid; i < kBins1; i += kTopkThreads) s.hist[i] = 0u;
+    __syncthreads();
+    for (int i0 = 0; i0 < gpw; i0 += kFastBatch) {
+      if (!resident) load_batch(i0);
+      bool fr[kFastBatch];
+      free_flags(i0, fr);
 #pragma unroll
-    for (int u = 0; u < kFastBatch; ++u) hist_add(s.hist, kb[u] >> 20, fr[u]);
+      for (int u = 0; u < kFastBatch; ++u) hist_add(s.hist, kb[u] >> 20, fr[u]);
+    }
   }
   __syncthreads();
   find_digit<kBins1>(s, need);
@@ -575,10 +586,20 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(TopkArgs a, int seg)
   if (!a.s_draft) m = 0;
   if (!a.s_target) m = k - P;
   int32_t* out = a.idx + (int64_t)b * a.idx_sb + (int64_t)go * a.idx_sg;
+  // the rows' histograms, when given (one selection group): each is read by the tier that
+  // uses it first, or else cleared here, so that every call leaves them at zero
+  uint32_t* const hd = a.hist_d ? a.hist_d + (int64_t)b * kBins1 : nullptr;
+  uint32_t* const ht = a.hist_t ? a.hist_t + (int64_t)b * kBins1 : nullptr;
+  auto clear = [&](uint32_t* h) {
+    if (h)
+      for (int i = tid; i < kBins1; i += kTopkThreads) h[i] = 0u;
+  };
   if (N <= k) {
     if (tier == 0) {
       for (int n = tid; n < N; n += kTopkThreads) out[n] = n;
       if (tid == 0) a.count[b * a.groups + go] = N;
+      clear(hd);
+      clear(ht);
     }
     return;
   }
@@ -588,6 +609,12 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(TopkArgs a, int seg)
   if (tier == 1 && !both) return;
   const bool run_d = both ? tier == 0 : has_d;
   const bool run_t = both ? tier == 1 : has_t;
+  // a histogram serves a tier that is its workgroup's first job (the target tier after the
+  // draft tier in one workgroup has I_D taken as well, which the histogram does not know)
+  if (tier == 0) {
+    if (!run_d) clear(hd);
+    if (!both && !(run_t && !run_d)) clear(ht);
+  }
 
   uint32_t* bm = dyn + seg;
   // protected positions (and the padding past N) start out taken
@@ -624,7 +651,8 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(TopkArgs a, int seg)
   for (int j = 0; j < jobs; ++j) {
     ks.row = j == 0 ? rows[0] : rows[1];
     ks.loaded = -1;
-    select_tier_fast(s, ks, j == 0 ? needs[0] : needs[1], bm, dyn, cap);
+    select_tier_fast(s, ks, j == 0 ? needs[0] : needs[1], bm, dyn, cap, j == 0 ? (run_d ? hd : ht) : nullptr,
+                     a.n_sink, a.n_window);
   }
 
   if (both) {

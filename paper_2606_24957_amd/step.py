@@ -9,8 +9,8 @@ from typing import List, Optional
 
 import torch
 
-from . import (plan_kv_append, plan_kv_commit, plan_score, plan_score_calls, plan_score_layers, plan_score_per_layer,
-               plan_sparse_verify_attn, plan_topk)
+from . import (digit_hist, plan_kv_append, plan_kv_commit, plan_score, plan_score_calls, plan_score_layers,
+               plan_score_per_layer, plan_sparse_verify_attn, plan_topk)
 
 
 def window_kv(s, layer) -> tuple:
@@ -43,6 +43,10 @@ class VerifyStep:
         self.cnt = torch.zeros((s.B, s.groups), dtype=torch.int32, device=device)
         self.outs = [torch.empty_like(l.q) for l in layers]
         self.windows = windows if windows is not None else [window_kv(s, l) for l in layers]
+        # with one selection group, the score calls count their outputs by top key digit and
+        # the top-k takes those counts in place of its first pass over each row
+        self.hist_t = digit_hist(s.B, device) if s.groups == 1 else None
+        self.hist_d = digit_hist(s.B, device) if s.groups == 1 and est.s_draft_given is None else None
         self.graph = None
         self.ops = self._plan()
 
@@ -57,15 +61,16 @@ class VerifyStep:
                             stream=stream)
         if est.s_draft_given is not None:
             given = est.s_draft_given
-            ops = [target, lambda: self.s_d.copy_(given)]
+            ops = [plan_score_calls([target], stream=stream, digit_hists=[self.hist_t]),
+                   lambda: self.s_d.copy_(given)]
         else:
             # the target's and the draft's scores in one call (one launch where the library can)
             draft = plan_score_layers(est.draft_q, est.draft_k, self.seq, s.draft.heads, n_query=self.gam,
                                       out=self.s_d, max_len=N, stream=stream, ws_tag="score_draft")
-            ops = [plan_score_calls([target, draft], stream=stream)]
+            ops = [plan_score_calls([target, draft], stream=stream, digit_hists=[self.hist_t, self.hist_d])]
         ops.append(plan_topk(self.s_d, self.s_t, self.seq, s.k_max, budget=self.bud, m=self.mm,
                              n_sink=s.n_sink, n_window=s.n_window, groups=s.groups, idx=self.idx,
-                             count=self.cnt, stream=stream))
+                             count=self.cnt, hist_d=self.hist_d, hist_t=self.hist_t, stream=stream))
         for L, o, (k_new, v_new) in zip(self.layers, self.outs, self.windows):
             if self.append:
                 ops.append(plan_kv_append(k_new, v_new, L.k, L.v, self.seq, n_query=self.nq,

@@ -69,7 +69,8 @@ static dustin_kv kv(int Hkv = 2, int d = 128, int cap = 200) {
 static int topk(const dustin_batch& bt, const void* sd = FAKE, const void* st = FAKE, int groups = 1,
                 void* idx = FAKE, void* ws = FAKE, size_t ws_bytes = (size_t)1 << 30) {
   return dustin_topk(static_cast<const float*>(sd), 0, 0, static_cast<const float*>(st), 0, 0, &bt, groups, 4, 16,
-                     static_cast<int32_t*>(idx), 0, 0, static_cast<int32_t*>(FAKE), ws, ws_bytes, nullptr);
+                     static_cast<int32_t*>(idx), 0, 0, static_cast<int32_t*>(FAKE), nullptr, nullptr, ws, ws_bytes,
+                     nullptr);
 }
 
 static int attn(int Hq = 8, dustin_kv k = kv(), dustin_kv v = kv(), dustin_batch bt = batch(), const void* q = FAKE,

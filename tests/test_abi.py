@@ -81,9 +81,10 @@ def _kv(Hkv=2, d=128, cap=200):
     return kv
 
 
-def _topk(L, bt, sd=FAKE, st=FAKE, groups=1, ns=4, nw=16, idx=FAKE, cnt=FAKE, ws=FAKE, ws_bytes=1 << 30):
+def _topk(L, bt, sd=FAKE, st=FAKE, groups=1, ns=4, nw=16, idx=FAKE, cnt=FAKE, ws=FAKE, ws_bytes=1 << 30,
+          hd=None, ht=None):
     return L.dustin_topk(sd, 0, 0, st, 0, 0, ctypes.byref(bt), groups, ns, nw, idx, 0, 0, cnt,
-                         ws, ws_bytes, None)
+                         hd, ht, ws, ws_bytes, None)
 
 
 def test_topk_rejects(L):
@@ -103,8 +104,14 @@ def test_topk_rejects(L):
     bt = _batch()
     bt.seq_lens = None
     assert _topk(L, bt) == D.ERR_INVALID_ARG
-    assert L.dustin_topk(FAKE, 0, 0, FAKE, 0, 0, None, 1, 4, 16, FAKE, 0, 0, FAKE, None, 0,
+    assert L.dustin_topk(FAKE, 0, 0, FAKE, 0, 0, None, 1, 4, 16, FAKE, 0, 0, FAKE, None, None, None, 0,
                          None) == D.ERR_INVALID_ARG
+    # the first-digit histograms: each with its score array, 16-byte aligned, distinct, one group
+    assert _topk(L, _batch(m=0), sd=None, hd=FAKE) == D.ERR_INVALID_ARG
+    assert _topk(L, _batch(m=20), st=None, ht=FAKE) == D.ERR_INVALID_ARG
+    assert _topk(L, _batch(), hd=FAKE + 4) == D.ERR_INVALID_ARG
+    assert _topk(L, _batch(), hd=FAKE, ht=FAKE) == D.ERR_INVALID_ARG
+    assert _topk(L, _batch(), groups=2, ht=FAKE) == D.ERR_INVALID_ARG
 
 
 def _attn(L, q=FAKE, kv=None, vv=None, bt=None, Hq=8, idx=FAKE, cnt=FAKE, groups=1, out=FAKE,
