@@ -718,6 +718,11 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
     const bool edge = win || v0 + kStep - 1 >= wstart;  // wave-uniform: masking only near the window
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt) {
+      // a pair with fewer query rows than the launch's widest skips its absent row tiles
+      // (their maxima stay -inf and their sums zero, which the merges below ignore); not in
+      // the dense contiguous kernels, where at five row tiles the branches cost a spill
+      if constexpr (kStage)
+        if (rt > 0 && rt * 16 >= rows) break;
       // (1) S^T tile: lane holds tokens v0 + 16 i + 4 lg + e for query row rt*16 + lr
       f32x4 sc[2];
 #pragma unroll
