@@ -99,6 +99,7 @@ __device__ __forceinline__ void lds_barrier() {
 
 // s_waitcnt with only one counter constrained (gfx9 encoding; the others at their maxima)
 __device__ __forceinline__ void wait_vmem_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }  // vmcnt(0)
+__device__ __forceinline__ void wait_vmem_8() { __builtin_amdgcn_s_waitcnt(0x0F78); }    // vmcnt(8)
 __device__ __forceinline__ void wait_lds_all() { __builtin_amdgcn_s_waitcnt(0xC07F); }   // lgkmcnt(0)
 
 // Inclusive prefix sum over the 64 lanes of a wave: a Hillis-Steele scan inside each row of
@@ -143,15 +144,22 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
   constexpr int NDT = kD / 16;     // output 16-column tiles
   constexpr int kQPitch = kD + 8;  // LDS row pitch (bf16) of staged queries
   constexpr int kPitch = kD + 4;   // LDS row pitch (fp32) of the merged accumulator
-  constexpr int kTilesBytes = kW * 2 * kTile;                    // K and V tiles of every wave
-  // The table of staged rows is an LDS object of its own up to three row tiles (then the
-  // compiler can tell that writing it does not touch a tile whose rows are in flight);
-  // beyond that it shares the tile area's object to leave LDS for the wave accumulators.
-  constexpr bool kOwnStage = kStage && RT <= 3;
+  // Beyond four row tiles a wave over a contiguous cache waits for a step's K rows and its
+  // V rows separately (the token loop below); the V tiles then form an LDS object of their
+  // own, so that the compiler can tell the two tiles' direct-to-LDS loads apart.  (In the
+  // paged kernels the compiler still waits for every load before the score tile's query
+  // reads, which made the split form slower there.)
+  constexpr bool kSplitKV = RT > 4 && !kPaged;
+  constexpr int kTilesBytes = kW * (kSplitKV ? 1 : 2) * kTile;   // K (and V) tiles of every wave
+  // The table of staged rows is an LDS object of its own up to three row tiles and beyond
+  // four (then the compiler can tell that accessing it does not touch a tile whose rows are
+  // in flight); at four it shares the tile area's object to leave LDS for the wave
+  // accumulators.
+  constexpr bool kOwnStage = kStage && (RT <= 3 || kSplitKV);
   constexpr int kStageBytes = kStage && !kOwnStage ? kStageSteps * kStep * 4 : 0;
   constexpr int kLoopBytes = kTilesBytes + kStageBytes;
   constexpr int kBufFloats = RT * 16 * kPitch;                  // one wave's accumulator
-  constexpr int kNB = RT <= 4 ? kW : (RT <= 6 ? 2 : 1);          // wave accumulators LDS holds
+  constexpr int kNB = RT <= 4 ? kW : (RT <= (kSplitKV ? 5 : 6) ? 2 : 1);  // wave accumulators LDS holds
   constexpr int kFinalBytes = kNB * kBufFloats * 4;
   __shared__ __attribute__((aligned(1024))) char smem[kLoopBytes > kFinalBytes ? kLoopBytes : kFinalBytes];
   __shared__ __attribute__((aligned(16))) uint32_t sm_phys_own[kOwnStage ? kStageSteps * kStep : 4];
@@ -174,8 +182,9 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);  // wave-uniform
   const int lr = lane & 15, lg = lane >> 4;
-  char* const ktile = smem + wave * 2 * kTile;
-  char* const vtile = ktile + kTile;
+  __shared__ __attribute__((aligned(1024))) char sm_vtiles[kSplitKV ? kW * kTile : 16];
+  char* const ktile = smem + wave * (kSplitKV ? 1 : 2) * kTile;
+  char* const vtile = kSplitKV ? sm_vtiles + wave * kTile : ktile + kTile;
   // Every kernel argument the prologue reads is held in SGPRs from here on: the arguments
   // then arrive as one batch with one wait, instead of in dependent batches between the
   // first global loads.
@@ -363,6 +372,20 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
   // beyond that bound leaves every int32 position inside it)
   const int cap_m1 = (int)(a.k.capacity - 1 < INT32_MAX ? a.k.capacity - 1 : INT32_MAX - 1);
 
+  // The K half and the V half of a step's loads alone (kernels that wait for K and V
+  // separately; buffer form).
+  auto issue_v_to = [&](const uint32_t (&ph)[8], char* vt, auto buffered) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int j = 8 * lg + i;
+      if constexpr (decltype(buffered)::value) load_lds16(vrs, ph[i] * vstride + 16 * v_chunk(j, lr), vt + i * 1024);
+      else load_lds16(vbase, ph[i] * vstride + 16 * v_chunk(j, lr), vt + i * 1024);
+    }
+  };
+  auto issue_rows_to_k = [&](const uint32_t (&ph)[8], char* kt) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) load_lds16(krs, ph[i] * kstride + 16 * k_chunk(8 * lg + i, lr), kt + i * 1024);
+  };
   // Loads of one step into a K and a V tile: this lane moves chunk lr of tokens 8 lg + i
   // (i = 0..7) of the step, whose physical rows are ph[i]; one instruction per i for K and
   // one for V.  Buffer loads in the prologue (see load_lds16), global ones in the loop.
@@ -372,12 +395,14 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
       const int j = 8 * lg + i;
       if constexpr (decltype(buffered)::value) {
         load_lds16(krs, ph[i] * kstride + 16 * k_chunk(j, lr), kt + i * 1024);
-        load_lds16(vrs, ph[i] * vstride + 16 * v_chunk(j, lr), vt + i * 1024);
+        if constexpr (!kSplitKV) load_lds16(vrs, ph[i] * vstride + 16 * v_chunk(j, lr), vt + i * 1024);
       } else {
         load_lds16(kbase, ph[i] * kstride + 16 * k_chunk(j, lr), kt + i * 1024);
-        load_lds16(vbase, ph[i] * vstride + 16 * v_chunk(j, lr), vt + i * 1024);
+        if constexpr (!kSplitKV) load_lds16(vbase, ph[i] * vstride + 16 * v_chunk(j, lr), vt + i * 1024);
       }
     }
+    // split waits: the step's eight V loads follow its eight K loads
+    if constexpr (kSplitKV) issue_v_to(ph, vt, buffered);
   };
   using Buffered = std::true_type;
   using Global = std::false_type;
@@ -395,8 +420,11 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
   // the staged page translations first, and beyond three row tiles the table shares the
   // tile area's LDS object: both issue the first step after staging, as do dense kernels
   // beyond four row tiles, where the extra live registers would spill.)
-  constexpr bool kSpec = !kPaged && (kOwnStage || (!kStage && RT <= 4));
+  constexpr bool kSpec = !kPaged && (kStage ? RT <= 3 : RT <= 4);
   static_assert(!kSpec || !kSparse || RT <= kAttnSepMaxRT, "speculative sparse rows need the window step");
+  // the token loop's form: buffer loads where the first step is speculative, and where K and
+  // V are waited for separately (the wait insertion counts FLAT loads as out of order)
+  using LoopForm = std::integral_constant<bool, kSpec || kSplitKV>;
   auto issue_first = [&](auto exact_pos) {
     uint32_t ph[8];
 #pragma unroll
@@ -649,9 +677,9 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
 
   int chunk_v0 = 0;  // first virtual token staged in sm_phys
 
-  auto issue = [&](int st) {
+  // physical rows of this lane's tokens in step st
+  auto step_rows = [&](int st, uint32_t (&ph)[8]) {
     const int v0 = st * kStep + 8 * lg;
-    uint32_t ph[8];
     if constexpr (kStage) {
       const u32x4* src = reinterpret_cast<const u32x4*>(sm_phys + (v0 - chunk_v0));
       const u32x4 p0 = src[0], p1 = src[1];
@@ -664,7 +692,11 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
 #pragma unroll
       for (int i = 0; i < 8; ++i) ph[i] = v0 + i < total ? (uint32_t)(v0 + i) : 0u;
     }
-    issue_rows_to(ph, ktile, vtile, std::integral_constant<bool, kSpec>{});
+  };
+  auto issue = [&](int st) {
+    uint32_t ph[8];
+    step_rows(st, ph);
+    issue_rows_to(ph, ktile, vtile, LoopForm{});
   };
 
   // With up to four row tiles a wave reads all of a step's operands into registers and
@@ -714,15 +746,17 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
   // v0: the virtual token of the tile's first row; vt: its V tile; win: the window step
   // (causal mask per query row), else a body step (with a window step, tokens from wstart on
   // belong to the window step and are masked here).
+  // A pair with fewer query rows than the launch's widest skips its absent row tiles (their
+  // maxima stay -inf and their sums zero, which the merges below ignore).  Not up to three
+  // row tiles (the branches changed that code, and it measured 0.1-0.2 us per layer slower
+  // at the Qwen2.5-72B shape), nor in the dense contiguous kernels, where at five row tiles
+  // they cost a spill.
+  auto tile_absent = [&](int rt) { return kStage && RT > 3 && rt > 0 && rt * 16 >= rows; };
   auto compute = [&](int v0, const Operands& op, const char* vt, bool win) {
     const bool edge = win || v0 + kStep - 1 >= wstart;  // wave-uniform: masking only near the window
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt) {
-      // a pair with fewer query rows than the launch's widest skips its absent row tiles
-      // (their maxima stay -inf and their sums zero, which the merges below ignore); not in
-      // the dense contiguous kernels, where at five row tiles the branches cost a spill
-      if constexpr (kStage)
-        if (rt > 0 && rt * 16 >= rows) break;
+      if (tile_absent(rt)) break;
       // (1) S^T tile: lane holds tokens v0 + 16 i + 4 lg + e for query row rt*16 + lr
       f32x4 sc[2];
 #pragma unroll
@@ -768,6 +802,71 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
       for (int dt = 0; dt < NDT; ++dt) {
         if constexpr (kOverlap) acc[rt][dt] = mfma16x16x32(op.vt[dt], pT, acc[rt][dt]);
         else acc[rt][dt] = mfma16x16x32(read_vt(vt, dt), pT, acc[rt][dt]);
+      }
+    }
+  };
+  // The same step in two halves (kernels that wait for K and V separately; body steps
+  // only, as these kernels have no window step): (1) and (2) of every row tile from the
+  // K rows, then (3) of every row tile from the V tile, each V^T operand read once.
+  // (1) and (2) of row tile rt, the same steps as in compute(): returns the tile's
+  // probabilities as the B operand of its value product, after adding their row sums.
+  auto tile_probs = [&](int rt, int v0, const Operands& op, bool win, bool edge) -> bf16x8 {
+    // (1) S^T tile: lane holds tokens v0 + 16 i + 4 lg + e for query row rt*16 + lr
+    f32x4 sc[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      f32x4 c = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) c = mfma16x16x32(op.k[i][ks], q_operand(rt, ks), c);
+      sc[i] = c;
+    }
+    // (2) masked row maxima, lazy rescale, probabilities
+    if (edge) {
+      const int lim = win ? limit[rt] : min(limit[rt], body_limit);
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (v0 + 16 * i + 4 * lg + e > lim) sc[i][e] = -INFINITY;
+    }
+    const float m = fmaxf(fmaxf(fmaxf(sc[0][0], sc[0][1]), fmaxf(sc[0][2], sc[0][3])),
+                          fmaxf(fmaxf(sc[1][0], sc[1][1]), fmaxf(sc[1][2], sc[1][3])));
+    const float mx = max_over_lane_groups(m) * a.scale_log2;
+    if (__any(mx > m_ref[rt] + kRescaleLog2)) {  // wave-uniform, rare after the first step
+      const float mn = fmaxf(m_ref[rt], mx);
+      const float alpha = m_ref[rt] == -INFINITY ? 0.f : fast_exp2(m_ref[rt] - mn);
+      m_ref[rt] = mn;
+      accl[rt] *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt) acc[rt][dt] *= alpha;
+    }
+    const float nmu = m_ref[rt] == -INFINITY ? 0.f : -m_ref[rt];
+    float p[2][4];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) p[i][e] = fast_exp2(fmaf(sc[i][e], a.scale_log2, nmu));
+    const bf16x8 pT = as_bf16x8(u32x4{cvt_pk_bf16(p[0][0], p[0][1]), cvt_pk_bf16(p[0][2], p[0][3]),
+                                      cvt_pk_bf16(p[1][0], p[1][1]), cvt_pk_bf16(p[1][2], p[1][3])});
+    accl[rt] = mfma16x16x32(ones, pT, accl[rt]);
+    return pT;
+  };
+  auto compute_scores = [&](int v0, const Operands& op, bf16x8 (&pT)[RT]) {
+    const bool edge = v0 + kStep - 1 >= wstart;
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) {
+      if (tile_absent(rt)) break;
+      pT[rt] = tile_probs(rt, v0, op, false, edge);
+    }
+  };
+  auto compute_values = [&](const char* vt, const bf16x8 (&pT)[RT]) {
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt) {
+      const bf16x8 v = read_vt(vt, dt);
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) {
+        if (tile_absent(rt)) break;
+        acc[rt][dt] = mfma16x16x32(v, pT[rt], acc[rt][dt]);
       }
     }
   };
@@ -826,7 +925,7 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
       uint32_t ph[8];
 #pragma unroll
       for (int i = 0; i < 8; ++i) ph[i] = phys_at(pos_of(first_v0 + i, first_sel[i]), 0);
-      issue_rows_to(ph, ktile, vtile, Global{});
+      issue_rows_to(ph, ktile, vtile, LoopForm{});
       first_issued = true;
     }
   }
@@ -867,6 +966,34 @@ __global__ __launch_bounds__(kW * kWave) void verify_attn_kernel(AttnArgs a) {
       compute(wstart, opw, sm_win + kTile, true);
     }
     while (true) {
+      if constexpr (kSplitKV) {
+        // Outstanding here: this step's K loads, then its V loads.  The K rows go to
+        // registers and the next step's K loads into the freed tile; the scores are computed
+        // while this step's V rows (and the next K rows) arrive; then the value products, and
+        // the next step's V loads into the freed V tile.
+        wait_vmem_8();  // this step's K rows are in the tile
+        Operands op;
+        read_tiles(op);
+        const int next = st + kW;
+        if (next < ce) {
+          uint32_t ph[8];
+          step_rows(next, ph);
+          wait_lds_all();  // the K tile has been read out
+          issue_rows_to_k(ph, ktile);
+        }
+        bf16x8 pT[RT];
+        compute_scores(st * kStep, op, pT);
+        if (next < ce) wait_vmem_8();  // this step's V rows are in the tile (the next K rows may not be)
+        else wait_vmem_all();
+        compute_values(vtile, pT);
+        if (next >= ce) break;
+        uint32_t ph[8];
+        step_rows(next, ph);
+        wait_lds_all();  // the V tile has been read out
+        issue_v_to(ph, vtile, Buffered{});
+        st = next;
+        continue;
+      }
       wait_vmem_all();  // this step's rows are in the tiles
       Operands op;
       read_tiles(op);
