@@ -46,7 +46,7 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-sample-seqs", type=int, default=16)
     p.add_argument("--no-secondary", action="store_true",
-                   help="skip the other workloads (ragged, 131k, k = 512) that the headline run also times")
+                   help="skip the other workloads (ragged, 131k, k = 512) that the default run also times")
     p.add_argument("--no-digit-hist", action="store_true",
                    help="the top-k makes its own first pass over each row instead of taking the score calls' "
                         "first-digit histograms")
@@ -524,7 +524,7 @@ SECONDARY = (("qwen72b", 512), ("ragged", None), ("long131k", None))
 
 
 def secondary(name, k, steps, warmup, dev):
-    """One more workload through the same timed step as the headline (estimation, then its L
+    """One more workload through the same timed step as the main workload (estimation, then its L
     sparse and L dense layers back to back): per-layer and per-step figures."""
     import torch
     from paper_2606_24957_amd import workloads as W
@@ -722,7 +722,7 @@ def main():
         del buf, probe
         log(f"[bench] 2 GiB streaming read: {read_gbps} GB/s")
 
-    # the other workloads through the same timed step, after the headline's buffers are gone
+    # the other workloads through the same timed step, after the main workload's buffers are gone
     others = None
     if args.only == "all" and not args.no_secondary and args.workload == "qwen72b" and args.k is None \
             and args.layers is None and args.groups == "1":

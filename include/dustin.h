@@ -411,7 +411,7 @@ dustin_status dustin_sparse_verify_attn(const void* q, int64_t q_sb, int64_t q_s
  * Scratch: the split partials and counters live in a fixed device array of the library,
  * DUSTIN_NOALLOC_SCRATCH_BYTES (48 MiB) per GPU, held until the process ends.  A call that
  * needs more than that (dustin_attn_workspace(..., sparse = 1) > the limit) returns
- * DUSTIN_ERR_SCRATCH_LIMIT with nothing enqueued; at the headline shape (B = 16, 8 KV
+ * DUSTIN_ERR_SCRATCH_LIMIT with nothing enqueued; at the Qwen2.5-72B shape (B = 16, 8 KV
  * heads, 40 rows per KV head) a call needs 6.6 MB.  The first call on a device looks the
  * array up and enqueues one small fill kernel on `stream` that zeroes its counter region:
  * make that first call outside graph capture.  Every call on one GPU shares that GPU's array, which keeps

@@ -228,7 +228,7 @@ def test_full_size_131k_layer():
 
 
 def test_full_size_per_kv_head_step():
-    """One index set per KV head at the headline shape (groups = 8, one target scoring head
+    """One index set per KV head at the Qwen2.5-72B shape (groups = 8, one target scoring head
     per KV head): the step's per-group target score against the oracle, its per-group sets
     bit-exact against the oracle's Eq. 6 on the same scores, and sampled attention rows with
     those sets against the oracle."""
