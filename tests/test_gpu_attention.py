@@ -165,6 +165,19 @@ def test_split_counts_agree_and_are_deterministic(splits, monkeypatch):
     assert torch.equal(dn.view(torch.int16), dn2.view(torch.int16))
 
 
+@pytest.mark.parametrize("t,paged", [(5, False), (7, True), (9, False), (9, True), (16, False)])
+def test_one_split_crosses_staging_chunks(t, paged, monkeypatch):
+    """With one split per pair, a pair of 2500 selected positions takes 79 steps, more than
+    one 64-step chunk of the staged row table, and the dense pass over 4000 positions takes
+    126: the token loop stages the next chunk's rows between chunks, in every kernel form
+    (three row tiles with the speculative first step, four, five with K and V waited for
+    separately over a contiguous cache and together over a paged one, eight)."""
+    monkeypatch.setenv("DUSTIN_ATTN_SPLITS", "1")
+    s = _shape(1, 4000, t, 64, 8, 2500, paged=paged, name=f"chunks_t{t}_{'paged' if paged else 'contig'}")
+    _run_sparse_case(s, G=1, seed=21)
+    _run_dense_case(s)
+
+
 @pytest.mark.parametrize("nq,paged,splits", [((5, 9, 2), True, None), ((3, 5, 4), False, None),
                                              ((3, 5, 4), False, 3), ((5, 9, 2), False, 7)])
 def test_ragged_lengths_share_balanced_splits(nq, paged, splits, monkeypatch):
